@@ -1,0 +1,252 @@
+/*
+ * moe_apk.h -- C ABI of the MI355X (gfx950) routed-expert MoE hot path.
+ *
+ * One GPU's share of a routed-expert MoE layer whose prefill and decode tokens
+ * share the same local experts (ExpertPlex: Overview; Adaptive Persistent
+ * Kernel; Evaluation "Implementation"):
+ *
+ *   moe_topk_route              top-k softmax gating                (step a1)
+ *   moe_permute                 per-expert contiguous layout        (step a2)
+ *   moe_grouped_ffn_persistent  SwiGLU expert FFN as one persistent
+ *                               kernel with a device tile scheduler (steps a3-a6)
+ *   moe_combine                 weighted combine to token order     (step a7)
+ *
+ * Conventions (all calls):
+ *  - Pointers are DEVICE pointers unless marked "host".  The caller owns every
+ *    buffer; no call allocates device memory.  Scratch space is a
+ *    caller-allocated workspace whose size is returned by a *_workspace_bytes
+ *    query.
+ *  - Calls are asynchronous on `stream` (a hipStream_t; NULL = the default
+ *    stream) and never synchronise.
+ *  - Argument errors are detected on the host before anything is launched and
+ *    returned as a negative moe_status_t; moe_last_error() then holds a
+ *    message (thread-local).
+ *  - Data-dependent errors (an expert id out of range, a capacity overflow, a
+ *    bounded wait that timed out, an abort) are written by the kernels to the
+ *    caller's device status word (first error wins); kernels never write out
+ *    of bounds because of them.  The caller reads the word when it next
+ *    synchronises.
+ *  - No C++ exception crosses this interface.
+ *  - Supported device: gfx950 only (MOE_ERR_UNSUPPORTED elsewhere).
+ */
+#ifndef MOE_APK_H
+#define MOE_APK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t moe_status_t;
+#define MOE_OK               0
+#define MOE_ERR_INVALID_ARG (-1) /* null pointer, bad size, inconsistent descriptor            */
+#define MOE_ERR_UNSUPPORTED (-2) /* dtype / shape / device not supported by the kernels        */
+#define MOE_ERR_CAPACITY    (-3) /* buffer capacity below the maximum routed volume            */
+#define MOE_ERR_HIP         (-4) /* a HIP runtime call or kernel launch failed                 */
+#define MOE_ERR_ABORTED     (-5) /* device: the abort word was set                             */
+#define MOE_ERR_TIMEOUT     (-6) /* device: a bounded wait exceeded its spin limit             */
+#define MOE_ERR_BAD_EXPERT  (-7) /* device: an expert id outside [-1, E_local)                 */
+
+typedef int32_t moe_dtype_t;
+#define MOE_F32      0
+#define MOE_BF16     1
+#define MOE_FP8_E4M3 2   /* OCP E4M3FN, max 448, no infinities */
+
+typedef int32_t moe_phase_t;
+#define MOE_PREFILL 0
+#define MOE_DECODE  1
+
+#define MOE_MAX_OPS 16   /* operations per persistent launch */
+
+/* ------------------------------------------------------------------------- a1
+ * Top-k gating (Background, "MoE LLM Inference": the router selects a top-k
+ * subset of routed experts per token).  Reading taken for the unspecified
+ * gating function: softmax over the k largest fp32 logits (equal to softmax
+ * over all experts, select, renormalise), slots in descending-logit order,
+ * equal logits (including -0.0 and +0.0) to the lower expert index.
+ *
+ *  logits    [T, E_global] f32, row-major; must be finite (NaN/inf give
+ *            unspecified ids and weights, never out-of-bounds writes)
+ *  topk_ids  [T, top_k] i32 out: local id (global id - local_begin) when the
+ *            expert lies in [local_begin, local_begin + E_local), else -1
+ *  topk_w    [T, top_k] f32 out: renormalised weights over all k slots
+ *            (non-local slots keep their weight; the other expert-parallel
+ *            ranks hold the rest of the sum)
+ * Limits: 1 <= E_global <= 1024, 1 <= top_k <= min(E_global, 32), T >= 0
+ * (T == 0 launches nothing), 0 <= local_begin, E_local >= 1.
+ */
+moe_status_t moe_topk_route(const float* logits, int32_t T, int32_t E_global, int32_t top_k,
+                            int32_t local_begin, int32_t E_local,
+                            int32_t* topk_ids, float* topk_w, void* stream);
+
+/* ------------------------------------------------------------------------- a2
+ * Permutation into per-expert contiguous segments at final offsets
+ * (Background, "Prefill-Decode Disaggregation": the contiguous layout;
+ * "One-Sided Dispatch and Combine": routing fixes each expert's destination
+ * and final offset before activations are written, into buffers sized for
+ * the maximum routed volume).
+ *
+ * Assignment a = t*top_k + j.  Expert e's segment starts at offsets[e], a
+ * multiple of row_align; its rows are e's assignments in ascending a
+ * (deterministic, bit-exact); the segment is padded to a multiple of
+ * row_align with rows whose row_to_assign is -1 and whose x_perm row is zero.
+ *
+ *  topk_ids       [T, top_k] i32 (from moe_topk_route); ids outside
+ *                 [-1, E_local) set MOE_ERR_BAD_EXPERT and are treated as -1
+ *  x              [T, H] activations: bf16, or fp8 codes with
+ *  x_scales       [T, H/128] f32 per-row group scales (fp8 only, else NULL)
+ *  row_align      M_t of the FFN op that consumes the layout
+ *                 (moe_ffn_row_align()); 1 <= row_align <= 1024
+ *  capacity       rows of row_to_assign / x_perm; must be at least
+ *                 T*min(top_k, E_local) + E_local*(row_align-1)
+ *  counts         [E_local] i32 out     offsets [E_local+1] i32 out
+ *  row_to_assign  [capacity] i32 out (rows >= offsets[E_local] untouched)
+ *  assign_to_row  [T*top_k] i32 out (-1 for non-local slots)
+ *  x_perm         [capacity, H] out, same dtype as x (rows >= offsets[E_local]
+ *                 untouched);  x_perm_scales [capacity, H/128] f32 out (fp8)
+ *  workspace      moe_permute_workspace_bytes(T, top_k, E_local) bytes
+ *  error_flag     device i32 status word (data errors; not cleared here)
+ * Limits: 1 <= E_local <= 1024, H a multiple of 128.
+ */
+size_t moe_permute_workspace_bytes(int32_t T, int32_t top_k, int32_t E_local);
+moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t top_k, int32_t E_local,
+                         const void* x, moe_dtype_t x_dtype, const float* x_scales, int32_t H,
+                         int32_t row_align, int32_t capacity,
+                         int32_t* counts, int32_t* offsets, int32_t* row_to_assign,
+                         int32_t* assign_to_row, void* x_perm, float* x_perm_scales,
+                         void* workspace, int32_t* error_flag, void* stream);
+
+/* ------------------------------------------------------------------------- a3-a6
+ * Operation template (Adaptive Persistent Kernel, "Tile-Level Scheduling":
+ * buffers and descriptors of every MoE operation are built before the
+ * persistent kernel starts; at run time a ready signal instantiates the
+ * operation into the decode or prefill queue).
+ *
+ * The op computes, for every local expert e and each of its rows r,
+ *   h[r]      = silu(x_perm[r] . Wg_e^T) * (x_perm[r] . Wu_e^T)     (GEMM-1 + activation)
+ *   y_perm[r] = h[r] . Wd_e^T                                        (GEMM-2)
+ * with fp32 accumulation.  bf16 ops round h to bf16; fp8 ops quantize h per
+ * row per 128 columns (scale = max(amax, 1e-4)/448, round to nearest even,
+ * clamped to +-448).  y_perm rows of padding (row >= count within a segment)
+ * are either zero or left untouched; they are never combined.
+ */
+typedef struct moe_op_desc {
+    int32_t phase;            /* MOE_PREFILL or MOE_DECODE                              */
+    int32_t layer;            /* informational; recorded in the trace                   */
+    int32_t E_local, H, I;    /* H, I multiples of 256                                  */
+    int32_t capacity;         /* rows of x_perm / h / y_perm                            */
+    int32_t row_align;        /* must equal moe_ffn_row_align(phase, dtype)             */
+    moe_dtype_t dtype;        /* MOE_BF16 or MOE_FP8_E4M3 (activations and weights)      */
+    const int32_t* counts;    /* [E_local]     from moe_permute                          */
+    const int32_t* offsets;   /* [E_local+1]   from moe_permute                          */
+    const void*  x_perm;      /* [capacity, H]                                          */
+    const float* x_perm_scales;      /* [capacity, H/128]            fp8 only           */
+    const void*  w_gate_up;          /* [E_local, 2I, H] gate rows 0..I-1, up rows I..2I-1 */
+    const float* w_gate_up_scales;   /* [E_local, 2I/128, H/128]     fp8 only           */
+    const void*  w_down;             /* [E_local, H, I]                                  */
+    const float* w_down_scales;      /* [E_local, H/128, I/128]      fp8 only           */
+    void*  h;                 /* [capacity, I] intermediate (bf16, or fp8 codes)         */
+    float* h_scales;          /* [capacity, I/128]              fp8 only                 */
+    void*  y_perm;            /* [capacity, H] bf16 out                                  */
+    /* Readiness ("One-Sided Dispatch and Combine": a ready signal is published
+     * only after the payload is visible).  The op is ready when ALL hold:   */
+    const uint32_t* release_word; /* NULL, or *release_word != 0 (system-scope acquire) */
+    int64_t release_after_ns;     /* < 0: no time condition; else device wall clock >=
+                                     kernel start + release_after_ns                     */
+    int32_t depends_on_op;        /* -1, or an EARLIER op index that must be done...     */
+    int32_t reserved0;
+    int64_t gap_ns;               /* ...for at least gap_ns                              */
+    uint32_t* done_word;          /* NULL, or set to 1 (system-scope release) when the
+                                     op's last tile has committed                        */
+} moe_op_desc;
+
+/* Per-tile trace record (times in device wall-clock ticks, 100 MHz on gfx950). */
+typedef struct moe_trace_rec {
+    int16_t op, stage;        /* stage 1 = GEMM-1 (+activation), 2 = GEMM-2             */
+    int16_t wg, xcc;          /* workgroup index and the XCD it ran on                  */
+    int32_t expert, mblk;     /* local expert and row-block within its segment          */
+    int32_t nblk, rows;       /* column block and valid rows in the tile               */
+    uint64_t t_claim, t_start, t_end; /* claimed, dependencies met, committed           */
+} moe_trace_rec;
+
+/* Per-op statistics written by the persistent kernel (times in wall-clock ticks). */
+typedef struct moe_op_stats {
+    uint64_t t_ready;         /* instantiation (release observed)                       */
+    uint64_t t_first;         /* first tile started                                     */
+    uint64_t t_done;          /* last tile committed                                    */
+    int32_t x_moe;            /* Eq. (3) footprint at the op's row_align                */
+    int32_t n_tiles;          /* GEMM-1 + GEMM-2 tiles                                  */
+    int32_t quota;            /* decode ops: q' of Eq. (4) in workgroups; prefill: 0    */
+    int32_t reserved;
+} moe_op_stats;
+
+/* Scheduler policy ("Online SM Reallocation", Eq. (4)): under contention decode
+ * may hold up to q' = min(Q_max, ceil_c(q * x_moe / x*_moe)) workgroups and
+ * prefill takes the rest; a lone ready phase takes every workgroup.  Workgroups
+ * with index < q' prefer decode tiles, the others prefer prefill; any
+ * workgroup takes the other phase's tile when its preferred queue is empty;
+ * a workgroup switches phase only between tiles. */
+typedef struct moe_sched_config {
+    int32_t n_workgroups;     /* 0 = one per CU                                         */
+    int32_t decode_quota_wg;  /* q  (e.g. 64 = 25% of 256)                              */
+    int32_t decode_quota_max_wg; /* Q_max; 0 = n_workgroups / 2                          */
+    int32_t x_moe_expected;   /* x*_moe; <= 0 selects the fixed quota (ratio 1)         */
+    int32_t round_multiple;   /* c; 0 = 8 (one workgroup per XCD)                       */
+    int32_t reserved0;
+    const uint32_t* abort_word;   /* NULL, or host/peer-writable: non-zero stops the
+                                     kernel at the next tile boundary (MOE_ERR_ABORTED) */
+    moe_trace_rec* trace;     /* NULL, or [trace_capacity] records                      */
+    int64_t trace_capacity;
+    moe_op_stats* op_stats;   /* NULL, or [n_ops]                                       */
+    int64_t spin_limit;       /* bounded waits, in polls; 0 = default (about 2 s)       */
+} moe_sched_config;
+
+/* Tile height M_t the FFN uses for ops of this phase and dtype; moe_permute's
+ * row_align for such an op must equal it.  Returns <= 0 if unsupported. */
+int32_t moe_ffn_row_align(moe_phase_t phase, moe_dtype_t dtype);
+
+/* Device scratch needed by one persistent launch over these ops (host array). */
+size_t moe_ffn_workspace_bytes(const moe_op_desc* ops, int32_t n_ops, const moe_sched_config* cfg);
+
+/* Launch the adaptive persistent kernel over n_ops operations (ops, cfg: host
+ * pointers, read before the call returns).  status_word is a device i32 that
+ * this call resets to MOE_OK (on the stream) and the kernel sets to the first
+ * data-dependent error.  workspace is moe_ffn_workspace_bytes() bytes. */
+moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32_t n_ops,
+                                        const moe_sched_config* cfg, void* workspace,
+                                        int32_t* status_word, void* stream);
+
+/* ------------------------------------------------------------------------- a7
+ * Weighted combine (Background, "MoE LLM Inference": the chosen experts'
+ * outputs are combined before the next layer):
+ *   y[t] = sum over j ascending with assign_to_row[t*top_k+j] >= 0 of
+ *          topk_w[t*top_k+j] * y_perm[assign_to_row[t*top_k+j]]
+ * accumulated in fp32.  A token with no local slot gets exactly 0.
+ *  y_perm [*, H] bf16; assign_to_row [T*top_k]; topk_w [T*top_k] f32
+ *  y      [T, H] out, y_dtype MOE_BF16 (round to nearest even) or MOE_F32
+ * Limits: H a multiple of 8, 1 <= top_k <= 32.
+ */
+moe_status_t moe_combine(const void* y_perm, const int32_t* assign_to_row, const float* topk_w,
+                         int32_t T, int32_t top_k, int32_t H, void* y, moe_dtype_t y_dtype,
+                         void* stream);
+
+/* ------------------------------------------------------------------------- host helpers
+ * Pure host arithmetic shared with the kernels (no device access):
+ * Eq. (3) footprint over host counts, and Eq. (4) quota in workgroups. */
+int32_t moe_x_moe(const int32_t* counts_host, int32_t E_local, int32_t M_t);
+int32_t moe_decode_quota(int32_t q, int32_t x_moe, int32_t x_moe_expected, int32_t q_max,
+                         int32_t round_multiple);
+
+/* sizeof() of the ABI structs, so bindings can check their layout:
+ * 0 moe_op_desc, 1 moe_sched_config, 2 moe_trace_rec, 3 moe_op_stats; 0 otherwise. */
+size_t moe_abi_sizeof(int32_t which);
+
+const char* moe_status_string(moe_status_t status);
+const char* moe_last_error(void);   /* thread-local message of the last failing call */
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOE_APK_H */

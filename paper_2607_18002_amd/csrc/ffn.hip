@@ -1,0 +1,534 @@
+// a3-a6: the SwiGLU expert FFN as one adaptive persistent kernel.
+//
+// Paper passages: Adaptive Persistent Kernel -- "Tile-Level Scheduling" (a
+// tile is the scheduling unit; phases switch only when a tile commits;
+// operation templates are instantiated into a decode or a prefill queue when
+// their ready signal is seen), "Bounded Tile-level Preemption" (a decision is
+// read once per tile boundary and broadcast to the whole cooperating unit),
+// "Online SM Reallocation" Eq. (4) (decode quota under contention, a lone
+// phase takes everything), "Tile-aware Latency Model" Eq. (3) (the number of
+// executed row tiles); Evaluation "Implementation" (two grouped GEMMs and the
+// activation fused into one long-lived kernel).
+//
+// MI355X design.  One 256-thread workgroup per CU, fixed grid.  CDNA4 has no
+// thread-block clusters, so the unit of scheduling is the workgroup: wave 0
+// polls the operation words (one lane per operation), claims a tile with one
+// device-scope atomic and broadcasts it through LDS; the whole workgroup then
+// runs the tile and wave 0's first lane commits it.  Each operation's tiles
+// are numbered GEMM-1 tiles first (row tile major), then GEMM-2 tiles; a GEMM-2
+// tile waits (bounded) on a per-row-tile counter that GEMM-1 tiles bump with
+// agent-scope release semantics, so the h handoff is coherent across the
+// eight XCD-private L2 caches.  Every claimed tile belongs to a running
+// workgroup, so the dependency waits cannot deadlock.
+#include <cstring>
+
+#include "tile_bf16.hpp"
+
+namespace {
+
+using namespace moeapk;
+
+using ShapeP = TileShape<128, 256, 64, 2, 2>;    // prefill: 128 x 256 tile, K step 64
+using ShapeD = TileShape<128, 128, 128, 2, 2>;   // decode : 128 x 128 tile, K step 128 (more bytes in flight)
+constexpr int kLdsBytes = ShapeP::LDS > ShapeD::LDS ? ShapeP::LDS : ShapeD::LDS;
+constexpr int kRowAlign = 128;                   // M_t of both bf16 classes
+
+enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1 };
+enum : int32_t { ST_WAIT = 0, ST_INIT = 1, ST_ACTIVE = 2, ST_DONE = 3 };
+enum : int32_t { CMD_EXIT = 0, CMD_TILE = 1, CMD_INST = 2, CMD_IDLE = 3 };
+
+struct OpArg {
+    const int32_t* counts;
+    const int32_t* offsets;
+    const uint16_t* x;
+    const uint16_t* wgu;
+    const uint16_t* wd;
+    uint16_t* h;
+    uint16_t* y;
+    uint32_t* done_word;
+    int32_t cls, phase, layer, E, H, I, capacity, mt, n1, n2, max_mtiles, table_off, g1_off, pad;
+};
+
+struct KArgs {
+    OpArg op[MOE_MAX_OPS];
+    int32_t n_ops, q, q_max, x_star, c, pad;
+    int64_t spin_limit;
+    const uint32_t* abort_word;
+    moe_trace_rec* trace;
+    int64_t trace_cap;
+    moe_op_stats* stats;
+    int32_t* status;
+    char* ws;
+};
+
+// Static polling fields per op, written by the init kernel (so wave 0 can read
+// them with one lane per op) plus the run-time state of the op.
+struct OpSt {
+    int32_t state, claim, done, x_moe;                 // 0
+    int32_t total, n1t, quota, phase;                  // 16
+    int32_t dep, pad0;                                 // 32
+    const uint32_t* rel_word;                          // 40
+    int64_t rel_after, gap;                            // 48  (ticks; rel_after < 0: none)
+    unsigned long long t_ready, t_first, t_done;       // 64
+    char pad[128 - 88];
+};
+static_assert(sizeof(OpSt) == 128, "one L2 line per op");
+
+struct Hdr {
+    unsigned long long t0;
+    int32_t ops_done, quota, trace_count, stop;
+};
+
+constexpr size_t kHdrBytes = 256;
+constexpr size_t kArraysOff = kHdrBytes + MOE_MAX_OPS * sizeof(OpSt);
+
+__device__ __forceinline__ Hdr* hdr_of(char* ws) { return (Hdr*)ws; }
+__device__ __forceinline__ OpSt* opst_of(char* ws) { return (OpSt*)(ws + kHdrBytes); }
+__device__ __forceinline__ int32_t* arr_of(char* ws) { return (int32_t*)(ws + kArraysOff); }
+
+// ----------------------------------------------------------------------------- init
+// Readiness fields of every op, passed by value (no host staging buffer).
+struct InitArgs {
+    const uint32_t* rel_words[MOE_MAX_OPS];
+    int64_t rel_after[MOE_MAX_OPS];
+    int64_t gaps[MOE_MAX_OPS];
+    int32_t deps[MOE_MAX_OPS];
+    int32_t phases[MOE_MAX_OPS];
+    int32_t n_ops, ws_words;
+    char* ws;
+    int32_t* status;
+};
+
+// Zeroes the scheduler state and publishes the polling fields; one workgroup,
+// launched on the same stream right before the persistent kernel.
+__global__ __launch_bounds__(256) void apk_init_kernel(const InitArgs a) {
+    int32_t* w = (int32_t*)a.ws;
+    for (int i = threadIdx.x; i < a.ws_words; i += 256) w[i] = 0;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        OpSt* st = opst_of(a.ws);
+        for (int o = 0; o < a.n_ops; ++o) {
+            st[o].phase = a.phases[o];
+            st[o].dep = a.deps[o];
+            st[o].rel_word = a.rel_words[o];
+            st[o].rel_after = a.rel_after[o];
+            st[o].gap = a.gaps[o];
+        }
+        *a.status = MOE_OK;
+    }
+}
+
+// ----------------------------------------------------------------------------- tiles
+__device__ __forceinline__ void run_tile(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds) {
+    const long H = op.H, I = op.I;
+    if (op.cls == CLS_P_BF16) {
+        if (stage == 1) {
+            gemm_tile_bf16<ShapeP, true>(op.x + row0 * H, (int)H, rows32,
+                                         op.wgu + (long)e * 2 * I * H + (long)nb * (ShapeP::BN / 2) * H, (int)H, I * H,
+                                         (int)H, op.h + row0 * I + nb * (ShapeP::BN / 2), (int)I, lds);
+        } else {
+            gemm_tile_bf16<ShapeP, false>(op.h + row0 * I, (int)I, rows32,
+                                          op.wd + (long)e * H * I + (long)nb * ShapeP::BN * I, (int)I, 0, (int)I,
+                                          op.y + row0 * H + nb * ShapeP::BN, (int)H, lds);
+        }
+    } else {
+        if (stage == 1) {
+            gemm_tile_bf16<ShapeD, true>(op.x + row0 * H, (int)H, rows32,
+                                         op.wgu + (long)e * 2 * I * H + (long)nb * (ShapeD::BN / 2) * H, (int)H, I * H,
+                                         (int)H, op.h + row0 * I + nb * (ShapeD::BN / 2), (int)I, lds);
+        } else {
+            gemm_tile_bf16<ShapeD, false>(op.h + row0 * I, (int)I, rows32,
+                                          op.wd + (long)e * H * I + (long)nb * ShapeD::BN * I, (int)I, 0, (int)I,
+                                          op.y + row0 * H + nb * ShapeD::BN, (int)H, lds);
+        }
+    }
+}
+
+// ----------------------------------------------------------------------------- scheduler
+// Shared command block written by wave 0 and read by the whole workgroup.
+struct Cmd {
+    int32_t kind, op, stage, e, row0, rows32, nb, mtile, mblk, rows, t;
+    unsigned long long t_claim, t_start;
+};
+
+// Wave 0: read the decision words once per tile boundary and pick the next action.
+__device__ void schedule(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, int64_t& idle) {
+    const int lane = threadIdx.x;
+    Hdr* hdr = hdr_of(a.ws);
+    OpSt* st = opst_of(a.ws);
+    int stop = 0;
+    if (lane == 0) {
+        stop = ld_relaxed_agent(&hdr->stop);
+        if (!stop && a.abort_word && ld_acquire_system(a.abort_word) != 0u) {
+            set_status(a.status, MOE_ERR_ABORTED);
+            st_release_agent(&hdr->stop, 1);
+            stop = 1;
+        }
+        if (!stop && idle > a.spin_limit) {                       // nothing claimable for too long
+            set_status(a.status, MOE_ERR_TIMEOUT);
+            st_release_agent(&hdr->stop, 1);
+            stop = 1;
+        }
+    }
+    if (__shfl(stop, 0, 64)) {
+        if (lane == 0) cmd->kind = CMD_EXIT;
+        return;
+    }
+    const bool has = lane < a.n_ops;
+    OpSt* my = st + (has ? lane : 0);
+    const int state = has ? ld_acquire_agent(&my->state) : ST_DONE;
+    if (__ballot(state != ST_DONE) == 0) {
+        if (lane == 0) cmd->kind = CMD_EXIT;
+        return;
+    }
+    const uint64_t now = wall_ticks();
+
+    // 1. ready signals of waiting operation templates -> instantiate one of them
+    bool ready = false;
+    if (state == ST_WAIT) {
+        ready = true;
+        const uint32_t* rw = my->rel_word;
+        if (rw) ready = ld_acquire_system(rw) != 0u;
+        if (ready && my->rel_after >= 0) ready = now >= t0 + (uint64_t)my->rel_after;
+        const int dep = my->dep;
+        if (ready && dep >= 0) {
+            ready = ld_acquire_agent(&st[dep].state) == ST_DONE &&
+                    now >= ld_relaxed_agent(&st[dep].t_done) + (uint64_t)my->gap;
+        }
+    }
+    const uint64_t rmask = __ballot(ready);
+    if (rmask) {
+        const int o = __ffsll((long long)rmask) - 1;
+        int won = 0;
+        if (lane == o) won = atomicCAS(&my->state, ST_WAIT, ST_INIT) == ST_WAIT;
+        if (__ballot(won)) {
+            if (lane == 0) { cmd->kind = CMD_INST; cmd->op = o; }
+            return;
+        }
+    }
+
+    // 2. claim a tile: decode first on workgroups below q', prefill first elsewhere
+    const int claim = (state == ST_ACTIVE) ? ld_relaxed_agent(&my->claim) : 0;
+    const int total = (state == ST_ACTIVE) ? my->total : 0;
+    const bool avail = state == ST_ACTIVE && claim < total;
+    const int phase = has ? my->phase : 0;
+    const uint64_t dmask = __ballot(avail && phase == MOE_DECODE);
+    const uint64_t pmask = __ballot(avail && phase == MOE_PREFILL);
+    const int q = ld_relaxed_agent(&hdr->quota);
+    const bool prefer_decode = wg < q;
+    uint64_t order[2] = {prefer_decode ? dmask : pmask, prefer_decode ? pmask : dmask};
+    for (int p = 0; p < 2; ++p) {
+        uint64_t m = order[p];
+        while (m) {                                                  // wave-uniform loop
+            const int o = __ffsll((long long)m) - 1;
+            m &= m - 1;
+            const int tot = __shfl(total, o, 64);
+            int t = 0;
+            if (lane == 0) t = atomicAdd(&st[o].claim, 1);
+            t = __shfl(t, 0, 64);
+            if (t >= tot) continue;
+            if (lane == 0) {
+                const OpArg& op = a.op[o];
+                const int n1t = st[o].n1t;
+                int stage, mtile, nb;
+                if (t < n1t) { stage = 1; mtile = t / op.n1; nb = t % op.n1; }
+                else { stage = 2; mtile = (t - n1t) / op.n2; nb = (t - n1t) % op.n2; }
+                const int entry = arr_of(a.ws)[op.table_off + mtile];
+                const int e = entry >> 16, mb = entry & 0xFFFF;
+                const int rows_left = op.counts[e] - mb * op.mt;
+                const int rows = rows_left < op.mt ? rows_left : op.mt;
+                cmd->kind = CMD_TILE; cmd->op = o; cmd->stage = stage; cmd->e = e; cmd->mblk = mb;
+                cmd->row0 = op.offsets[e] + mb * op.mt; cmd->rows = rows; cmd->rows32 = (rows + 31) & ~31;
+                cmd->nb = nb; cmd->mtile = mtile; cmd->t = t;
+                cmd->t_claim = wall_ticks();
+                if (t == 0) st[o].t_first = cmd->t_claim;
+                bool ok = true;
+                if (stage == 2) {                                     // GEMM-1 of this row tile must be committed
+                    const int32_t* g1 = arr_of(a.ws) + op.g1_off + mtile;
+                    int64_t spins = 0;
+                    while (ld_acquire_agent(g1) < op.n1) {
+                        if (++spins > a.spin_limit || ld_relaxed_agent(&hdr->stop)) { ok = false; break; }
+                        __builtin_amdgcn_s_sleep(2);
+                    }
+                    if (!ok) {
+                        set_status(a.status, MOE_ERR_TIMEOUT);
+                        st_release_agent(&hdr->stop, 1);
+                        cmd->kind = CMD_EXIT;
+                    }
+                }
+                cmd->t_start = wall_ticks();
+            }
+            idle = 0;
+            return;
+        }
+    }
+    if (lane == 0) cmd->kind = CMD_IDLE;
+    ++idle;
+}
+
+// Whole workgroup: build the row-tile table of an operation whose ready signal was seen.
+__device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
+    const OpArg& op = a.op[o];
+    OpSt* st = opst_of(a.ws) + o;
+    int32_t* table = arr_of(a.ws) + op.table_off;
+    for (int e = threadIdx.x; e < op.E; e += 256) {
+        const int c = op.counts[e];
+        scan[e] = c > 0 ? (c + op.mt - 1) / op.mt : 0;
+    }
+    __syncthreads();
+    __shared__ int32_t s_total, s_bad;
+    if (threadIdx.x == 0) {
+        int run = 0;
+        for (int e = 0; e < op.E; ++e) { const int v = scan[e]; scan[e] = run; run += v; }
+        s_total = run;
+        s_bad = 0;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < op.E; e += 256) {
+        const int c = op.counts[e];
+        const int nt = c > 0 ? (c + op.mt - 1) / op.mt : 0;
+        const int pos = scan[e];
+        if (pos + nt > op.max_mtiles || (long)op.offsets[e] + (long)nt * op.mt > op.capacity) { s_bad = 1; continue; }
+        for (int mb = 0; mb < nt; ++mb) table[pos + mb] = (e << 16) | mb;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        Hdr* hdr = hdr_of(a.ws);
+        if (s_bad) {
+            set_status(a.status, MOE_ERR_CAPACITY);
+            st_release_agent(&hdr->stop, 1);
+            return;
+        }
+        const int xm = s_total;
+        st->x_moe = xm;
+        st->n1t = xm * op.n1;
+        st->total = xm * (op.n1 + op.n2);
+        st->t_ready = wall_ticks();
+        int qd = 0;
+        if (op.phase == MOE_DECODE) {
+            qd = decode_quota(a.q, xm, a.x_star, a.q_max, a.c);
+            st_release_agent(&hdr->quota, qd);
+        }
+        st->quota = qd;
+        if (xm == 0) {                                   // nothing routed here: done at once
+            st->t_first = st->t_ready;
+            st->t_done = st->t_ready;
+            st_release_agent(&st->state, (int32_t)ST_DONE);
+            if (op.done_word) st_release_system(op.done_word, 1u);
+            if (a.stats) {
+                moe_op_stats s = {st->t_ready, st->t_ready, st->t_ready, 0, 0, qd, 0};
+                a.stats[o] = s;
+            }
+            add_relaxed_agent(&hdr->ops_done, 1);
+        } else {
+            st_release_agent(&st->state, (int32_t)ST_ACTIVE);
+        }
+    }
+}
+
+__global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
+    extern __shared__ __align__(16) char lds[];
+    __shared__ Cmd cmd;
+    __shared__ int32_t scan[1024];
+    __shared__ unsigned long long s_t0;
+    const int tid = threadIdx.x;
+    const int wg = blockIdx.x;
+    if (tid == 0) {
+        const unsigned long long now = wall_ticks();
+        const unsigned long long prev = atomicCAS(&hdr_of(a.ws)->t0, 0ull, now);
+        s_t0 = prev ? prev : now;
+    }
+    __syncthreads();
+    const uint64_t t0 = s_t0;
+    int64_t idle = 0;
+    for (;;) {
+        if (tid < 64) schedule(a, t0, wg, &cmd, idle);
+        __syncthreads();
+        const int kind = cmd.kind;
+        if (kind == CMD_EXIT) break;
+        if (kind == CMD_IDLE) {
+            __builtin_amdgcn_s_sleep(8);
+            __syncthreads();                                  // cmd is rewritten next iteration
+            continue;
+        }
+        if (kind == CMD_INST) {
+            const int o = __builtin_amdgcn_readfirstlane(cmd.op);
+            __syncthreads();
+            instantiate(a, o, scan);
+            __syncthreads();
+            continue;
+        }
+        const int o = __builtin_amdgcn_readfirstlane(cmd.op);
+        const int stage = __builtin_amdgcn_readfirstlane(cmd.stage);
+        const int row0 = __builtin_amdgcn_readfirstlane(cmd.row0);
+        const int rows32 = __builtin_amdgcn_readfirstlane(cmd.rows32);
+        const int nb = __builtin_amdgcn_readfirstlane(cmd.nb);
+        const int e = __builtin_amdgcn_readfirstlane(cmd.e);
+        __syncthreads();                                      // every thread has read cmd
+        run_tile(a.op[o], stage, row0, rows32, nb, e, lds);
+        __syncthreads();                                      // all stores of the tile issued and complete
+        if (tid == 0) {
+            const OpArg& op = a.op[o];
+            OpSt* st = opst_of(a.ws) + o;
+            Hdr* hdr = hdr_of(a.ws);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // publish h / y of this tile
+            if (stage == 1) add_relaxed_agent(arr_of(a.ws) + op.g1_off + cmd.mtile, 1);
+            const int total = st->total;
+            const int done = add_relaxed_agent(&st->done, 1) + 1;
+            const unsigned long long t_end = wall_ticks();
+            if (done == total) {
+                st->t_done = t_end;
+                st_release_agent(&st->state, (int32_t)ST_DONE);
+                if (op.done_word) st_release_system(op.done_word, 1u);
+                if (a.stats) {
+                    moe_op_stats s = {st->t_ready, st->t_first, t_end, st->x_moe, total, st->quota, 0};
+                    a.stats[o] = s;
+                }
+                add_relaxed_agent(&hdr->ops_done, 1);
+            }
+            if (a.trace) {
+                const int idx = add_relaxed_agent(&hdr->trace_count, 1);
+                if (idx < a.trace_cap) {
+                    moe_trace_rec r;
+                    r.op = (int16_t)o; r.stage = (int16_t)stage; r.wg = (int16_t)wg; r.xcc = (int16_t)xcc_id();
+                    r.expert = cmd.e; r.mblk = cmd.mblk; r.nblk = cmd.nb; r.rows = cmd.rows;
+                    r.t_claim = cmd.t_claim; r.t_start = cmd.t_start; r.t_end = t_end;
+                    a.trace[idx] = r;
+                }
+            }
+        }
+    }
+}
+
+struct ClassInfo {
+    int bn, bk;
+};
+ClassInfo class_info(int cls) { return cls == CLS_P_BF16 ? ClassInfo{ShapeP::BN, ShapeP::BK} : ClassInfo{ShapeD::BN, ShapeD::BK}; }
+
+size_t ws_words_for(const moe_op_desc* ops, int n_ops) {
+    size_t words = kArraysOff / 4;
+    for (int o = 0; o < n_ops; ++o) {
+        const int mt = ops[o].row_align > 0 ? ops[o].row_align : 1;
+        const size_t mm = (size_t)((ops[o].capacity + mt - 1) / mt) + 1;
+        words += 2 * mm;
+    }
+    return (words + 63) & ~(size_t)63;
+}
+
+}  // namespace
+
+extern "C" int32_t moe_ffn_row_align(moe_phase_t phase, moe_dtype_t dtype) {
+    if (phase != MOE_PREFILL && phase != MOE_DECODE) return -1;
+    if (dtype != MOE_BF16) return -2;
+    return kRowAlign;
+}
+
+extern "C" size_t moe_ffn_workspace_bytes(const moe_op_desc* ops, int32_t n_ops, const moe_sched_config* cfg) {
+    (void)cfg;
+    if (!ops || n_ops < 1 || n_ops > MOE_MAX_OPS) return 0;
+    return ws_words_for(ops, n_ops) * 4;
+}
+
+extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32_t n_ops, const moe_sched_config* cfg,
+                                                   void* workspace, int32_t* status_word, void* stream) {
+    using moeapk_host::fail;
+    if (!ops || !cfg || !workspace || !status_word) return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn_persistent: null pointer");
+    if (n_ops < 1 || n_ops > MOE_MAX_OPS)
+        return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn_persistent: n_ops=%d outside [1,%d]", n_ops, MOE_MAX_OPS);
+    int cu = 0, wc_khz = 0;
+    moe_status_t st = moeapk_host::check_device(&cu, &wc_khz);
+    if (st != MOE_OK) return st;
+
+    KArgs a;
+    memset(&a, 0, sizeof(a));
+    InitArgs ia;
+    memset(&ia, 0, sizeof(ia));
+    size_t words = kArraysOff / 4;
+    for (int o = 0; o < n_ops; ++o) {
+        const moe_op_desc& d = ops[o];
+        if (d.phase != MOE_PREFILL && d.phase != MOE_DECODE) return fail(MOE_ERR_INVALID_ARG, "op %d: bad phase %d", o, d.phase);
+        if (d.dtype != MOE_BF16) return fail(MOE_ERR_UNSUPPORTED, "op %d: dtype %d not supported by the FFN kernel", o, d.dtype);
+        const int cls = d.phase == MOE_PREFILL ? CLS_P_BF16 : CLS_D_BF16;
+        const ClassInfo ci = class_info(cls);
+        if (d.E_local < 1 || d.E_local > 1024 || d.E_local >= 32768) return fail(MOE_ERR_UNSUPPORTED, "op %d: E_local=%d", o, d.E_local);
+        if (d.H < ci.bn || d.H % ci.bn != 0 || d.H % ci.bk != 0 || d.H % 256 != 0)
+            return fail(MOE_ERR_UNSUPPORTED, "op %d: H=%d must be a positive multiple of 256", o, d.H);
+        if (d.I < ci.bn / 2 || d.I % (ci.bn / 2) != 0 || d.I % ci.bk != 0 || d.I % 256 != 0)
+            return fail(MOE_ERR_UNSUPPORTED, "op %d: I=%d must be a positive multiple of 256", o, d.I);
+        if (d.row_align != kRowAlign)
+            return fail(MOE_ERR_INVALID_ARG, "op %d: row_align=%d but the FFN tile height is %d", o, d.row_align, kRowAlign);
+        if (d.capacity < d.row_align) return fail(MOE_ERR_CAPACITY, "op %d: capacity=%d below one tile", o, d.capacity);
+        if ((int64_t)d.capacity * d.H > INT32_MAX || (int64_t)d.capacity * d.I > INT32_MAX)
+            return fail(MOE_ERR_UNSUPPORTED, "op %d: capacity*H exceeds 2^31 elements", o);
+        if (!d.counts || !d.offsets || !d.x_perm || !d.w_gate_up || !d.w_down || !d.h || !d.y_perm)
+            return fail(MOE_ERR_INVALID_ARG, "op %d: null buffer", o);
+        if (d.depends_on_op >= o || d.depends_on_op < -1)
+            return fail(MOE_ERR_INVALID_ARG, "op %d: depends_on_op=%d must be -1 or an earlier op", o, d.depends_on_op);
+        if (d.gap_ns < 0) return fail(MOE_ERR_INVALID_ARG, "op %d: gap_ns < 0", o);
+        OpArg& p = a.op[o];
+        p.counts = d.counts;
+        p.offsets = d.offsets;
+        p.x = (const uint16_t*)d.x_perm;
+        p.wgu = (const uint16_t*)d.w_gate_up;
+        p.wd = (const uint16_t*)d.w_down;
+        p.h = (uint16_t*)d.h;
+        p.y = (uint16_t*)d.y_perm;
+        p.done_word = d.done_word;
+        p.cls = cls;
+        p.phase = d.phase;
+        p.layer = d.layer;
+        p.E = d.E_local;
+        p.H = d.H;
+        p.I = d.I;
+        p.capacity = d.capacity;
+        p.mt = d.row_align;
+        p.n1 = d.I / (ci.bn / 2);
+        p.n2 = d.H / ci.bn;
+        const int mm = (d.capacity + d.row_align - 1) / d.row_align + 1;
+        p.max_mtiles = mm;
+        p.table_off = (int)(words - kArraysOff / 4);
+        p.g1_off = p.table_off + mm;
+        words += 2 * (size_t)mm;
+        ia.rel_words[o] = d.release_word;
+        ia.rel_after[o] = d.release_after_ns < 0 ? -1 : d.release_after_ns * (int64_t)wc_khz / 1000000;
+        ia.gaps[o] = d.gap_ns * (int64_t)wc_khz / 1000000;
+        ia.deps[o] = d.depends_on_op;
+        ia.phases[o] = d.phase;
+    }
+    int n_wg = cfg->n_workgroups > 0 ? cfg->n_workgroups : cu;
+    a.n_ops = n_ops;
+    a.q = cfg->decode_quota_wg < 0 ? 0 : cfg->decode_quota_wg;
+    a.q_max = cfg->decode_quota_max_wg > 0 ? cfg->decode_quota_max_wg : n_wg / 2;
+    a.x_star = cfg->x_moe_expected;
+    a.c = cfg->round_multiple > 0 ? cfg->round_multiple : 8;
+    a.spin_limit = cfg->spin_limit > 0 ? cfg->spin_limit : (int64_t)2000000;
+    a.abort_word = cfg->abort_word;
+    a.trace = cfg->trace;
+    a.trace_cap = cfg->trace ? cfg->trace_capacity : 0;
+    a.stats = cfg->op_stats;
+    a.status = status_word;
+    a.ws = (char*)workspace;
+
+    static bool attr_set = false;
+    if (!attr_set) {
+        if (hipFuncSetAttribute((const void*)apk_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes) != hipSuccess)
+            return fail(MOE_ERR_HIP, "hipFuncSetAttribute(LDS=%d) failed", kLdsBytes);
+        attr_set = true;
+    }
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)apk_kernel, 256, kLdsBytes) != hipSuccess)
+        return fail(MOE_ERR_HIP, "occupancy query failed");
+    if (per_cu < 1) return fail(MOE_ERR_UNSUPPORTED, "persistent kernel does not fit on a CU");
+    if (n_wg > per_cu * cu) return fail(MOE_ERR_INVALID_ARG, "n_workgroups=%d exceeds co-resident capacity %d", n_wg, per_cu * cu);
+
+    ia.n_ops = n_ops;
+    ia.ws_words = (int32_t)words;
+    ia.ws = (char*)workspace;
+    ia.status = status_word;
+    hipStream_t s = (hipStream_t)stream;
+    hipLaunchKernelGGL(apk_init_kernel, dim3(1), dim3(256), 0, s, ia);
+    hipLaunchKernelGGL(apk_kernel, dim3(n_wg), dim3(256), kLdsBytes, s, a);
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return fail(MOE_ERR_HIP, "moe_grouped_ffn_persistent: launch failed: %s", hipGetErrorString(err));
+    return MOE_OK;
+}

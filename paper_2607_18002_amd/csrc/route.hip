@@ -1,0 +1,101 @@
+// a1: top-k softmax gating (Background, "MoE LLM Inference").
+//
+// One 64-wide wave per token.  Lane l holds experts l, l+64, ... as 64-bit
+// order keys: high half = the fp32 logit mapped to an unsigned integer that
+// orders like the float (-0.0 folded onto +0.0), low half = ~expert so that
+// equal logits prefer the lower expert index.  Each of the k rounds takes a
+// wave-wide max with xor-shuffles and retires the winner; lane j keeps slot j.
+#include "common.hpp"
+
+namespace {
+
+constexpr int kTokensPerBlock = 4;  // one wave each
+
+__device__ __forceinline__ uint64_t order_key(float v, uint32_t e) {
+    uint32_t u = __float_as_uint(v);
+    if (u == 0x80000000u) u = 0u;                        // -0.0 ties with +0.0
+    uint32_t k = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return ((uint64_t)k << 32) | (uint64_t)(0xFFFFFFFFu - e);
+}
+
+__device__ __forceinline__ float key_value(uint64_t key) {
+    uint32_t k = (uint32_t)(key >> 32);
+    uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+    return __uint_as_float(u);
+}
+
+template <int EPL>
+__global__ __launch_bounds__(256) void topk_route_kernel(const float* __restrict__ logits, int T, int E, int k,
+                                                        int local_begin, int E_local, int32_t* __restrict__ ids,
+                                                        float* __restrict__ wts) {
+    const int lane = threadIdx.x & 63;
+    const int t = blockIdx.x * kTokensPerBlock + (threadIdx.x >> 6);
+    if (t >= T) return;  // wave-uniform
+    const float* row = logits + (size_t)t * E;
+    uint64_t key[EPL];
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) {
+        const int e = lane + 64 * i;
+        key[i] = (e < E) ? order_key(row[e], (uint32_t)e) : 0ull;
+    }
+    int my_e = -1;
+    float my_v = 0.f;
+    for (int r = 0; r < k; ++r) {
+        uint64_t best = 0;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) best = key[i] > best ? key[i] : best;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            const uint64_t o = __shfl_xor(best, off, 64);
+            best = o > best ? o : best;
+        }
+        const int e = (int)(0xFFFFFFFFu - (uint32_t)best);
+#pragma unroll
+        for (int i = 0; i < EPL; ++i)
+            if (lane + 64 * i == e) key[i] = 0ull;       // retire the winner
+        if (lane == r) {
+            my_e = e;
+            my_v = key_value(best);
+        }
+    }
+    const float m = __shfl(my_v, 0, 64);                 // the largest selected logit
+    const float ex = (lane < k) ? expf(my_v - m) : 0.f;
+    float s = ex;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+    if (lane < k) {
+        const int loc = my_e - local_begin;
+        ids[(size_t)t * k + lane] = (loc >= 0 && loc < E_local) ? loc : -1;
+        wts[(size_t)t * k + lane] = ex / s;
+    }
+}
+
+}  // namespace
+
+extern "C" moe_status_t moe_topk_route(const float* logits, int32_t T, int32_t E_global, int32_t top_k,
+                                       int32_t local_begin, int32_t E_local, int32_t* topk_ids, float* topk_w,
+                                       void* stream) {
+    using moeapk_host::fail;
+    if (T < 0) return fail(MOE_ERR_INVALID_ARG, "moe_topk_route: T=%d < 0", T);
+    if (E_global < 1 || E_global > 1024)
+        return fail(MOE_ERR_UNSUPPORTED, "moe_topk_route: E_global=%d outside [1,1024]", E_global);
+    if (top_k < 1 || top_k > E_global || top_k > 32)
+        return fail(MOE_ERR_INVALID_ARG, "moe_topk_route: top_k=%d outside [1, min(E_global,32)]", top_k);
+    if (local_begin < 0 || E_local < 1)
+        return fail(MOE_ERR_INVALID_ARG, "moe_topk_route: local_begin=%d E_local=%d", local_begin, E_local);
+    if (T == 0) return MOE_OK;
+    if (!logits || !topk_ids || !topk_w) return fail(MOE_ERR_INVALID_ARG, "moe_topk_route: null pointer");
+    moe_status_t st = moeapk_host::check_device();
+    if (st != MOE_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    const dim3 grid((T + kTokensPerBlock - 1) / kTokensPerBlock), block(256);
+    const int epl = (E_global + 63) / 64;
+    if (epl <= 1) hipLaunchKernelGGL(topk_route_kernel<1>, grid, block, 0, s, logits, T, E_global, top_k, local_begin, E_local, topk_ids, topk_w);
+    else if (epl <= 2) hipLaunchKernelGGL(topk_route_kernel<2>, grid, block, 0, s, logits, T, E_global, top_k, local_begin, E_local, topk_ids, topk_w);
+    else if (epl <= 4) hipLaunchKernelGGL(topk_route_kernel<4>, grid, block, 0, s, logits, T, E_global, top_k, local_begin, E_local, topk_ids, topk_w);
+    else if (epl <= 8) hipLaunchKernelGGL(topk_route_kernel<8>, grid, block, 0, s, logits, T, E_global, top_k, local_begin, E_local, topk_ids, topk_w);
+    else hipLaunchKernelGGL(topk_route_kernel<16>, grid, block, 0, s, logits, T, E_global, top_k, local_begin, E_local, topk_ids, topk_w);
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return fail(MOE_ERR_HIP, "moe_topk_route: launch failed: %s", hipGetErrorString(err));
+    return MOE_OK;
+}

@@ -1,0 +1,123 @@
+"""Thin Python binding of the C ABI (include/moe_apk.h): same names, torch
+tensors in, device pointers and the current HIP stream out.  Every step runs
+in the HIP library; nothing here computes."""
+from __future__ import annotations
+
+import ctypes as C
+from typing import Optional, Sequence
+
+import torch
+
+from . import _lib
+from ._lib import MOE_BF16, MOE_F32, MOE_FP8_E4M3, OpDesc, SchedConfig, check, load_library
+
+
+def _stream(stream: Optional[torch.cuda.Stream]) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return int(s.cuda_stream)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("expected a device tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return t.data_ptr()
+
+
+def act_dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return MOE_BF16
+    if t.dtype in (torch.uint8, getattr(torch, "float8_e4m3fn", torch.uint8)):
+        return MOE_FP8_E4M3
+    raise ValueError(f"unsupported activation dtype {t.dtype}")
+
+
+def moe_topk_route(logits: torch.Tensor, top_k: int, local_begin: int, E_local: int,
+                   topk_ids: Optional[torch.Tensor] = None, topk_w: Optional[torch.Tensor] = None,
+                   stream=None):
+    lib = load_library()
+    T, E = logits.shape
+    if topk_ids is None:
+        topk_ids = torch.empty((T, top_k), dtype=torch.int32, device=logits.device)
+    if topk_w is None:
+        topk_w = torch.empty((T, top_k), dtype=torch.float32, device=logits.device)
+    check(lib.moe_topk_route(_ptr(logits), T, E, top_k, local_begin, E_local, _ptr(topk_ids), _ptr(topk_w),
+                             _stream(stream)), "moe_topk_route")
+    return topk_ids, topk_w
+
+
+def moe_permute_workspace_bytes(T: int, top_k: int, E_local: int) -> int:
+    return int(load_library().moe_permute_workspace_bytes(T, top_k, E_local))
+
+
+def moe_permute(topk_ids: torch.Tensor, E_local: int, x: torch.Tensor, x_scales: Optional[torch.Tensor],
+                row_align: int, capacity: int, counts: torch.Tensor, offsets: torch.Tensor,
+                row_to_assign: torch.Tensor, assign_to_row: torch.Tensor, x_perm: torch.Tensor,
+                x_perm_scales: Optional[torch.Tensor], workspace: torch.Tensor, error_flag: torch.Tensor,
+                stream=None) -> None:
+    lib = load_library()
+    T, k = topk_ids.shape
+    H = x.shape[1]
+    check(lib.moe_permute(_ptr(topk_ids), T, k, E_local, _ptr(x), act_dtype_code(x), _ptr(x_scales), H,
+                          row_align, capacity, _ptr(counts), _ptr(offsets), _ptr(row_to_assign),
+                          _ptr(assign_to_row), _ptr(x_perm), _ptr(x_perm_scales), _ptr(workspace),
+                          _ptr(error_flag), _stream(stream)), "moe_permute")
+
+
+def moe_ffn_row_align(phase: int, dtype: int) -> int:
+    return int(load_library().moe_ffn_row_align(phase, dtype))
+
+
+def _op_array(ops: Sequence[OpDesc]):
+    arr = (OpDesc * len(ops))()
+    for i, o in enumerate(ops):
+        arr[i] = o
+    return arr
+
+
+def moe_ffn_workspace_bytes(ops: Sequence[OpDesc], cfg: SchedConfig) -> int:
+    lib = load_library()
+    return int(lib.moe_ffn_workspace_bytes(_op_array(ops), len(ops), C.byref(cfg)))
+
+
+def moe_grouped_ffn_persistent(ops: Sequence[OpDesc], cfg: SchedConfig, workspace: torch.Tensor,
+                               status_word: torch.Tensor, stream=None) -> None:
+    lib = load_library()
+    check(lib.moe_grouped_ffn_persistent(_op_array(ops), len(ops), C.byref(cfg), _ptr(workspace),
+                                         _ptr(status_word), _stream(stream)), "moe_grouped_ffn_persistent")
+
+
+def moe_combine(y_perm: torch.Tensor, assign_to_row: torch.Tensor, topk_w: torch.Tensor, T: int, top_k: int,
+                y: Optional[torch.Tensor] = None, out_dtype: torch.dtype = torch.bfloat16, stream=None):
+    lib = load_library()
+    H = y_perm.shape[1]
+    if y is None:
+        y = torch.empty((T, H), dtype=out_dtype, device=y_perm.device)
+    code = MOE_BF16 if y.dtype == torch.bfloat16 else MOE_F32 if y.dtype == torch.float32 else None
+    if code is None:
+        raise ValueError("y must be bf16 or f32")
+    check(lib.moe_combine(_ptr(y_perm), _ptr(assign_to_row), _ptr(topk_w), T, top_k, H, _ptr(y), code,
+                          _stream(stream)), "moe_combine")
+    return y
+
+
+def moe_x_moe(counts: Sequence[int], M_t: int) -> int:
+    lib = load_library()
+    arr = (C.c_int32 * len(counts))(*[int(c) for c in counts])
+    return int(lib.moe_x_moe(arr, len(counts), M_t))
+
+
+def moe_decode_quota(q: int, x_moe: int, x_moe_expected: int, q_max: int, round_multiple: int) -> int:
+    return int(load_library().moe_decode_quota(q, x_moe, x_moe_expected, q_max, round_multiple))
+
+
+def status_string(status: int) -> str:
+    return load_library().moe_status_string(status).decode()
+
+
+__all__ = ["moe_topk_route", "moe_permute_workspace_bytes", "moe_permute", "moe_ffn_row_align",
+           "moe_ffn_workspace_bytes", "moe_grouped_ffn_persistent", "moe_combine", "moe_x_moe",
+           "moe_decode_quota", "status_string", "OpDesc", "SchedConfig", "_lib"]

@@ -1,0 +1,200 @@
+"""Buffer plumbing around the four C-ABI calls for a set of MoE operations
+(layers x phases) that share one persistent FFN launch.  Allocates the
+capacity-sized buffers once (device memory comes from torch), then issues
+route -> permute for every op, one moe_grouped_ffn_persistent over all ops,
+and combine for every op, all on one stream.  No arithmetic happens here."""
+from __future__ import annotations
+
+import ctypes as C
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import numpy as np
+import torch
+
+from . import ops as K
+from ._lib import MOE_BF16, MOE_DECODE, MOE_FP8_E4M3, MOE_PREFILL, OpDesc, OpStats, SchedConfig, TraceRec
+
+TRACE_DTYPE = np.dtype([("op", "<i2"), ("stage", "<i2"), ("wg", "<i2"), ("xcc", "<i2"), ("expert", "<i4"),
+                        ("mblk", "<i4"), ("nblk", "<i4"), ("rows", "<i4"), ("t_claim", "<u8"),
+                        ("t_start", "<u8"), ("t_end", "<u8")])
+STATS_DTYPE = np.dtype([("t_ready", "<u8"), ("t_first", "<u8"), ("t_done", "<u8"), ("x_moe", "<i4"),
+                        ("n_tiles", "<i4"), ("quota", "<i4"), ("reserved", "<i4")])
+assert TRACE_DTYPE.itemsize == C.sizeof(TraceRec) and STATS_DTYPE.itemsize == C.sizeof(OpStats)
+
+
+def bf16_tensor(bits: np.ndarray, device) -> torch.Tensor:
+    """bf16 bit patterns (uint16 numpy) -> device bf16 tensor (same bits)."""
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(device)
+
+
+def bits_of(t: torch.Tensor) -> np.ndarray:
+    """device bf16 tensor -> uint16 numpy bit patterns."""
+    return t.detach().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+@dataclass
+class LayerWeights:
+    H: int
+    I: int
+    dtype: int                                  # MOE_BF16 | MOE_FP8_E4M3
+    w_gate_up: torch.Tensor                     # [E_l, 2I, H]
+    w_down: torch.Tensor                        # [E_l, H, I]
+    w_gate_up_scales: Optional[torch.Tensor] = None
+    w_down_scales: Optional[torch.Tensor] = None
+
+    @staticmethod
+    def from_numpy(w: dict, H: int, I: int, device) -> "LayerWeights":
+        if w["w_gate_up"].dtype == np.uint16:
+            return LayerWeights(H, I, MOE_BF16, bf16_tensor(w["w_gate_up"], device), bf16_tensor(w["w_down"], device))
+        return LayerWeights(H, I, MOE_FP8_E4M3, torch.from_numpy(w["w_gate_up"]).to(device),
+                            torch.from_numpy(w["w_down"]).to(device),
+                            torch.from_numpy(w["w_gate_up_scales"]).to(device),
+                            torch.from_numpy(w["w_down_scales"]).to(device))
+
+
+@dataclass
+class OpSpec:
+    phase: int
+    layer: int
+    logits: torch.Tensor                        # [T, E_global] f32, device
+    x: torch.Tensor                             # [T, H] bf16 or uint8 codes, device
+    weights: LayerWeights
+    E_local: int
+    top_k: int
+    local_begin: int = 0
+    x_scales: Optional[torch.Tensor] = None     # [T, H/128] f32 (fp8)
+    release_after_ns: int = -1
+    depends_on_op: int = -1
+    gap_ns: int = 0
+    release_word: Optional[torch.Tensor] = None  # uint32 tensor (device or pinned host)
+
+
+@dataclass
+class OpBuffers:
+    spec: OpSpec
+    T: int
+    capacity: int
+    row_align: int
+    topk_ids: torch.Tensor
+    topk_w: torch.Tensor
+    counts: torch.Tensor
+    offsets: torch.Tensor
+    row_to_assign: torch.Tensor
+    assign_to_row: torch.Tensor
+    x_perm: torch.Tensor
+    x_perm_scales: Optional[torch.Tensor]
+    h: torch.Tensor
+    h_scales: Optional[torch.Tensor]
+    y_perm: torch.Tensor
+    y: torch.Tensor
+    perm_ws: torch.Tensor
+    done_word: torch.Tensor
+
+
+class MoEPipeline:
+    def __init__(self, specs: List[OpSpec], n_workgroups: int = 0, decode_quota_wg: int = 64,
+                 decode_quota_max_wg: int = 0, x_moe_expected: int = 0, round_multiple: int = 8,
+                 trace_capacity: int = 0, spin_limit: int = 0, abort_word: Optional[torch.Tensor] = None,
+                 y_dtype: torch.dtype = torch.bfloat16):
+        if not specs:
+            raise ValueError("no operations")
+        self.device = specs[0].logits.device
+        dev = self.device
+        self.bufs: List[OpBuffers] = []
+        for s in specs:
+            T = s.logits.shape[0]
+            H, I = s.weights.H, s.weights.I
+            fp8 = s.weights.dtype == MOE_FP8_E4M3
+            ra = K.moe_ffn_row_align(s.phase, s.weights.dtype)
+            if ra <= 0:
+                raise ValueError(f"no FFN tile class for phase={s.phase} dtype={s.weights.dtype}")
+            cap = T * min(s.top_k, s.E_local) + s.E_local * (ra - 1)
+            act = torch.uint8 if fp8 else torch.bfloat16
+            self.bufs.append(OpBuffers(
+                spec=s, T=T, capacity=cap, row_align=ra,
+                topk_ids=torch.empty((T, s.top_k), dtype=torch.int32, device=dev),
+                topk_w=torch.empty((T, s.top_k), dtype=torch.float32, device=dev),
+                counts=torch.zeros(s.E_local, dtype=torch.int32, device=dev),
+                offsets=torch.zeros(s.E_local + 1, dtype=torch.int32, device=dev),
+                row_to_assign=torch.full((cap,), -1, dtype=torch.int32, device=dev),
+                assign_to_row=torch.empty((T * s.top_k,), dtype=torch.int32, device=dev),
+                x_perm=torch.zeros((cap, H), dtype=act, device=dev),
+                x_perm_scales=torch.zeros((cap, H // 128), dtype=torch.float32, device=dev) if fp8 else None,
+                h=torch.zeros((cap, I), dtype=act, device=dev),
+                h_scales=torch.zeros((cap, I // 128), dtype=torch.float32, device=dev) if fp8 else None,
+                y_perm=torch.zeros((cap, H), dtype=torch.bfloat16, device=dev),
+                y=torch.empty((T, H), dtype=y_dtype, device=dev),
+                perm_ws=torch.empty((max(1, K.moe_permute_workspace_bytes(T, s.top_k, s.E_local)),),
+                                    dtype=torch.uint8, device=dev),
+                done_word=torch.zeros(1, dtype=torch.int32, device=dev),
+            ))
+        self.error_flag = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.status = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.trace_capacity = trace_capacity
+        self.trace = torch.zeros((max(1, trace_capacity) * TRACE_DTYPE.itemsize,), dtype=torch.uint8, device=dev)
+        self.stats = torch.zeros((len(specs) * STATS_DTYPE.itemsize,), dtype=torch.uint8, device=dev)
+        self.abort_word = abort_word
+        self.cfg = SchedConfig(n_workgroups=n_workgroups, decode_quota_wg=decode_quota_wg,
+                               decode_quota_max_wg=decode_quota_max_wg, x_moe_expected=x_moe_expected,
+                               round_multiple=round_multiple,
+                               abort_word=abort_word.data_ptr() if abort_word is not None else None,
+                               trace=self.trace.data_ptr() if trace_capacity > 0 else None,
+                               trace_capacity=trace_capacity, op_stats=self.stats.data_ptr(),
+                               spin_limit=spin_limit)
+        self.descs = [self._desc(i, b) for i, b in enumerate(self.bufs)]
+        self.ffn_ws = torch.zeros((K.moe_ffn_workspace_bytes(self.descs, self.cfg),), dtype=torch.uint8, device=dev)
+
+    @staticmethod
+    def _desc(i: int, b: OpBuffers) -> OpDesc:
+        s, w = b.spec, b.spec.weights
+        p = lambda t: None if t is None else t.data_ptr()  # noqa: E731
+        return OpDesc(phase=s.phase, layer=s.layer, E_local=s.E_local, H=w.H, I=w.I, capacity=b.capacity,
+                      row_align=b.row_align, dtype=w.dtype, counts=p(b.counts), offsets=p(b.offsets),
+                      x_perm=p(b.x_perm), x_perm_scales=p(b.x_perm_scales), w_gate_up=p(w.w_gate_up),
+                      w_gate_up_scales=p(w.w_gate_up_scales), w_down=p(w.w_down),
+                      w_down_scales=p(w.w_down_scales), h=p(b.h), h_scales=p(b.h_scales), y_perm=p(b.y_perm),
+                      release_word=p(s.release_word), release_after_ns=s.release_after_ns,
+                      depends_on_op=s.depends_on_op, gap_ns=s.gap_ns, done_word=p(b.done_word))
+
+    # ---------------------------------------------------------------- the four calls
+    def route(self, stream=None):
+        for b in self.bufs:
+            s = b.spec
+            K.moe_topk_route(s.logits, s.top_k, s.local_begin, s.E_local, b.topk_ids, b.topk_w, stream)
+
+    def permute(self, stream=None):
+        for b in self.bufs:
+            s = b.spec
+            K.moe_permute(b.topk_ids, s.E_local, s.x, s.x_scales, b.row_align, b.capacity, b.counts, b.offsets,
+                          b.row_to_assign, b.assign_to_row, b.x_perm, b.x_perm_scales, b.perm_ws,
+                          self.error_flag, stream)
+
+    def ffn(self, stream=None):
+        K.moe_grouped_ffn_persistent(self.descs, self.cfg, self.ffn_ws, self.status, stream)
+
+    def combine(self, stream=None):
+        for b in self.bufs:
+            K.moe_combine(b.y_perm, b.assign_to_row, b.topk_w, b.T, b.spec.top_k, b.y, stream=stream)
+
+    def run(self, stream=None):
+        self.route(stream)
+        self.permute(stream)
+        self.ffn(stream)
+        self.combine(stream)
+
+    # ---------------------------------------------------------------- read-back helpers
+    def statuses(self):
+        return int(self.error_flag.item()), int(self.status.item())
+
+    def trace_records(self) -> np.ndarray:
+        n = min(self.trace_capacity, int(self.ffn_ws[16:20].view(torch.int32).item()))
+        raw = self.trace[: n * TRACE_DTYPE.itemsize].cpu().numpy()
+        return raw.view(TRACE_DTYPE)
+
+    def kernel_t0(self) -> int:
+        """Device wall-clock tick at which the last persistent launch started."""
+        return int(self.ffn_ws[:8].view(torch.int64).item())
+
+    def op_stats(self) -> np.ndarray:
+        return self.stats.cpu().numpy().view(STATS_DTYPE)

@@ -1,0 +1,174 @@
+"""The persistent kernel's scheduler, observed through its per-tile trace and
+per-op statistics: every tile runs exactly once (Eq. (3) tile counts),
+GEMM-2 tiles start after their row tile's GEMM-1 tiles committed, ops start
+only after their release condition, lone phases use every workgroup, the
+decode quota holds under contention, results are bitwise independent of the
+schedule, and abort / never-released ops end cleanly (forced from the host
+with a small spin limit; every wait in the kernel is bounded)."""
+import numpy as np
+import pytest
+
+import oracle
+from _helpers import layer_specs
+from workload import CONFIGS, custom_config, make_layer
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+TICK_NS = 10.0   # 100 MHz device wall clock
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2607_18002_amd import load_library
+    load_library()
+    return torch.device("cuda:0")
+
+
+def _mixed_cfg():
+    return custom_config(2, cfg_id=401, H=512, I=512, prefill_tokens=2048, decode_tokens=256, E_global=64,
+                         E_local=16, top_k=4, zipf_s=(1.1,))
+
+
+def _pipe(dev, specs, **kw):
+    from paper_2607_18002_amd.pipeline import MoEPipeline
+    p = MoEPipeline(specs, **kw)
+    p.run()
+    torch.cuda.synchronize()
+    return p
+
+
+def _tiles_per_op(pipe, i):
+    b = pipe.bufs[i]
+    counts = b.counts.cpu().numpy()
+    H, I = b.spec.weights.H, b.spec.weights.I
+    bn = 256 if b.spec.phase == 0 else 128
+    xm = oracle.x_moe(counts, b.row_align)
+    return xm, xm * (I // (bn // 2)) + xm * (H // bn)
+
+
+def test_every_tile_exactly_once_and_dependencies(dev):
+    cfg = _mixed_cfg()
+    specs, lay, _ = layer_specs(cfg, 0, dev)
+    pipe = _pipe(dev, specs, trace_capacity=1 << 16)
+    assert pipe.statuses() == (0, 0)
+    tr = pipe.trace_records()
+    st = pipe.op_stats()
+    for i in range(len(specs)):
+        xm, ntiles = _tiles_per_op(pipe, i)
+        mine = tr[tr["op"] == i]
+        assert st["x_moe"][i] == xm                           # Eq. (3) on the device
+        assert st["n_tiles"][i] == ntiles == len(mine)
+        keys = set(zip(mine["stage"], mine["expert"], mine["mblk"], mine["nblk"]))
+        assert len(keys) == len(mine), "a tile ran twice"
+        for (e, mb) in set(zip(mine["expert"], mine["mblk"])):
+            g1 = mine[(mine["stage"] == 1) & (mine["expert"] == e) & (mine["mblk"] == mb)]
+            g2 = mine[(mine["stage"] == 2) & (mine["expert"] == e) & (mine["mblk"] == mb)]
+            assert len(g1) and len(g2)
+            assert g2["t_start"].min() >= g1["t_end"].max(), "GEMM-2 started before its GEMM-1 row tile committed"
+        assert np.all(mine["t_claim"] >= st["t_ready"][i])
+        assert st["t_done"][i] == mine["t_end"].max()
+        assert np.all(mine["t_start"] <= mine["t_end"])
+
+
+def test_release_delay_and_layer_dependency(dev):
+    """Decode released 10 us after the start, later layers after the previous
+    layer of the same phase is done plus a gap."""
+    cfg = custom_config(2, cfg_id=402, H=512, I=512, prefill_tokens=1024, decode_tokens=128, E_global=64,
+                        E_local=16, top_k=4, zipf_s=(1.1, 0.8), n_layers=2)
+    specs = []
+    for layer in range(2):
+        ready = {"prefill": dict(depends_on_op=(-1 if layer == 0 else 0)),
+                 "decode": dict(release_after_ns=10_000 if layer == 0 else -1,
+                                depends_on_op=(-1 if layer == 0 else 1), gap_ns=20_000)}
+        s, _, _ = layer_specs(cfg, layer, dev, **ready)
+        specs += s
+    pipe = _pipe(dev, specs, trace_capacity=1 << 16)
+    assert pipe.statuses() == (0, 0)
+    st = pipe.op_stats()
+    t0 = pipe.kernel_t0()
+    assert t0 > 0
+    assert st["t_ready"][0] >= t0
+    assert st["t_ready"][1] >= t0 + int(10_000 / TICK_NS)                    # decode layer 0: 10 us after start
+    assert st["t_ready"][2] >= st["t_done"][0]                               # prefill layer 1 after layer 0
+    assert st["t_ready"][3] >= st["t_done"][1] + int(20_000 / TICK_NS)       # decode layer 1 after gap
+
+
+def test_lone_phase_uses_every_workgroup(dev):
+    cfg = custom_config(2, cfg_id=403, H=1024, I=1024, prefill_tokens=4096, decode_tokens=0, E_global=64,
+                        E_local=16, top_k=8)
+    specs, _, _ = layer_specs(cfg, 0, dev)
+    pipe = _pipe(dev, specs, trace_capacity=1 << 16, decode_quota_wg=64)
+    tr = pipe.trace_records()
+    assert len(np.unique(tr["wg"])) == 256
+    assert set(np.unique(tr["xcc"]).tolist()) == set(range(8))
+
+
+def test_decode_quota_under_contention(dev):
+    """While prefill still has unclaimed tiles, decode tiles run only on
+    workgroups below q'."""
+    cfg = custom_config(2, cfg_id=404, H=1024, I=1024, prefill_tokens=8192, decode_tokens=256, E_global=64,
+                        E_local=16, top_k=8)
+    specs, _, _ = layer_specs(cfg, 0, dev, decode=dict(release_after_ns=5_000))
+    pipe = _pipe(dev, specs, trace_capacity=1 << 17, decode_quota_wg=64)
+    assert pipe.statuses() == (0, 0)
+    tr = pipe.trace_records()
+    st = pipe.op_stats()
+    assert st["quota"][1] == 64
+    last_prefill_claim = tr[tr["op"] == 0]["t_claim"].max()
+    dec = tr[(tr["op"] == 1) & (tr["t_claim"] + 500 < last_prefill_claim)]   # 5 us margin
+    assert len(dec) > 0
+    assert dec["wg"].max() < 64
+
+
+def test_results_independent_of_schedule(dev):
+    cfg = _mixed_cfg()
+    outs = []
+    for kw in (dict(), dict(decode_quota_wg=0), dict(decode_quota_wg=256, decode_quota_max_wg=256),
+               dict(n_workgroups=24)):
+        specs, _, _ = layer_specs(cfg, 0, dev, decode=dict(release_after_ns=3_000))
+        pipe = _pipe(dev, specs, **kw)
+        assert pipe.statuses() == (0, 0)
+        outs.append([b.y.view(torch.int16).cpu().numpy().copy() for b in pipe.bufs])
+    for o in outs[1:]:
+        for a, b in zip(outs[0], o):
+            np.testing.assert_array_equal(a, b)
+
+
+def test_adaptive_quota_eq4(dev):
+    cfg = _mixed_cfg()
+    specs, _, _ = layer_specs(cfg, 0, dev)
+    pipe = _pipe(dev, specs, decode_quota_wg=64, x_moe_expected=4, decode_quota_max_wg=128, round_multiple=8)
+    st = pipe.op_stats()
+    xm = int(st["x_moe"][1])
+    assert st["quota"][1] == oracle.decode_quota(64, xm, 4, 128, 8)
+
+
+def test_abort_word_stops_the_kernel(dev):
+    cfg = _mixed_cfg()
+    abort = torch.ones(1, dtype=torch.int32, device=dev)
+    specs, _, _ = layer_specs(cfg, 0, dev)
+    pipe = _pipe(dev, specs, abort_word=abort)
+    assert pipe.statuses()[1] == -5
+
+
+def test_never_released_op_times_out(dev):
+    cfg = _mixed_cfg()
+    never = torch.zeros(1, dtype=torch.int32, device=dev)
+    specs, _, _ = layer_specs(cfg, 0, dev, decode=dict(release_word=never))
+    pipe = _pipe(dev, specs, spin_limit=20000, trace_capacity=1 << 16)
+    assert pipe.statuses()[1] == -6
+    st = pipe.op_stats()
+    assert st["t_done"][0] > 0                                 # the released prefill op still completed
+    assert st["t_ready"][1] == 0
+
+
+def test_release_word_set_before_launch(dev):
+    cfg = _mixed_cfg()
+    word = torch.ones(1, dtype=torch.int32, device=dev)
+    specs, lay, _ = layer_specs(cfg, 0, dev, decode=dict(release_word=word))
+    pipe = _pipe(dev, specs)
+    assert pipe.statuses() == (0, 0)
+    assert int(pipe.bufs[1].done_word.item()) == 1 and int(pipe.bufs[0].done_word.item()) == 1

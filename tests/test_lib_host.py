@@ -1,0 +1,106 @@
+"""CPU-only checks of the C-ABI library: it loads, exports every symbol the
+header declares, its struct layouts match the binding, its host helpers agree
+with the oracle's Eq. (3)/(4), and argument errors are reported before any
+device work."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "moe_apk.h")
+LIB = os.path.join(ROOT, "paper_2607_18002_amd", "libmoe_apk.so")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="library not built (run __graft_entry__.build())")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*[A-Za-z_][\w\s\*]*?\b(moe_\w+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_the_four_calls():
+    names = declared_functions()
+    for n in ("moe_topk_route", "moe_permute", "moe_grouped_ffn_persistent", "moe_combine"):
+        assert n in names
+
+
+def test_exports_every_declared_symbol():
+    lib = C.CDLL(LIB)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_binding_layouts_match_library():
+    from paper_2607_18002_amd import _lib
+    lib = _lib.load_library()
+    assert lib.moe_abi_sizeof(0) == C.sizeof(_lib.OpDesc)
+    assert lib.moe_abi_sizeof(1) == C.sizeof(_lib.SchedConfig)
+    assert lib.moe_abi_sizeof(2) == C.sizeof(_lib.TraceRec) == 48
+    assert lib.moe_abi_sizeof(3) == C.sizeof(_lib.OpStats) == 40
+    assert lib.moe_abi_sizeof(9) == 0
+
+
+def test_status_strings():
+    from paper_2607_18002_amd import ops
+    assert ops.status_string(0) == "MOE_OK"
+    assert ops.status_string(-3) == "MOE_ERR_CAPACITY"
+    assert ops.status_string(-7) == "MOE_ERR_BAD_EXPERT"
+
+
+def test_x_moe_matches_oracle():
+    from paper_2607_18002_amd import ops
+    rng = np.random.default_rng(3)
+    for _ in range(50):
+        counts = rng.integers(0, 700, size=int(rng.integers(1, 40)))
+        counts[rng.random(len(counts)) < 0.2] = 0
+        mt = int(rng.choice([1, 16, 32, 128, 256]))
+        assert ops.moe_x_moe(counts, mt) == oracle.x_moe(counts, mt)
+
+
+def test_decode_quota_matches_oracle():
+    from paper_2607_18002_amd import ops
+    rng = np.random.default_rng(4)
+    for _ in range(500):
+        q = int(rng.integers(0, 257))
+        x = int(rng.integers(0, 400))
+        xs = int(rng.integers(-2, 300))
+        qmax = int(rng.integers(1, 257))
+        c = int(rng.choice([1, 2, 8, 16]))
+        assert ops.moe_decode_quota(q, x, xs, qmax, c) == oracle.decode_quota(q, x, xs, qmax, c)
+
+
+def test_row_align_and_workspace_queries():
+    from paper_2607_18002_amd import _lib, ops
+    assert ops.moe_ffn_row_align(_lib.MOE_PREFILL, _lib.MOE_BF16) == 128
+    assert ops.moe_ffn_row_align(_lib.MOE_DECODE, _lib.MOE_BF16) == 128
+    assert ops.moe_ffn_row_align(7, _lib.MOE_BF16) < 0
+    assert ops.moe_permute_workspace_bytes(16384, 8, 32) >= 32 * 32 * 4
+    d = _lib.OpDesc(capacity=69600, row_align=128)
+    cfg = _lib.SchedConfig()
+    assert ops.moe_ffn_workspace_bytes([d], cfg) >= 2 * (69600 // 128) * 4
+
+
+def test_argument_errors_before_any_launch():
+    """Invalid arguments are rejected on the host with a message and never
+    reach the device (this container has no GPU)."""
+    from paper_2607_18002_amd import _lib
+    lib = _lib.load_library()
+    assert lib.moe_topk_route(None, -1, 8, 2, 0, 8, None, None, None) == _lib.MOE_ERR_INVALID_ARG
+    assert b"T=-1" in lib.moe_last_error()
+    assert lib.moe_topk_route(None, 4, 2000, 2, 0, 8, None, None, None) == _lib.MOE_ERR_UNSUPPORTED
+    assert lib.moe_topk_route(None, 4, 8, 9, 0, 8, None, None, None) == _lib.MOE_ERR_INVALID_ARG
+    assert lib.moe_topk_route(None, 0, 8, 2, 0, 8, None, None, None) == _lib.MOE_OK     # T == 0: nothing to do
+    args = [None, 10, 8, 4, None, _lib.MOE_BF16, None, 256, 128, 10] + [None] * 9
+    assert lib.moe_permute(*args) == _lib.MOE_ERR_CAPACITY          # capacity 10 < 10*4 + 4*127
+    args[7] = 100                                                    # H not a multiple of 128
+    assert lib.moe_permute(*args) == _lib.MOE_ERR_UNSUPPORTED
+    assert lib.moe_combine(None, None, None, 4, 2, 12, None, _lib.MOE_BF16, None) == _lib.MOE_ERR_UNSUPPORTED
+    assert lib.moe_combine(None, None, None, 4, 2, 16, None, 7, None) == _lib.MOE_ERR_UNSUPPORTED
+    assert lib.moe_grouped_ffn_persistent(None, 1, None, None, None, None) == _lib.MOE_ERR_INVALID_ARG
