@@ -1,0 +1,259 @@
+#!/usr/bin/env python3
+"""Benchmark of the routed-expert MoE hot path on one MI355X.
+
+A step is one pass of the whole path over one batch: moe_topk_route and
+moe_permute for every operation, ONE moe_grouped_ffn_persistent launch over
+all operations, and moe_combine for every operation.  The default workload is
+the mixed prefill+decode configuration: 4 layers x (8192 prefill + 1024 decode
+tokens), 32 of 256 experts local, top-8, hidden 3072, expert intermediate
+1536, bf16, in one persistent launch; decode layer 0 is released 10 us after
+the launch starts, each later layer of a phase when that phase's previous
+layer is done (+20 us for decode), decode quota 64 of 256 workgroups.
+
+Prints ONE JSON line.  value = routed-expert TFLOP/s of the whole step
+(6*H*I flop per local routed row).  roofline = the persistent FFN kernel
+against the HBM bound (algorithmic bytes: each op's active expert weights
+once plus x_perm in and y_perm out), timed with HIP events on its stream.
+cpu_baseline = the float64 CPU oracle on a bounded sample of the same
+workload, on this host's cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0}
+TICK_NS = 10.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=4, help="workload configuration (1-5); default 4")
+    ap.add_argument("--quota", type=int, default=64, help="decode quota q in workgroups")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def build_specs(cfg, dev):
+    from paper_2607_18002_amd import MOE_DECODE, MOE_PREFILL
+    from paper_2607_18002_amd.pipeline import LayerWeights, OpSpec, bf16_tensor
+    from workload import make_layer
+    import torch
+
+    specs, layers = [], []
+    prev = {"prefill": -1, "decode": -1}
+    for layer in range(cfg.n_layers):
+        lay = make_layer(cfg, layer)
+        w = LayerWeights.from_numpy(lay.weights, cfg.H, cfg.I, dev)
+        for ph in lay.phases:
+            x = bf16_tensor(ph.x, dev) if ph.x.dtype == np.uint16 else torch.from_numpy(ph.x).to(dev)
+            xs = torch.from_numpy(ph.x_scales).to(dev) if ph.x_scales is not None else None
+            decode = ph.phase == "decode"
+            ready = dict(release_after_ns=-1, depends_on_op=prev[ph.phase], gap_ns=0)
+            if decode and layer == 0 and cfg.prefill_tokens > 0:
+                ready["release_after_ns"] = 10_000
+            if decode and layer > 0:
+                ready["gap_ns"] = 20_000
+            prev[ph.phase] = len(specs)
+            specs.append(OpSpec(phase=MOE_DECODE if decode else MOE_PREFILL, layer=layer,
+                                logits=torch.from_numpy(ph.logits).to(dev), x=x, x_scales=xs, weights=w,
+                                E_local=cfg.E_local, top_k=cfg.top_k, local_begin=cfg.local_begin, **ready))
+        layers.append(lay)
+        del lay
+    return specs, layers
+
+
+def algorithmic_work(pipe, cfg):
+    """flops and HBM bytes the method itself must move, per persistent launch."""
+    b_w = 1 if cfg.dtype == "fp8" else 2
+    b_x = 1 if cfg.dtype == "fp8" else 2
+    flops = 0.0
+    bytes_ = 0.0
+    rows_total = 0
+    for b in pipe.bufs:
+        counts = b.counts.cpu().numpy()
+        R = int(counts.sum())
+        active = int(np.count_nonzero(counts))
+        rows_total += R
+        flops += 6.0 * cfg.H * cfg.I * R
+        bytes_ += active * 3.0 * cfg.H * cfg.I * b_w + R * cfg.H * (b_x + 2)
+        if cfg.dtype == "fp8":
+            bytes_ += active * 3.0 * (cfg.H // 128) * (cfg.I // 128) * 4 + R * (cfg.H // 128) * 4
+    return flops, bytes_, rows_total
+
+
+def decode_latency(pipe, specs):
+    """Decode latency figures from one traced launch, in microseconds.
+
+    release(op) = the time the op became eligible (launch start + its delay,
+    or its predecessor's completion + gap).  Tile latency = t_end - release;
+    preemption wait = first tile start - release; op latency = last tile end -
+    release."""
+    st = pipe.op_stats()
+    tr = pipe.trace_records()
+    t0 = pipe.kernel_t0()
+    lat, waits, op_lat = [], [], []
+    for i, s in enumerate(specs):
+        if s.phase != 1:
+            continue
+        if s.release_after_ns >= 0:
+            rel = t0 + s.release_after_ns / TICK_NS
+        elif s.depends_on_op >= 0:
+            rel = float(st["t_done"][s.depends_on_op]) + s.gap_ns / TICK_NS
+        else:
+            rel = float(t0)
+        mine = tr[tr["op"] == i]
+        if len(mine) == 0:
+            continue
+        us = lambda t: (t.astype(np.float64) - rel) * TICK_NS / 1000.0  # noqa: E731
+        lat.extend(us(mine["t_end"]).tolist())
+        waits.append(float(us(mine["t_start"]).min()))
+        op_lat.append(float(us(mine["t_end"]).max()))
+    if not lat:
+        return None
+    pre = np.isin(tr["op"], [i for i, s in enumerate(specs) if s.phase == 0])
+    ptd = (tr["t_end"][pre].astype(np.float64) - tr["t_start"][pre]) * TICK_NS / 1000.0
+    return {"tile_p50_us": round(float(np.percentile(lat, 50)), 2),
+            "tile_p99_us": round(float(np.percentile(lat, 99)), 2),
+            "preempt_wait_max_us": round(max(waits), 2), "preempt_wait_mean_us": round(float(np.mean(waits)), 2),
+            "decode_op_latency_us": [round(v, 1) for v in op_lat],
+            "prefill_tile_max_us": round(float(ptd.max()), 2) if len(ptd) else None,
+            "prefill_tile_p50_us": round(float(np.percentile(ptd, 50)), 2) if len(ptd) else None}
+
+
+def cpu_baseline(cfg, layers):
+    """The oracle as it stands, on a bounded sample of the same workload:
+    every operation of layer 0 (all of its tokens, every step of the path)."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        cores = len(os.sched_getaffinity(0))
+    lay = layers[0]
+    flops, rows, dt = 0.0, 0, 0.0
+    for ph in lay.phases:
+        t = time.perf_counter()
+        res = oracle.moe_local_share(ph.logits, ph.x, lay.weights, cfg.top_k, cfg.local_begin, cfg.E_local, 128,
+                                     x_scales=ph.x_scales)
+        dt += time.perf_counter() - t
+        R = int(res["perm"].counts.sum())
+        rows += R
+        flops += 6.0 * cfg.H * cfg.I * R
+    desc = " + ".join(f"{ph.T} {ph.phase}" for ph in lay.phases)
+    return {"value": round(flops / dt / 1e12, 5), "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"layer 0 of {cfg.n_layers}: {desc} tokens ({rows} local rows), every step, float64 numpy, "
+                      f"{dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one MI355X: this path has no multi-GPU mode (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2607_18002_amd import load_library
+    from paper_2607_18002_amd.pipeline import MoEPipeline
+    from workload import CONFIGS
+
+    load_library()
+    dev = torch.device("cuda:0")
+    cfg = CONFIGS[args.config]
+    t_gen = time.perf_counter()
+    specs, layers = build_specs(cfg, dev)
+    t_gen = time.perf_counter() - t_gen
+    pipe = MoEPipeline(specs, decode_quota_wg=args.quota)
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        pipe.run()
+    torch.cuda.synchronize()
+    err, status = pipe.statuses()
+    if err or status:
+        raise SystemExit(f"device status after warmup: permute={err} ffn={status}")
+
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        pipe.route()
+        pipe.permute()
+        ev[i][0].record(stream)
+        pipe.ffn()
+        ev[i][1].record(stream)
+        pipe.combine()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ffn_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    ms_step = wall * 1000.0 / args.steps
+
+    flops, abytes, rows = algorithmic_work(pipe, cfg)
+    # one more launch with the per-tile trace for the decode latency figures
+    traced = MoEPipeline(specs, decode_quota_wg=args.quota, trace_capacity=1 << 18)
+    traced.run()
+    torch.cuda.synchronize()
+    lat = decode_latency(traced, specs)
+
+    dtype = cfg.dtype
+    t_mfma = flops / (MFMA_PEAK_TFLOPS[dtype] * 1e12)
+    t_hbm = abytes / (HBM_PEAK_GBS * 1e9)
+    bound = "hbm" if t_hbm >= t_mfma else "mfma"
+    if bound == "hbm":
+        ach = abytes / (ffn_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None}
+    else:
+        ach = flops / (ffn_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": MFMA_PEAK_TFLOPS[dtype], "unit": "TFLOP/s",
+                "frac": round(ach / MFMA_PEAK_TFLOPS[dtype], 4), "traffic": None}
+    roof["kernel"] = "apk_kernel (moe_grouped_ffn_persistent)"
+    roof["kernel_ms"] = round(ffn_ms, 4)
+    roof["alg_bytes"] = abytes
+    roof["alg_flops"] = flops
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, layers)
+
+    out = {
+        "metric": "routed-expert TFLOP/s + HBM GB/s per MI355X (mixed P/D); decode p99 tile latency",
+        "value": round(flops / (ms_step * 1e-3) / 1e12, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f8e4m3" if dtype == "fp8" else "bf16",
+        "data": "synthetic (seeded; random-init expert weights, Zipf-skewed router logits)",
+        "config": {"workload": cfg.name, "config_id": cfg.cfg_id, "layers": cfg.n_layers,
+                   "prefill_tokens": cfg.prefill_tokens, "decode_tokens": cfg.decode_tokens,
+                   "experts_local": cfg.E_local, "experts_global": cfg.E_global, "top_k": cfg.top_k,
+                   "hidden": cfg.H, "intermediate": cfg.I, "decode_quota_wg": args.quota,
+                   "local_rows": rows},
+        "hbm_gbps_alg": round(abytes / (ffn_ms * 1e-3) / 1e9, 1),
+        "ffn_tflops": round(flops / (ffn_ms * 1e-3) / 1e12, 2),
+        "decode_tile_latency": lat,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "input_gen_s": round(t_gen, 1),
+    }
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -207,6 +207,13 @@ typedef struct moe_sched_config {
  * row_align for such an op must equal it.  Returns <= 0 if unsupported. */
 int32_t moe_ffn_row_align(moe_phase_t phase, moe_dtype_t dtype);
 
+/* Output tile of the FFN kernel for ops of this phase and dtype: *bm rows
+ * (== moe_ffn_row_align), *bn columns (GEMM-1: bn/2 gate + bn/2 up columns,
+ * i.e. bn/2 columns of h; GEMM-2: bn columns of y_perm), *bk the K step.
+ * An op with footprint x_moe (Eq. 3) runs x_moe*(I/(bn/2)) GEMM-1 tiles and
+ * x_moe*(H/bn) GEMM-2 tiles.  Returns MOE_OK or MOE_ERR_UNSUPPORTED. */
+moe_status_t moe_ffn_tile_shape(moe_phase_t phase, moe_dtype_t dtype, int32_t* bm, int32_t* bn, int32_t* bk);
+
 /* Device scratch needed by one persistent launch over these ops (host array). */
 size_t moe_ffn_workspace_bytes(const moe_op_desc* ops, int32_t n_ops, const moe_sched_config* cfg);
 

@@ -28,8 +28,8 @@ namespace {
 
 using namespace moeapk;
 
-using ShapeP = TileShape<128, 256, 64, 2, 2>;    // prefill: 128 x 256 tile, K step 64
-using ShapeD = TileShape<128, 128, 128, 2, 2>;   // decode : 128 x 128 tile, K step 128 (more bytes in flight)
+using ShapeP = TileShape<128, 256, 64>;    // prefill: 128 x 256 tile, K step 64
+using ShapeD = TileShape<128, 256, 64>;    // decode : 128 x 256 tile, K step 64
 constexpr int kLdsBytes = ShapeP::LDS > ShapeD::LDS ? ShapeP::LDS : ShapeD::LDS;
 constexpr int kRowAlign = 128;                   // M_t of both bf16 classes
 
@@ -119,29 +119,23 @@ __global__ __launch_bounds__(256) void apk_init_kernel(const InitArgs a) {
 }
 
 // ----------------------------------------------------------------------------- tiles
-__device__ __forceinline__ void run_tile(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds) {
+template <class S>
+__device__ __forceinline__ void run_tile_cls(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds) {
     const long H = op.H, I = op.I;
-    if (op.cls == CLS_P_BF16) {
-        if (stage == 1) {
-            gemm_tile_bf16<ShapeP, true>(op.x + row0 * H, (int)H, rows32,
-                                         op.wgu + (long)e * 2 * I * H + (long)nb * (ShapeP::BN / 2) * H, (int)H, I * H,
-                                         (int)H, op.h + row0 * I + nb * (ShapeP::BN / 2), (int)I, lds);
-        } else {
-            gemm_tile_bf16<ShapeP, false>(op.h + row0 * I, (int)I, rows32,
-                                          op.wd + (long)e * H * I + (long)nb * ShapeP::BN * I, (int)I, 0, (int)I,
-                                          op.y + row0 * H + nb * ShapeP::BN, (int)H, lds);
-        }
+    if (stage == 1) {
+        gemm_tile_bf16_rows<S, true>(rows32, op.x + row0 * H, (int)H,
+                                     op.wgu + (long)e * 2 * I * H + (long)nb * (S::BN / 2) * H, (int)H, (int)I,
+                                     (int)H, op.h + row0 * I + nb * (S::BN / 2), (int)I, lds);
     } else {
-        if (stage == 1) {
-            gemm_tile_bf16<ShapeD, true>(op.x + row0 * H, (int)H, rows32,
-                                         op.wgu + (long)e * 2 * I * H + (long)nb * (ShapeD::BN / 2) * H, (int)H, I * H,
-                                         (int)H, op.h + row0 * I + nb * (ShapeD::BN / 2), (int)I, lds);
-        } else {
-            gemm_tile_bf16<ShapeD, false>(op.h + row0 * I, (int)I, rows32,
-                                          op.wd + (long)e * H * I + (long)nb * ShapeD::BN * I, (int)I, 0, (int)I,
-                                          op.y + row0 * H + nb * ShapeD::BN, (int)H, lds);
-        }
+        gemm_tile_bf16_rows<S, false>(rows32, op.h + row0 * I, (int)I, op.wd + (long)e * H * I + (long)nb * S::BN * I,
+                                      (int)I, 0, (int)I, op.y + row0 * H + nb * S::BN, (int)H, lds);
     }
+}
+
+__device__ __forceinline__ void run_tile(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds) {
+    // Both bf16 classes currently share one tile shape.
+    static_assert(ShapeP::BM == ShapeD::BM && ShapeP::BN == ShapeD::BN && ShapeP::BK == ShapeD::BK, "one shape");
+    run_tile_cls<ShapeP>(op, stage, row0, rows32, nb, e, lds);
 }
 
 // ----------------------------------------------------------------------------- scheduler
@@ -421,6 +415,17 @@ extern "C" int32_t moe_ffn_row_align(moe_phase_t phase, moe_dtype_t dtype) {
     if (phase != MOE_PREFILL && phase != MOE_DECODE) return -1;
     if (dtype != MOE_BF16) return -2;
     return kRowAlign;
+}
+
+extern "C" moe_status_t moe_ffn_tile_shape(moe_phase_t phase, moe_dtype_t dtype, int32_t* bm, int32_t* bn,
+                                           int32_t* bk) {
+    if ((phase != MOE_PREFILL && phase != MOE_DECODE) || dtype != MOE_BF16)
+        return moeapk_host::fail(MOE_ERR_UNSUPPORTED, "moe_ffn_tile_shape: phase %d dtype %d", phase, dtype);
+    const ClassInfo ci = class_info(phase == MOE_PREFILL ? CLS_P_BF16 : CLS_D_BF16);
+    if (bm) *bm = kRowAlign;
+    if (bn) *bn = ci.bn;
+    if (bk) *bk = ci.bk;
+    return MOE_OK;
 }
 
 extern "C" size_t moe_ffn_workspace_bytes(const moe_op_desc* ops, int32_t n_ops, const moe_sched_config* cfg) {

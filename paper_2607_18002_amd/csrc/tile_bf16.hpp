@@ -1,157 +1,172 @@
 // bf16 grouped-GEMM tile on gfx950 MFMA (v_mfma_f32_32x32x16_bf16).
 //
-// One 256-thread workgroup (4 waves in a WM x WN grid) computes a BM x BN
-// output tile over the full K in BK steps.  Both operands are K-contiguous
-// (A = activation rows, B = weight rows), so every global load is a 16-byte
-// vector of one row and every MFMA operand is one 16-byte LDS read.
+// One 256-thread workgroup computes a BM x BN output tile over the full K.
+// The four waves split the BN columns (BN/4 each) and all share the BM rows:
+//  * B (weight rows, K-contiguous) is private to a wave, so it streams from
+//    global memory straight into MFMA operand registers, double-buffered
+//    (two K steps in flight per wave), with no LDS round trip;
+//  * A (activation rows, shared by the four waves) is staged through LDS,
+//    double-buffered, with rows padded by 16 bytes so an operand read is free
+//    of bank conflicts.
+// K order inside a K step: lanes 0-31 take elements [0, BK/2) and lanes 32-63
+// take [BK/2, BK) across the BK/16 MFMAs, so each lane's B reads of a K step
+// are one contiguous BK-byte run (a full cache line at BK = 64 bf16).  A and B
+// use the same order; the sum over K is unchanged.
 //
-// Pipeline: global -> registers for step s+1 is issued before the MFMAs of
-// step s; the registers are written to the other LDS buffer afterwards; one
-// barrier per K step.  LDS rows are padded by 16 bytes so the 32 rows an MFMA
-// operand spans fall on distinct banks.
-//
-// GLU tiles (GEMM-1) load BN/2 gate rows followed by BN/2 up rows of the
-// [2I, H] gate/up matrix; each wave's gate and up accumulators cover the same
-// output columns, so the SiLU(g)*u epilogue is lane-local.  Row blocks of 32
-// that lie beyond the tile's valid rows are neither loaded nor computed.
+// GLU tiles (GEMM-1) take BN/2 gate rows and BN/2 up rows of the [2I, H]
+// gate/up matrix; every wave holds a gate block and the up block of the same
+// columns, so h = silu(g) * u is formed lane-locally in the epilogue.
+// MACT, the number of 32-row blocks with valid rows, is a template argument:
+// the K loop is branch-free and blocks past the valid rows cost nothing.
 #pragma once
 
 #include "common.hpp"
 
 namespace moeapk {
 
-template <int BM_, int BN_, int BK_, int WM_, int WN_>
+template <int BM_, int BN_, int BK_>
 struct TileShape {
-    static constexpr int BM = BM_, BN = BN_, BK = BK_, WM = WM_, WN = WN_;
-    static constexpr int WTM = BM / WM;              // rows per wave
-    static constexpr int MB = WTM / 32;              // 32-row MFMA blocks per wave
-    static constexpr int NBW = BN / WN / 32;         // 32-column MFMA blocks per wave
-    static constexpr int LDS_ROW = BK * 2 + 16;      // bytes per LDS row
-    static constexpr int A_BYTES = BM * LDS_ROW;
-    static constexpr int B_BYTES = BN * LDS_ROW;
-    static constexpr int STAGE = A_BYTES + B_BYTES;
-    static constexpr int LDS = 2 * STAGE;
-    static constexpr int CPR = BK / 8;               // 16-byte chunks per row and K step
-    static constexpr int CA = BM * CPR / 256;        // A chunks per thread and K step
-    static constexpr int CB = BN * CPR / 256;        // B chunks per thread and K step
-    static_assert(WM * WN == 4, "4 waves");
-    static_assert(MB >= 1 && NBW >= 2 && NBW % 2 == 0, "tile shape");
-    static_assert(CA * 256 == BM * CPR && CB * 256 == BN * CPR, "load split");
+    static constexpr int BM = BM_, BN = BN_, BK = BK_;
+    static constexpr int MB = BM / 32;               // 32-row blocks
+    static constexpr int WCOLS = BN / 4;             // B rows (output columns) per wave
+    static constexpr int NBW = WCOLS / 32;           // 32-column MFMA blocks per wave
+    static constexpr int KK = BK / 16;               // MFMAs along K per K step
+    static constexpr int LDS_ROW = BK * 2 + 16;      // bytes per LDS row of A
+    static constexpr int A_STAGE = BM * LDS_ROW;
+    static constexpr int LDS = 2 * A_STAGE;
+    static constexpr int CPR = BK / 8;               // 16-byte chunks per A row and K step
+    static constexpr int RPP = 256 / CPR;            // A rows loaded per pass of 256 threads
+    static_assert(NBW >= 2 && NBW % 2 == 0, "GLU needs a gate and an up block per wave");
+    static_assert(256 % CPR == 0 && RPP <= 32 && 32 % RPP == 0, "an A load pass stays inside one 32-row block");
 };
 
-// B row (within the tile's BN rows) of the wave's j-th 32-column block.
-template <class S, bool GLU>
-__device__ __forceinline__ int b_block_row(int wn, int j) {
-    if (GLU) {
-        constexpr int half = S::BN / 2, per_wave = half / S::WN, nb2 = S::NBW / 2;
-        return (j < nb2) ? wn * per_wave + 32 * j : half + wn * per_wave + 32 * (j - nb2);
-    }
-    return wn * (S::BN / S::WN) + 32 * j;
+template <class S, int MACT>
+struct TileRegs {
+    static constexpr int CA = MACT * 32 / S::RPP;    // A chunks per thread and K step
+};
+
+template <int CA>
+__device__ __forceinline__ void load_a(u32x4 (&ra)[CA], const char* __restrict__ A, const uint32_t (&aoff)[CA],
+                                       int k0b) {
+#pragma unroll
+    for (int i = 0; i < CA; ++i) ra[i] = *(const u32x4*)(A + aoff[i] + k0b);
 }
 
-// A : tile row 0 at k = 0, row stride lda (elements)
-// rows32 : rows to compute, a multiple of 32 in [32, BM]
-// B : first B row of the tile (GLU: gate row n0), row stride ldb
-// up_off : GLU only, element offset from the gate rows to the up rows
-// out : output tile origin, row stride ldo (bf16)
-template <class S, bool GLU>
-__device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, int lda, int rows32,
-                                               const uint16_t* __restrict__ B, int ldb, long up_off, int K,
+template <int CA>
+__device__ __forceinline__ void store_a(char* buf, const u32x4 (&ra)[CA], const uint32_t (&alds)[CA]) {
+#pragma unroll
+    for (int i = 0; i < CA; ++i) *(u32x4*)(buf + alds[i]) = ra[i];
+}
+
+template <class S>
+__device__ __forceinline__ void load_b(bf16x8 (&rb)[S::NBW][S::KK], const char* __restrict__ B,
+                                       const uint32_t (&boff)[S::NBW], int k0b) {
+#pragma unroll
+    for (int j = 0; j < S::NBW; ++j)
+#pragma unroll
+        for (int kk = 0; kk < S::KK; ++kk) rb[j][kk] = *(const bf16x8*)(B + boff[j] + k0b + kk * 16);
+}
+
+template <class S, int MACT>
+__device__ __forceinline__ void mma_step(f32x16 (&acc)[MACT][S::NBW], const bf16x8 (&rb)[S::NBW][S::KK],
+                                         const char* buf, int lane) {
+    const char* arow = buf + (lane & 31) * S::LDS_ROW + (lane >> 5) * S::BK;   // half-K split: +BK/2 elements
+#pragma unroll
+    for (int kk = 0; kk < S::KK; ++kk) {
+        bf16x8 af[MACT];
+#pragma unroll
+        for (int i = 0; i < MACT; ++i) af[i] = *(const bf16x8*)(arow + i * 32 * S::LDS_ROW + kk * 16);
+#pragma unroll
+        for (int i = 0; i < MACT; ++i)
+#pragma unroll
+            for (int j = 0; j < S::NBW; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], rb[j][kk], acc[i][j], 0, 0, 0);
+    }
+}
+
+// A   : tile row 0 at k = 0, row stride lda elements; rows [0, 32*MACT) are read
+// B   : first B row of the tile (GLU: gate row n0), row stride ldb elements
+// up_rows : GLU only, rows from the gate block to the matching up block (I)
+// out : output tile origin, row stride ldo (bf16); rows [0, 32*MACT) written
+template <class S, bool GLU, int MACT>
+__device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, int lda,
+                                               const uint16_t* __restrict__ B, int ldb, int up_rows, int K,
                                                uint16_t* __restrict__ out, int ldo, char* lds) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave / S::WN, wn = wave % S::WN;
-    int mact = (rows32 - wm * S::WTM) / 32;
-    mact = mact < 0 ? 0 : (mact > S::MB ? S::MB : mact);
+    constexpr int CA = TileRegs<S, MACT>::CA;
+    const int tid = threadIdx.x, lane = tid & 63, wn = tid >> 6;
 
-    int a_goff[S::CA], a_loff[S::CA];
-    bool a_ok[S::CA];
+    uint32_t boff[S::NBW];
 #pragma unroll
-    for (int i = 0; i < S::CA; ++i) {
-        const int idx = tid + 256 * i, r = idx / S::CPR, c = idx % S::CPR;
-        a_ok[i] = r < rows32;
-        a_goff[i] = r * lda + c * 8;
-        a_loff[i] = r * S::LDS_ROW + c * 16;
+    for (int j = 0; j < S::NBW; ++j) {
+        int row;
+        if (GLU) {
+            constexpr int half = S::NBW / 2;
+            const int jj = j < half ? j : j - half;
+            row = wn * (S::WCOLS / 2) + 32 * jj + (lane & 31) + (j < half ? 0 : up_rows);
+        } else {
+            row = wn * S::WCOLS + 32 * j + (lane & 31);
+        }
+        boff[j] = (uint32_t)row * (uint32_t)ldb * 2u + (uint32_t)((lane >> 5) * S::BK);
     }
-    long b_goff[S::CB];
-    int b_loff[S::CB];
+    uint32_t aoff[CA], alds[CA];
 #pragma unroll
-    for (int i = 0; i < S::CB; ++i) {
+    for (int i = 0; i < CA; ++i) {
         const int idx = tid + 256 * i, r = idx / S::CPR, c = idx % S::CPR;
-        long row_off;
-        if (GLU) row_off = (r < S::BN / 2) ? (long)r * ldb : up_off + (long)(r - S::BN / 2) * ldb;
-        else row_off = (long)r * ldb;
-        b_goff[i] = row_off + c * 8;
-        b_loff[i] = S::A_BYTES + r * S::LDS_ROW + c * 16;
+        aoff[i] = (uint32_t)r * (uint32_t)lda * 2u + c * 16;
+        alds[i] = r * S::LDS_ROW + c * 16;
     }
+    const char* Ab = (const char*)A;
+    const char* Bb = (const char*)B;
+    char* lds0 = lds;
+    char* lds1 = lds + S::A_STAGE;
 
-    uint4 ra[S::CA], rb[S::CB];
-    f32x16 acc[S::MB][S::NBW];
+    f32x16 acc[MACT][S::NBW];
 #pragma unroll
-    for (int i = 0; i < S::MB; ++i)
+    for (int i = 0; i < MACT; ++i)
 #pragma unroll
         for (int j = 0; j < S::NBW; ++j)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    auto gload = [&](int k0) {
-#pragma unroll
-        for (int i = 0; i < S::CA; ++i)
-            ra[i] = a_ok[i] ? *(const uint4*)(A + a_goff[i] + k0) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < S::CB; ++i) rb[i] = *(const uint4*)(B + b_goff[i] + k0);
-    };
-    auto sstore = [&](int buf) {
-        char* base = lds + buf * S::STAGE;
-#pragma unroll
-        for (int i = 0; i < S::CA; ++i)
-            if (a_ok[i]) *(uint4*)(base + a_loff[i]) = ra[i];
-#pragma unroll
-        for (int i = 0; i < S::CB; ++i) *(uint4*)(base + b_loff[i]) = rb[i];
-    };
-    auto compute = [&](int buf) {
-        const char* base = lds + buf * S::STAGE;
-#pragma unroll
-        for (int kk = 0; kk < S::BK / 16; ++kk) {
-            const int kofs = (kk * 16 + (lane >> 5) * 8) * 2;
-            bf16x8 bfr[S::NBW];
-#pragma unroll
-            for (int j = 0; j < S::NBW; ++j)
-                bfr[j] = *(const bf16x8*)(base + S::A_BYTES +
-                                          (b_block_row<S, GLU>(wn, j) + (lane & 31)) * S::LDS_ROW + kofs);
-#pragma unroll
-            for (int i = 0; i < S::MB; ++i) {
-                if (i < mact) {
-                    const bf16x8 af =
-                        *(const bf16x8*)(base + (wm * S::WTM + 32 * i + (lane & 31)) * S::LDS_ROW + kofs);
-#pragma unroll
-                    for (int j = 0; j < S::NBW; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bfr[j], acc[i][j], 0, 0, 0);
-                }
-            }
-        }
-    };
-
+    u32x4 ra[CA];
+    bf16x8 rb0[S::NBW][S::KK], rb1[S::NBW][S::KK];
     const int nk = K / S::BK;
-    gload(0);
-    sstore(0);
+    constexpr int KB = S::BK * 2;                     // bytes per K step
+
+    // K is a multiple of 2*BK (checked by the host), so the loop runs whole pairs of K steps.
+    load_b<S>(rb0, Bb, boff, 0);
+    load_a<CA>(ra, Ab, aoff, 0);
+    store_a<CA>(lds0, ra, alds);
+    load_b<S>(rb1, Bb, boff, KB);
+    load_a<CA>(ra, Ab, aoff, KB);
     __syncthreads();
-    for (int s = 0; s < nk; ++s) {
-        if (s + 1 < nk) gload((s + 1) * S::BK);
-        compute(s & 1);
-        if (s + 1 < nk) sstore((s + 1) & 1);
+    for (int s = 0; s < nk; s += 2) {
+        const bool more = s + 2 < nk;
+        mma_step<S, MACT>(acc, rb0, lds0, lane);
+        store_a<CA>(lds1, ra, alds);
+        if (more) {
+            load_b<S>(rb0, Bb, boff, (s + 2) * KB);
+            load_a<CA>(ra, Ab, aoff, (s + 2) * KB);
+        }
+        __syncthreads();
+        mma_step<S, MACT>(acc, rb1, lds1, lane);
+        if (more) {
+            store_a<CA>(lds0, ra, alds);
+            load_b<S>(rb1, Bb, boff, (s + 3) * KB);
+            load_a<CA>(ra, Ab, aoff, (s + 3) * KB);
+        }
         __syncthreads();
     }
 
     // Epilogue.  32x32 accumulator layout: lane holds column (lane & 31) and
     // rows (r/4)*8 + (lane/32)*4 + r%4 of its block, r = 0..15.
 #pragma unroll
-    for (int i = 0; i < S::MB; ++i) {
-        if (i >= mact) continue;
-        const int row_base = wm * S::WTM + 32 * i + (lane >> 5) * 4;
+    for (int i = 0; i < MACT; ++i) {
+        const int row_base = 32 * i + (lane >> 5) * 4;
         if (GLU) {
 #pragma unroll
             for (int j = 0; j < S::NBW / 2; ++j) {
-                const int col = wn * (S::BN / 2 / S::WN) + 32 * j + (lane & 31);
+                const int col = wn * (S::WCOLS / 2) + 32 * j + (lane & 31);
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const float g = acc[i][j][r], u = acc[i][j + S::NBW / 2][r];
@@ -162,12 +177,25 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
         } else {
 #pragma unroll
             for (int j = 0; j < S::NBW; ++j) {
-                const int col = wn * (S::BN / S::WN) + 32 * j + (lane & 31);
+                const int col = wn * S::WCOLS + 32 * j + (lane & 31);
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
                     out[(long)(row_base + (r >> 2) * 8 + (r & 3)) * ldo + col] = (uint16_t)f2bf_bits(acc[i][j][r]);
             }
         }
+    }
+}
+
+// Dispatch on the number of 32-row blocks holding valid rows (uniform per tile).
+template <class S, bool GLU>
+__device__ __forceinline__ void gemm_tile_bf16_rows(int rows32, const uint16_t* A, int lda, const uint16_t* B, int ldb,
+                                                    int up_rows, int K, uint16_t* out, int ldo, char* lds) {
+    static_assert(S::MB == 4, "dispatch written for 128-row tiles");
+    switch (rows32 >> 5) {
+        case 1: gemm_tile_bf16<S, GLU, 1>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
+        case 2: gemm_tile_bf16<S, GLU, 2>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
+        case 3: gemm_tile_bf16<S, GLU, 3>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
+        default: gemm_tile_bf16<S, GLU, 4>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
     }
 }
 

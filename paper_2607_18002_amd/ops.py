@@ -71,6 +71,14 @@ def moe_ffn_row_align(phase: int, dtype: int) -> int:
     return int(load_library().moe_ffn_row_align(phase, dtype))
 
 
+def moe_ffn_tile_shape(phase: int, dtype: int):
+    """(rows, columns, K step) of the FFN output tile for ops of this phase and dtype."""
+    bm, bn, bk = C.c_int32(), C.c_int32(), C.c_int32()
+    check(load_library().moe_ffn_tile_shape(phase, dtype, C.byref(bm), C.byref(bn), C.byref(bk)),
+          "moe_ffn_tile_shape")
+    return bm.value, bn.value, bk.value
+
+
 def _op_array(ops: Sequence[OpDesc]):
     arr = (OpDesc * len(ops))()
     for i, o in enumerate(ops):
@@ -118,6 +126,6 @@ def status_string(status: int) -> str:
     return load_library().moe_status_string(status).decode()
 
 
-__all__ = ["moe_topk_route", "moe_permute_workspace_bytes", "moe_permute", "moe_ffn_row_align",
+__all__ = ["moe_topk_route", "moe_permute_workspace_bytes", "moe_permute", "moe_ffn_row_align", "moe_ffn_tile_shape",
            "moe_ffn_workspace_bytes", "moe_grouped_ffn_persistent", "moe_combine", "moe_x_moe",
            "moe_decode_quota", "status_string", "OpDesc", "SchedConfig", "_lib"]

@@ -44,7 +44,9 @@ def _tiles_per_op(pipe, i):
     b = pipe.bufs[i]
     counts = b.counts.cpu().numpy()
     H, I = b.spec.weights.H, b.spec.weights.I
-    bn = 256 if b.spec.phase == 0 else 128
+    from paper_2607_18002_amd import ops
+    bm, bn, _ = ops.moe_ffn_tile_shape(b.spec.phase, b.spec.weights.dtype)
+    assert bm == b.row_align
     xm = oracle.x_moe(counts, b.row_align)
     return xm, xm * (I // (bn // 2)) + xm * (H // bn)
 

@@ -81,6 +81,9 @@ def test_row_align_and_workspace_queries():
     assert ops.moe_ffn_row_align(_lib.MOE_PREFILL, _lib.MOE_BF16) == 128
     assert ops.moe_ffn_row_align(_lib.MOE_DECODE, _lib.MOE_BF16) == 128
     assert ops.moe_ffn_row_align(7, _lib.MOE_BF16) < 0
+    for ph in (_lib.MOE_PREFILL, _lib.MOE_DECODE):
+        bm, bn, bk = ops.moe_ffn_tile_shape(ph, _lib.MOE_BF16)
+        assert bm == ops.moe_ffn_row_align(ph, _lib.MOE_BF16) and bn % 64 == 0 and bk % 16 == 0
     assert ops.moe_permute_workspace_bytes(16384, 8, 32) >= 32 * 32 * 4
     d = _lib.OpDesc(capacity=69600, row_align=128)
     cfg = _lib.SchedConfig()
