@@ -43,6 +43,7 @@ def parse():
     ap.add_argument("--config", type=int, default=4, help="workload configuration (1-5); default 4")
     ap.add_argument("--quota", type=int, default=64, help="decode quota q in workgroups")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--dump-trace", default=None, help="write the traced launch's per-tile records (.npy)")
     return ap.parse_args()
 
 
@@ -205,6 +206,9 @@ def main():
     traced.run()
     torch.cuda.synchronize()
     lat = decode_latency(traced, specs)
+    if args.dump_trace:
+        np.save(args.dump_trace, traced.trace_records())
+        np.save(args.dump_trace.replace(".npy", "_stats.npy"), traced.op_stats())
 
     dtype = cfg.dtype
     t_mfma = flops / (MFMA_PEAK_TFLOPS[dtype] * 1e12)

@@ -11,15 +11,25 @@
 // activation fused into one long-lived kernel).
 //
 // MI355X design.  One 256-thread workgroup per CU, fixed grid.  CDNA4 has no
-// thread-block clusters, so the unit of scheduling is the workgroup: wave 0
-// polls the operation words (one lane per operation), claims a tile with one
-// device-scope atomic and broadcasts it through LDS; the whole workgroup then
-// runs the tile and wave 0's first lane commits it.  Each operation's tiles
-// are numbered GEMM-1 tiles first (row tile major), then GEMM-2 tiles; a GEMM-2
-// tile waits (bounded) on a per-row-tile counter that GEMM-1 tiles bump with
-// agent-scope release semantics, so the h handoff is coherent across the
-// eight XCD-private L2 caches.  Every claimed tile belongs to a running
-// workgroup, so the dependency waits cannot deadlock.
+// thread-block clusters, so the scheduling unit is the workgroup: at every
+// tile boundary wave 0 commits the finished tile, polls the operation words
+// (one lane per operation), claims the next tile with one device-scope atomic
+// and broadcasts it through LDS; the whole workgroup runs the tile.  Each
+// operation's tiles are numbered GEMM-1 tiles first (row-tile major), then
+// GEMM-2 tiles; a GEMM-2 tile waits (bounded) on a per-row-tile counter that
+// GEMM-1 tiles bump after an agent-scope release.  Every claimed tile belongs
+// to a running workgroup, so the dependency waits cannot deadlock.
+//
+// Coherence across the eight XCD-private L2 caches.  An agent-scope acquire
+// invalidates the whole L2 of the XCD, which would destroy weight reuse if it
+// sat on the polling path.  So every scheduler word is read with relaxed
+// device-scope atomics (coherent loads that invalidate nothing), producers
+// write back their L2 (release fence) before bumping a counter, and consumers
+// of h never invalidate: within one launch a workgroup reads an h row only
+// after the row's GEMM-1 tiles committed and never before, so no L1/L2 can
+// hold a stale copy of it (launch boundaries make earlier launches' copies
+// coherent).  The one acquire per operation is taken by the workgroup that
+// completes it, before it publishes the done word.
 #include <cstring>
 
 #include "tile_bf16.hpp"
@@ -31,7 +41,8 @@ using namespace moeapk;
 using ShapeP = TileShape<128, 256, 64>;    // prefill: 128 x 256 tile, K step 64
 using ShapeD = TileShape<128, 256, 64>;    // decode : 128 x 256 tile, K step 64
 constexpr int kLdsBytes = ShapeP::LDS > ShapeD::LDS ? ShapeP::LDS : ShapeD::LDS;
-constexpr int kRowAlign = 128;                   // M_t of both bf16 classes
+constexpr int kRowAlign = 128;             // M_t of both bf16 classes
+constexpr int kMaxRowTiles = 1 << 14;      // per op (14-bit field of a table entry)
 
 enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1 };
 enum : int32_t { ST_WAIT = 0, ST_INIT = 1, ST_ACTIVE = 2, ST_DONE = 3 };
@@ -61,18 +72,23 @@ struct KArgs {
     char* ws;
 };
 
-// Static polling fields per op, written by the init kernel (so wave 0 can read
-// them with one lane per op) plus the run-time state of the op.
-struct OpSt {
-    int32_t state, claim, done, x_moe;                 // 0
-    int32_t total, n1t, quota, phase;                  // 16
-    int32_t dep, pad0;                                 // 32
-    const uint32_t* rel_word;                          // 40
-    int64_t rel_after, gap;                            // 48  (ticks; rel_after < 0: none)
-    unsigned long long t_ready, t_first, t_done;       // 64
-    char pad[128 - 88];
+// Run-time state of an op: every access is an atomic (one L2 line per op).
+struct OpDyn {
+    int32_t state, claim, done, x_moe;
+    int32_t total, n1t, quota, pad0;
+    unsigned long long t_ready, t_first, t_done;
+    char pad[128 - 56];
 };
-static_assert(sizeof(OpSt) == 128, "one L2 line per op");
+static_assert(sizeof(OpDyn) == 128, "one L2 line per op");
+
+// Readiness fields of an op: written by the init kernel, read-only during the launch.
+struct OpStatic {
+    int32_t phase, dep, pad0, pad1;
+    const uint32_t* rel_word;
+    int64_t rel_after, gap;                    // ticks; rel_after < 0: no time condition
+    char pad[128 - 40];
+};
+static_assert(sizeof(OpStatic) == 128, "one L2 line per op");
 
 struct Hdr {
     unsigned long long t0;
@@ -80,14 +96,23 @@ struct Hdr {
 };
 
 constexpr size_t kHdrBytes = 256;
-constexpr size_t kArraysOff = kHdrBytes + MOE_MAX_OPS * sizeof(OpSt);
+constexpr size_t kDynOff = kHdrBytes;
+constexpr size_t kStaticOff = kDynOff + MOE_MAX_OPS * sizeof(OpDyn);
+constexpr size_t kArraysOff = kStaticOff + MOE_MAX_OPS * sizeof(OpStatic);
 
 __device__ __forceinline__ Hdr* hdr_of(char* ws) { return (Hdr*)ws; }
-__device__ __forceinline__ OpSt* opst_of(char* ws) { return (OpSt*)(ws + kHdrBytes); }
-__device__ __forceinline__ int32_t* arr_of(char* ws) { return (int32_t*)(ws + kArraysOff); }
+__device__ __forceinline__ OpDyn* dyn_of(char* ws) { return (OpDyn*)(ws + kDynOff); }
+__device__ __forceinline__ OpStatic* static_of(char* ws) { return (OpStatic*)(ws + kStaticOff); }
+__device__ __forceinline__ char* arr_of(char* ws) { return ws + kArraysOff; }
+
+// A row-tile table entry packs everything a claim needs into one 64-bit word:
+// bits 0-9 expert, 10-23 row block, 24-31 valid rows, 32-63 first row.
+__device__ __forceinline__ uint64_t pack_entry(int e, int mb, int rows, int row0) {
+    return (uint64_t)(uint32_t)e | ((uint64_t)(uint32_t)mb << 10) | ((uint64_t)(uint32_t)rows << 24) |
+           ((uint64_t)(uint32_t)row0 << 32);
+}
 
 // ----------------------------------------------------------------------------- init
-// Readiness fields of every op, passed by value (no host staging buffer).
 struct InitArgs {
     const uint32_t* rel_words[MOE_MAX_OPS];
     int64_t rel_after[MOE_MAX_OPS];
@@ -99,14 +124,14 @@ struct InitArgs {
     int32_t* status;
 };
 
-// Zeroes the scheduler state and publishes the polling fields; one workgroup,
+// Zeroes the scheduler state and writes the readiness fields; one workgroup,
 // launched on the same stream right before the persistent kernel.
 __global__ __launch_bounds__(256) void apk_init_kernel(const InitArgs a) {
     int32_t* w = (int32_t*)a.ws;
     for (int i = threadIdx.x; i < a.ws_words; i += 256) w[i] = 0;
     __syncthreads();
     if (threadIdx.x == 0) {
-        OpSt* st = opst_of(a.ws);
+        OpStatic* st = static_of(a.ws);
         for (int o = 0; o < a.n_ops; ++o) {
             st[o].phase = a.phases[o];
             st[o].dep = a.deps[o];
@@ -139,115 +164,177 @@ __device__ __forceinline__ void run_tile(const OpArg& op, int stage, int row0, i
 }
 
 // ----------------------------------------------------------------------------- scheduler
-// Shared command block written by wave 0 and read by the whole workgroup.
+// Command block written by wave 0 and read by the whole workgroup.
 struct Cmd {
-    int32_t kind, op, stage, e, row0, rows32, nb, mtile, mblk, rows, t;
+    int32_t kind, op, stage, e, row0, rows32, nb, mtile, mblk, rows, t, pad;
     unsigned long long t_claim, t_start;
 };
 
-// Wave 0: read the decision words once per tile boundary and pick the next action.
-__device__ void schedule(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, int64_t& idle) {
+// Lane 0: an op's last tile has committed.  The acquire takes in every other
+// workgroup's released writes of this op before the done word publishes them.
+__device__ void finish_op(const KArgs& a, int o, int total) {
+    Hdr* hdr = hdr_of(a.ws);
+    OpDyn* d = dyn_of(a.ws) + o;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    const unsigned long long t = wall_ticks();
+    __hip_atomic_store(&d->t_done, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    st_release_agent(&d->state, (int32_t)ST_DONE);
+    if (a.op[o].done_word) st_release_system(a.op[o].done_word, 1u);
+    if (a.stats) {
+        moe_op_stats s;
+        s.t_ready = ld_relaxed_agent(&d->t_ready);
+        s.t_first = ld_relaxed_agent(&d->t_first);
+        s.t_done = t;
+        s.x_moe = ld_relaxed_agent(&d->x_moe);
+        s.n_tiles = total;
+        s.quota = ld_relaxed_agent(&d->quota);
+        s.reserved = 0;
+        a.stats[o] = s;
+    }
+    add_relaxed_agent(&hdr->ops_done, 1);
+}
+
+// Wave 0 at a tile boundary: commit the previous tile (if any), read the
+// decision words once, and pick the next action for the workgroup.
+__device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, const Cmd& prev, bool have_prev,
+                         int64_t& idle) {
     const int lane = threadIdx.x;
     Hdr* hdr = hdr_of(a.ws);
-    OpSt* st = opst_of(a.ws);
-    int stop = 0;
+    OpDyn* dyn = dyn_of(a.ws);
+    const OpStatic* sta = static_of(a.ws);
+
+    // 1. commit: publish the tile's h / y, then count it (the completion count returns later)
+    int done_after = -1, prev_total = -1;
+    unsigned long long t_end = 0;
+    if (have_prev && lane == 0) {
+        t_end = wall_ticks();                                  // the tile's last store has completed
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        if (prev.stage == 1) {
+            int32_t* g1 = (int32_t*)(arr_of(a.ws) + a.op[prev.op].g1_off);
+            __hip_atomic_fetch_add(g1 + prev.mtile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        done_after = add_relaxed_agent(&dyn[prev.op].done, 1) + 1;
+        prev_total = ld_relaxed_agent(&dyn[prev.op].total);
+    }
+
+    // 2. poll (all loads independent, issued together)
+    const bool has = lane < a.n_ops;
+    const int o_l = has ? lane : 0;
+    const int state = has ? ld_relaxed_agent(&dyn[o_l].state) : ST_DONE;
+    const int claim = has ? ld_relaxed_agent(&dyn[o_l].claim) : 0;
+    const int total = has ? ld_relaxed_agent(&dyn[o_l].total) : 0;
+    const int n1t = has ? ld_relaxed_agent(&dyn[o_l].n1t) : 0;
+    const int phase = has ? sta[o_l].phase : 0;
+    int stop = 0, q = 0;
     if (lane == 0) {
         stop = ld_relaxed_agent(&hdr->stop);
-        if (!stop && a.abort_word && ld_acquire_system(a.abort_word) != 0u) {
+        q = ld_relaxed_agent(&hdr->quota);
+        if (!stop && a.abort_word &&
+            __hip_atomic_load(a.abort_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != 0u) {
             set_status(a.status, MOE_ERR_ABORTED);
             st_release_agent(&hdr->stop, 1);
             stop = 1;
         }
-        if (!stop && idle > a.spin_limit) {                       // nothing claimable for too long
+        if (!stop && idle > a.spin_limit) {                    // nothing claimable for too long
             set_status(a.status, MOE_ERR_TIMEOUT);
             st_release_agent(&hdr->stop, 1);
             stop = 1;
+        }
+        // 3. finish the previous tile's op if that tile was its last; trace it
+        if (have_prev) {
+            if (done_after == prev_total) finish_op(a, prev.op, prev_total);
+            if (a.trace) {
+                const int idx = add_relaxed_agent(&hdr->trace_count, 1);
+                if (idx < a.trace_cap) {
+                    moe_trace_rec r;
+                    r.op = (int16_t)prev.op; r.stage = (int16_t)prev.stage; r.wg = (int16_t)wg;
+                    r.xcc = (int16_t)xcc_id(); r.expert = prev.e; r.mblk = prev.mblk; r.nblk = prev.nb;
+                    r.rows = prev.rows; r.t_claim = prev.t_claim; r.t_start = prev.t_start; r.t_end = t_end;
+                    a.trace[idx] = r;
+                }
+            }
         }
     }
     if (__shfl(stop, 0, 64)) {
         if (lane == 0) cmd->kind = CMD_EXIT;
         return;
     }
-    const bool has = lane < a.n_ops;
-    OpSt* my = st + (has ? lane : 0);
-    const int state = has ? ld_acquire_agent(&my->state) : ST_DONE;
+    q = __shfl(q, 0, 64);
     if (__ballot(state != ST_DONE) == 0) {
+        // every op was DONE when polled; ops finished in step 3 are DONE too
         if (lane == 0) cmd->kind = CMD_EXIT;
         return;
     }
     const uint64_t now = wall_ticks();
 
-    // 1. ready signals of waiting operation templates -> instantiate one of them
+    // 4. ready signals of waiting operation templates -> instantiate one of them
     bool ready = false;
     if (state == ST_WAIT) {
         ready = true;
-        const uint32_t* rw = my->rel_word;
-        if (rw) ready = ld_acquire_system(rw) != 0u;
-        if (ready && my->rel_after >= 0) ready = now >= t0 + (uint64_t)my->rel_after;
-        const int dep = my->dep;
+        const uint32_t* rw = sta[o_l].rel_word;
+        if (rw) ready = __hip_atomic_load(rw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != 0u;
+        if (ready && sta[o_l].rel_after >= 0) ready = now >= t0 + (uint64_t)sta[o_l].rel_after;
+        const int dep = sta[o_l].dep;
         if (ready && dep >= 0) {
-            ready = ld_acquire_agent(&st[dep].state) == ST_DONE &&
-                    now >= ld_relaxed_agent(&st[dep].t_done) + (uint64_t)my->gap;
+            ready = ld_relaxed_agent(&dyn[dep].state) == ST_DONE &&
+                    now >= ld_relaxed_agent(&dyn[dep].t_done) + (uint64_t)sta[o_l].gap;
         }
     }
     const uint64_t rmask = __ballot(ready);
     if (rmask) {
         const int o = __ffsll((long long)rmask) - 1;
         int won = 0;
-        if (lane == o) won = atomicCAS(&my->state, ST_WAIT, ST_INIT) == ST_WAIT;
+        if (lane == o) won = atomicCAS(&dyn[o].state, ST_WAIT, ST_INIT) == ST_WAIT;
         if (__ballot(won)) {
             if (lane == 0) { cmd->kind = CMD_INST; cmd->op = o; }
+            idle = 0;
             return;
         }
     }
 
-    // 2. claim a tile: decode first on workgroups below q', prefill first elsewhere
-    const int claim = (state == ST_ACTIVE) ? ld_relaxed_agent(&my->claim) : 0;
-    const int total = (state == ST_ACTIVE) ? my->total : 0;
+    // 5. claim: decode first on workgroups below q', prefill first elsewhere
     const bool avail = state == ST_ACTIVE && claim < total;
-    const int phase = has ? my->phase : 0;
     const uint64_t dmask = __ballot(avail && phase == MOE_DECODE);
     const uint64_t pmask = __ballot(avail && phase == MOE_PREFILL);
-    const int q = ld_relaxed_agent(&hdr->quota);
     const bool prefer_decode = wg < q;
-    uint64_t order[2] = {prefer_decode ? dmask : pmask, prefer_decode ? pmask : dmask};
+    const uint64_t order[2] = {prefer_decode ? dmask : pmask, prefer_decode ? pmask : dmask};
     for (int p = 0; p < 2; ++p) {
         uint64_t m = order[p];
         while (m) {                                                  // wave-uniform loop
             const int o = __ffsll((long long)m) - 1;
             m &= m - 1;
             const int tot = __shfl(total, o, 64);
+            const int o_n1t = __shfl(n1t, o, 64);
             int t = 0;
-            if (lane == 0) t = atomicAdd(&st[o].claim, 1);
+            if (lane == 0) t = atomicAdd(&dyn[o].claim, 1);
             t = __shfl(t, 0, 64);
             if (t >= tot) continue;
             if (lane == 0) {
                 const OpArg& op = a.op[o];
-                const int n1t = st[o].n1t;
                 int stage, mtile, nb;
-                if (t < n1t) { stage = 1; mtile = t / op.n1; nb = t % op.n1; }
-                else { stage = 2; mtile = (t - n1t) / op.n2; nb = (t - n1t) % op.n2; }
-                const int entry = arr_of(a.ws)[op.table_off + mtile];
-                const int e = entry >> 16, mb = entry & 0xFFFF;
-                const int rows_left = op.counts[e] - mb * op.mt;
-                const int rows = rows_left < op.mt ? rows_left : op.mt;
-                cmd->kind = CMD_TILE; cmd->op = o; cmd->stage = stage; cmd->e = e; cmd->mblk = mb;
-                cmd->row0 = op.offsets[e] + mb * op.mt; cmd->rows = rows; cmd->rows32 = (rows + 31) & ~31;
+                if (t < o_n1t) { stage = 1; mtile = t / op.n1; nb = t % op.n1; }
+                else { stage = 2; mtile = (t - o_n1t) / op.n2; nb = (t - o_n1t) % op.n2; }
+                const uint64_t* table = (const uint64_t*)(arr_of(a.ws) + op.table_off);
+                const uint64_t ent = ld_relaxed_agent(table + mtile);
+                const int rows = (int)((ent >> 24) & 0xFF);
+                cmd->kind = CMD_TILE; cmd->op = o; cmd->stage = stage;
+                cmd->e = (int)(ent & 0x3FF); cmd->mblk = (int)((ent >> 10) & 0x3FFF);
+                cmd->row0 = (int)(ent >> 32); cmd->rows = rows; cmd->rows32 = (rows + 31) & ~31;
                 cmd->nb = nb; cmd->mtile = mtile; cmd->t = t;
                 cmd->t_claim = wall_ticks();
-                if (t == 0) st[o].t_first = cmd->t_claim;
-                bool ok = true;
+                if (t == 0)
+                    __hip_atomic_store(&dyn[o].t_first, cmd->t_claim, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 if (stage == 2) {                                     // GEMM-1 of this row tile must be committed
-                    const int32_t* g1 = arr_of(a.ws) + op.g1_off + mtile;
+                    const int32_t* g1 = (const int32_t*)(arr_of(a.ws) + op.g1_off) + mtile;
                     int64_t spins = 0;
-                    while (ld_acquire_agent(g1) < op.n1) {
-                        if (++spins > a.spin_limit || ld_relaxed_agent(&hdr->stop)) { ok = false; break; }
-                        __builtin_amdgcn_s_sleep(2);
-                    }
-                    if (!ok) {
-                        set_status(a.status, MOE_ERR_TIMEOUT);
-                        st_release_agent(&hdr->stop, 1);
-                        cmd->kind = CMD_EXIT;
+                    while (ld_relaxed_agent(g1) < op.n1) {
+                        if (++spins > a.spin_limit || ld_relaxed_agent(&hdr->stop)) {
+                            set_status(a.status, MOE_ERR_TIMEOUT);
+                            st_release_agent(&hdr->stop, 1);
+                            cmd->kind = CMD_EXIT;
+                            break;
+                        }
+                        __builtin_amdgcn_s_sleep(1);
                     }
                 }
                 cmd->t_start = wall_ticks();
@@ -263,8 +350,9 @@ __device__ void schedule(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, int64_t&
 // Whole workgroup: build the row-tile table of an operation whose ready signal was seen.
 __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
     const OpArg& op = a.op[o];
-    OpSt* st = opst_of(a.ws) + o;
-    int32_t* table = arr_of(a.ws) + op.table_off;
+    OpDyn* d = dyn_of(a.ws) + o;
+    if (static_of(a.ws)[o].rel_word) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");  // system scope: peer-written inputs
+    uint64_t* table = (uint64_t*)(arr_of(a.ws) + op.table_off);
     for (int e = threadIdx.x; e < op.E; e += 256) {
         const int c = op.counts[e];
         scan[e] = c > 0 ? (c + op.mt - 1) / op.mt : 0;
@@ -282,8 +370,12 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
         const int c = op.counts[e];
         const int nt = c > 0 ? (c + op.mt - 1) / op.mt : 0;
         const int pos = scan[e];
-        if (pos + nt > op.max_mtiles || (long)op.offsets[e] + (long)nt * op.mt > op.capacity) { s_bad = 1; continue; }
-        for (int mb = 0; mb < nt; ++mb) table[pos + mb] = (e << 16) | mb;
+        const int off = op.offsets[e];
+        if (pos + nt > op.max_mtiles || off < 0 || (long)off + (long)nt * op.mt > op.capacity) { s_bad = 1; continue; }
+        for (int mb = 0; mb < nt; ++mb) {
+            const int rows = (c - mb * op.mt) < op.mt ? (c - mb * op.mt) : op.mt;
+            table[pos + mb] = pack_entry(e, mb, rows, off + mb * op.mt);
+        }
     }
     __syncthreads();
     if (threadIdx.x == 0) {
@@ -294,28 +386,22 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
             return;
         }
         const int xm = s_total;
-        st->x_moe = xm;
-        st->n1t = xm * op.n1;
-        st->total = xm * (op.n1 + op.n2);
-        st->t_ready = wall_ticks();
+        const unsigned long long t = wall_ticks();
         int qd = 0;
         if (op.phase == MOE_DECODE) {
             qd = decode_quota(a.q, xm, a.x_star, a.q_max, a.c);
-            st_release_agent(&hdr->quota, qd);
+            __hip_atomic_store(&hdr->quota, qd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        st->quota = qd;
+        __hip_atomic_store(&d->x_moe, xm, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&d->n1t, xm * op.n1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&d->total, xm * (op.n1 + op.n2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&d->quota, qd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&d->t_ready, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (xm == 0) {                                   // nothing routed here: done at once
-            st->t_first = st->t_ready;
-            st->t_done = st->t_ready;
-            st_release_agent(&st->state, (int32_t)ST_DONE);
-            if (op.done_word) st_release_system(op.done_word, 1u);
-            if (a.stats) {
-                moe_op_stats s = {st->t_ready, st->t_ready, st->t_ready, 0, 0, qd, 0};
-                a.stats[o] = s;
-            }
-            add_relaxed_agent(&hdr->ops_done, 1);
+            __hip_atomic_store(&d->t_first, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            finish_op(a, o, 0);
         } else {
-            st_release_agent(&st->state, (int32_t)ST_ACTIVE);
+            st_release_agent(&d->state, (int32_t)ST_ACTIVE);   // table entries written before this
         }
     }
 }
@@ -335,10 +421,13 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
     __syncthreads();
     const uint64_t t0 = s_t0;
     int64_t idle = 0;
+    Cmd prev;                                   // meaningful in wave 0 only
+    bool have_prev = false;
     for (;;) {
-        if (tid < 64) schedule(a, t0, wg, &cmd, idle);
+        if (tid < 64) boundary(a, t0, wg, &cmd, prev, have_prev, idle);
         __syncthreads();
         const int kind = cmd.kind;
+        have_prev = false;
         if (kind == CMD_EXIT) break;
         if (kind == CMD_IDLE) {
             __builtin_amdgcn_s_sleep(8);
@@ -358,39 +447,11 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
         const int rows32 = __builtin_amdgcn_readfirstlane(cmd.rows32);
         const int nb = __builtin_amdgcn_readfirstlane(cmd.nb);
         const int e = __builtin_amdgcn_readfirstlane(cmd.e);
+        if (tid < 64) prev = cmd;
         __syncthreads();                                      // every thread has read cmd
         run_tile(a.op[o], stage, row0, rows32, nb, e, lds);
-        __syncthreads();                                      // all stores of the tile issued and complete
-        if (tid == 0) {
-            const OpArg& op = a.op[o];
-            OpSt* st = opst_of(a.ws) + o;
-            Hdr* hdr = hdr_of(a.ws);
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // publish h / y of this tile
-            if (stage == 1) add_relaxed_agent(arr_of(a.ws) + op.g1_off + cmd.mtile, 1);
-            const int total = st->total;
-            const int done = add_relaxed_agent(&st->done, 1) + 1;
-            const unsigned long long t_end = wall_ticks();
-            if (done == total) {
-                st->t_done = t_end;
-                st_release_agent(&st->state, (int32_t)ST_DONE);
-                if (op.done_word) st_release_system(op.done_word, 1u);
-                if (a.stats) {
-                    moe_op_stats s = {st->t_ready, st->t_first, t_end, st->x_moe, total, st->quota, 0};
-                    a.stats[o] = s;
-                }
-                add_relaxed_agent(&hdr->ops_done, 1);
-            }
-            if (a.trace) {
-                const int idx = add_relaxed_agent(&hdr->trace_count, 1);
-                if (idx < a.trace_cap) {
-                    moe_trace_rec r;
-                    r.op = (int16_t)o; r.stage = (int16_t)stage; r.wg = (int16_t)wg; r.xcc = (int16_t)xcc_id();
-                    r.expert = cmd.e; r.mblk = cmd.mblk; r.nblk = cmd.nb; r.rows = cmd.rows;
-                    r.t_claim = cmd.t_claim; r.t_start = cmd.t_start; r.t_end = t_end;
-                    a.trace[idx] = r;
-                }
-            }
-        }
+        __syncthreads();                                      // the whole tile is written before the commit
+        have_prev = true;
     }
 }
 
@@ -399,14 +460,20 @@ struct ClassInfo {
 };
 ClassInfo class_info(int cls) { return cls == CLS_P_BF16 ? ClassInfo{ShapeP::BN, ShapeP::BK} : ClassInfo{ShapeD::BN, ShapeD::BK}; }
 
-size_t ws_words_for(const moe_op_desc* ops, int n_ops) {
-    size_t words = kArraysOff / 4;
-    for (int o = 0; o < n_ops; ++o) {
-        const int mt = ops[o].row_align > 0 ? ops[o].row_align : 1;
-        const size_t mm = (size_t)((ops[o].capacity + mt - 1) / mt) + 1;
-        words += 2 * mm;
-    }
-    return (words + 63) & ~(size_t)63;
+// Per op: a row-tile table (8 bytes per row tile) and GEMM-1 counters (4 bytes
+// per row tile), each padded to 256 bytes so no L2 line is shared between ops.
+size_t op_array_bytes(int capacity, int mt, size_t* table_bytes) {
+    const size_t mm = (size_t)((capacity + mt - 1) / mt) + 1;
+    const size_t tb = (mm * 8 + 255) & ~(size_t)255;
+    const size_t gb = (mm * 4 + 255) & ~(size_t)255;
+    if (table_bytes) *table_bytes = tb;
+    return tb + gb;
+}
+
+size_t ws_bytes_for(const moe_op_desc* ops, int n_ops) {
+    size_t bytes = kArraysOff;
+    for (int o = 0; o < n_ops; ++o) bytes += op_array_bytes(ops[o].capacity, ops[o].row_align > 0 ? ops[o].row_align : 1, nullptr);
+    return (bytes + 255) & ~(size_t)255;
 }
 
 }  // namespace
@@ -431,7 +498,7 @@ extern "C" moe_status_t moe_ffn_tile_shape(moe_phase_t phase, moe_dtype_t dtype,
 extern "C" size_t moe_ffn_workspace_bytes(const moe_op_desc* ops, int32_t n_ops, const moe_sched_config* cfg) {
     (void)cfg;
     if (!ops || n_ops < 1 || n_ops > MOE_MAX_OPS) return 0;
-    return ws_words_for(ops, n_ops) * 4;
+    return ws_bytes_for(ops, n_ops);
 }
 
 extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32_t n_ops, const moe_sched_config* cfg,
@@ -448,23 +515,26 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
     memset(&a, 0, sizeof(a));
     InitArgs ia;
     memset(&ia, 0, sizeof(ia));
-    size_t words = kArraysOff / 4;
+    size_t off = 0;                                   // bytes from the arrays base
     for (int o = 0; o < n_ops; ++o) {
         const moe_op_desc& d = ops[o];
         if (d.phase != MOE_PREFILL && d.phase != MOE_DECODE) return fail(MOE_ERR_INVALID_ARG, "op %d: bad phase %d", o, d.phase);
         if (d.dtype != MOE_BF16) return fail(MOE_ERR_UNSUPPORTED, "op %d: dtype %d not supported by the FFN kernel", o, d.dtype);
         const int cls = d.phase == MOE_PREFILL ? CLS_P_BF16 : CLS_D_BF16;
         const ClassInfo ci = class_info(cls);
-        if (d.E_local < 1 || d.E_local > 1024 || d.E_local >= 32768) return fail(MOE_ERR_UNSUPPORTED, "op %d: E_local=%d", o, d.E_local);
-        if (d.H < ci.bn || d.H % ci.bn != 0 || d.H % ci.bk != 0 || d.H % 256 != 0)
+        if (d.E_local < 1 || d.E_local > 1024) return fail(MOE_ERR_UNSUPPORTED, "op %d: E_local=%d outside [1,1024]", o, d.E_local);
+        // H and I are the K of a GEMM (whole pairs of K steps) and split into whole output tiles
+        if (d.H < ci.bn || d.H % ci.bn != 0 || d.H % (2 * ci.bk) != 0 || d.H % 256 != 0)
             return fail(MOE_ERR_UNSUPPORTED, "op %d: H=%d must be a positive multiple of 256", o, d.H);
-        if (d.I < ci.bn / 2 || d.I % (ci.bn / 2) != 0 || d.I % ci.bk != 0 || d.I % 256 != 0)
+        if (d.I < ci.bn / 2 || d.I % (ci.bn / 2) != 0 || d.I % (2 * ci.bk) != 0 || d.I % 256 != 0)
             return fail(MOE_ERR_UNSUPPORTED, "op %d: I=%d must be a positive multiple of 256", o, d.I);
         if (d.row_align != kRowAlign)
             return fail(MOE_ERR_INVALID_ARG, "op %d: row_align=%d but the FFN tile height is %d", o, d.row_align, kRowAlign);
         if (d.capacity < d.row_align) return fail(MOE_ERR_CAPACITY, "op %d: capacity=%d below one tile", o, d.capacity);
         if ((int64_t)d.capacity * d.H > INT32_MAX || (int64_t)d.capacity * d.I > INT32_MAX)
             return fail(MOE_ERR_UNSUPPORTED, "op %d: capacity*H exceeds 2^31 elements", o);
+        if (d.capacity / d.row_align >= kMaxRowTiles)
+            return fail(MOE_ERR_UNSUPPORTED, "op %d: capacity=%d exceeds %d row tiles", o, d.capacity, kMaxRowTiles);
         if (!d.counts || !d.offsets || !d.x_perm || !d.w_gate_up || !d.w_down || !d.h || !d.y_perm)
             return fail(MOE_ERR_INVALID_ARG, "op %d: null buffer", o);
         if (d.depends_on_op >= o || d.depends_on_op < -1)
@@ -489,17 +559,19 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
         p.mt = d.row_align;
         p.n1 = d.I / (ci.bn / 2);
         p.n2 = d.H / ci.bn;
-        const int mm = (d.capacity + d.row_align - 1) / d.row_align + 1;
-        p.max_mtiles = mm;
-        p.table_off = (int)(words - kArraysOff / 4);
-        p.g1_off = p.table_off + mm;
-        words += 2 * (size_t)mm;
+        p.max_mtiles = (d.capacity + d.row_align - 1) / d.row_align + 1;
+        size_t tb = 0;
+        const size_t ob = op_array_bytes(d.capacity, d.row_align, &tb);
+        p.table_off = (int32_t)off;
+        p.g1_off = (int32_t)(off + tb);
+        off += ob;
         ia.rel_words[o] = d.release_word;
         ia.rel_after[o] = d.release_after_ns < 0 ? -1 : d.release_after_ns * (int64_t)wc_khz / 1000000;
         ia.gaps[o] = d.gap_ns * (int64_t)wc_khz / 1000000;
         ia.deps[o] = d.depends_on_op;
         ia.phases[o] = d.phase;
     }
+    if (kArraysOff + off > (size_t)INT32_MAX) return fail(MOE_ERR_UNSUPPORTED, "scheduler workspace too large");
     int n_wg = cfg->n_workgroups > 0 ? cfg->n_workgroups : cu;
     a.n_ops = n_ops;
     a.q = cfg->decode_quota_wg < 0 ? 0 : cfg->decode_quota_wg;
@@ -527,7 +599,7 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
     if (n_wg > per_cu * cu) return fail(MOE_ERR_INVALID_ARG, "n_workgroups=%d exceeds co-resident capacity %d", n_wg, per_cu * cu);
 
     ia.n_ops = n_ops;
-    ia.ws_words = (int32_t)words;
+    ia.ws_words = (int32_t)((kArraysOff + off) / 4);
     ia.ws = (char*)workspace;
     ia.status = status_word;
     hipStream_t s = (hipStream_t)stream;

@@ -134,26 +134,29 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
     constexpr int KB = S::BK * 2;                     // bytes per K step
 
     // K is a multiple of 2*BK (checked by the host), so the loop runs whole pairs of K steps.
-    load_b<S>(rb0, Bb, boff, 0);
+    // A loads are issued before the B loads of the same K step: staging A into
+    // LDS then waits only for A (vmcnt counts in issue order) and leaves the
+    // later B loads in flight.
     load_a<CA>(ra, Ab, aoff, 0);
+    load_b<S>(rb0, Bb, boff, 0);
     store_a<CA>(lds0, ra, alds);
-    load_b<S>(rb1, Bb, boff, KB);
     load_a<CA>(ra, Ab, aoff, KB);
+    load_b<S>(rb1, Bb, boff, KB);
     __syncthreads();
     for (int s = 0; s < nk; s += 2) {
         const bool more = s + 2 < nk;
         mma_step<S, MACT>(acc, rb0, lds0, lane);
         store_a<CA>(lds1, ra, alds);
         if (more) {
-            load_b<S>(rb0, Bb, boff, (s + 2) * KB);
             load_a<CA>(ra, Ab, aoff, (s + 2) * KB);
+            load_b<S>(rb0, Bb, boff, (s + 2) * KB);
         }
         __syncthreads();
         mma_step<S, MACT>(acc, rb1, lds1, lane);
         if (more) {
             store_a<CA>(lds0, ra, alds);
-            load_b<S>(rb1, Bb, boff, (s + 3) * KB);
             load_a<CA>(ra, Ab, aoff, (s + 3) * KB);
+            load_b<S>(rb1, Bb, boff, (s + 3) * KB);
         }
         __syncthreads();
     }

@@ -282,3 +282,26 @@ def test_full_size_prefill_config(dev):
 
 def test_full_size_mixed_config_two_layers(dev):
     _sampled_full_size(dev, 4, layers=(0, 1), n_sample=6)
+
+
+def test_buffers_reused_across_launches_with_new_inputs(dev):
+    """Second launch on the same buffers with different inputs and weights:
+    the persistent kernel never invalidates caches on its h handoff, so a
+    stale copy from the first launch would show up here."""
+    from paper_2607_18002_amd.pipeline import MoEPipeline, bf16_tensor
+    cfg = custom_config(2, cfg_id=501, H=512, I=512, prefill_tokens=900, decode_tokens=200, E_global=64,
+                        E_local=16, top_k=4, zipf_s=(1.1, 0.7), n_layers=2)
+    specs, lay0, w = layer_specs(cfg, 0, dev)
+    pipe = MoEPipeline(specs)
+    for layer in (0, 1, 0):
+        lay = make_layer(cfg, layer)
+        for s, ph in zip(specs, lay.phases):
+            s.logits.copy_(torch.from_numpy(ph.logits).to(dev))
+            s.x.copy_(bf16_tensor(ph.x, dev))
+        w.w_gate_up.copy_(bf16_tensor(lay.weights["w_gate_up"], dev))
+        w.w_down.copy_(bf16_tensor(lay.weights["w_down"], dev))
+        pipe.run()
+        torch.cuda.synchronize()
+        assert pipe.statuses() == (0, 0)
+        for i, ph in enumerate(lay.phases):
+            _check_op(pipe, i, cfg, lay, ph)

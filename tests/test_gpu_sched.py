@@ -71,7 +71,8 @@ def test_every_tile_exactly_once_and_dependencies(dev):
             assert len(g1) and len(g2)
             assert g2["t_start"].min() >= g1["t_end"].max(), "GEMM-2 started before its GEMM-1 row tile committed"
         assert np.all(mine["t_claim"] >= st["t_ready"][i])
-        assert st["t_done"][i] == mine["t_end"].max()
+        assert st["t_done"][i] >= mine["t_end"].max()                 # done is published after every commit
+        assert st["t_done"][i] - mine["t_end"].max() < 2000           # ... promptly (20 us)
         assert np.all(mine["t_start"] <= mine["t_end"])
 
 
