@@ -60,6 +60,10 @@ typedef int32_t moe_phase_t;
 
 #define MOE_MAX_OPS 16   /* operations per persistent launch */
 
+typedef int32_t moe_layout_t;
+#define MOE_LAYOUT_ROWMAJOR 0   /* [E, N, K], K contiguous                        */
+#define MOE_LAYOUT_PACKED   1   /* written by moe_pack_weights (see below)        */
+
 /* ------------------------------------------------------------------------- a1
  * Top-k gating (Background, "MoE LLM Inference": the router selects a top-k
  * subset of routed experts per token).  Reading taken for the unspecified
@@ -156,7 +160,7 @@ typedef struct moe_op_desc {
     int64_t release_after_ns;     /* < 0: no time condition; else device wall clock >=
                                      kernel start + release_after_ns                     */
     int32_t depends_on_op;        /* -1, or an EARLIER op index that must be done...     */
-    int32_t reserved0;
+    moe_layout_t weight_layout;   /* layout of w_gate_up / w_down: MOE_LAYOUT_PACKED      */
     int64_t gap_ns;               /* ...for at least gap_ns                              */
     uint32_t* done_word;          /* NULL, or set to 1 (system-scope release) when the
                                      op's last tile has committed                        */
@@ -224,6 +228,20 @@ size_t moe_ffn_workspace_bytes(const moe_op_desc* ops, int32_t n_ops, const moe_
 moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32_t n_ops,
                                         const moe_sched_config* cfg, void* workspace,
                                         int32_t* status_word, void* stream);
+
+/* Weight layout streamed by the FFN kernel (one-time conversion, outside the
+ * hot path).  A bf16 matrix [N, K] (N a multiple of 32, K a multiple of 64) is
+ * cut into 32-row blocks; a block is K/64 chunks of 4 KB; chunk c of block b
+ * holds, for q = 0..3 and lane = 0..63 in that order, the 8 elements
+ *   row 32*b + lane%32,  columns 64*c + (lane/32)*32 + 8*q .. +8,
+ * i.e. exactly the 16 bytes lane `lane` feeds to the q-th 32x32x16 MFMA of
+ * the chunk, so each 64-lane load reads 1 KB contiguous.  The packed matrix
+ * has the same size as the row-major one and block b starts at the same byte
+ * offset as row 32*b.
+ *  src  [E, N, K] row-major (device);  dst  same size (device, not aliasing src)
+ * Limits: dtype MOE_BF16; N % 32 == 0; K % 64 == 0. */
+moe_status_t moe_pack_weights(const void* src, void* dst, int32_t E, int32_t N, int32_t K, moe_dtype_t dtype,
+                              void* stream);
 
 /* ------------------------------------------------------------------------- a7
  * Weighted combine (Background, "MoE LLM Inference": the chosen experts'

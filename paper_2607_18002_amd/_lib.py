@@ -20,6 +20,7 @@ MOE_ERR_BAD_EXPERT = -7
 
 MOE_F32, MOE_BF16, MOE_FP8_E4M3 = 0, 1, 2
 MOE_PREFILL, MOE_DECODE = 0, 1
+MOE_LAYOUT_ROWMAJOR, MOE_LAYOUT_PACKED = 0, 1
 MOE_MAX_OPS = 16
 
 _p = C.c_void_p
@@ -35,7 +36,7 @@ class OpDesc(C.Structure):
         ("w_gate_up", _p), ("w_gate_up_scales", _p), ("w_down", _p), ("w_down_scales", _p),
         ("h", _p), ("h_scales", _p), ("y_perm", _p),
         ("release_word", _p), ("release_after_ns", _i64),
-        ("depends_on_op", _i32), ("reserved0", _i32), ("gap_ns", _i64),
+        ("depends_on_op", _i32), ("weight_layout", _i32), ("gap_ns", _i64),
         ("done_word", _p),
     ]
 
@@ -75,6 +76,7 @@ PROTOTYPES = {
     "moe_ffn_workspace_bytes": (C.c_size_t, [C.POINTER(OpDesc), _i32, C.POINTER(SchedConfig)]),
     "moe_grouped_ffn_persistent": (_i32, [C.POINTER(OpDesc), _i32, C.POINTER(SchedConfig), _p, _p, _p]),
     "moe_combine": (_i32, [_p, _p, _p, _i32, _i32, _i32, _p, _i32, _p]),
+    "moe_pack_weights": (_i32, [_p, _p, _i32, _i32, _i32, _i32, _p]),
     "moe_x_moe": (_i32, [C.POINTER(_i32), _i32, _i32]),
     "moe_decode_quota": (_i32, [_i32, _i32, _i32, _i32, _i32]),
     "moe_abi_sizeof": (C.c_size_t, [_i32]),

@@ -19,7 +19,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libmoe_apk.so")
-SOURCES = ["api.cpp", "route.hip", "permute.hip", "combine.hip", "ffn.hip"]
+SOURCES = ["api.cpp", "route.hip", "permute.hip", "combine.hip", "ffn.hip", "pack.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

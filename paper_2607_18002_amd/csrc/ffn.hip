@@ -74,8 +74,8 @@ struct KArgs {
 
 // Run-time state of an op: every access is an atomic (one L2 line per op).
 struct OpDyn {
-    int32_t state, claim, done, x_moe;
-    int32_t total, n1t, quota, pad0;
+    int32_t state, pad_a, done, x_moe;
+    int32_t total, pad_b, quota, pad0;
     unsigned long long t_ready, t_first, t_done;
     char pad[128 - 56];
 };
@@ -95,15 +95,49 @@ struct Hdr {
     int32_t ops_done, quota, trace_count, stop;
 };
 
+// One tile queue per (op, XCD): the op's row tiles are cut into kXcds
+// contiguous, balanced ranges [m_lo, m_lo + n_mt); queue x holds the GEMM-1
+// tiles of its range, then its GEMM-2 tiles.  Workgroups claim from their own
+// XCD's queue, so the activation rows and h of a row tile stay in one L2;
+// a workgroup whose queue is empty steals from the others.  claim is an
+// atomic counter; size / m_lo / n_mt are written once at instantiation.
+constexpr int kXcds = 8;
+struct XQueue {
+    int32_t claim, size, m_lo, n_mt;
+    char pad[128 - 16];
+};
+static_assert(sizeof(XQueue) == 128, "one L2 line per queue");
+
+// Within a queue, tiles run in groups of kGroupM row tiles: for each column
+// block, the group's row tiles back to back, so a weight slice fetched into
+// L2 serves kGroupM tiles while it is hot.
+constexpr int kGroupM = 4;
+
 constexpr size_t kHdrBytes = 256;
 constexpr size_t kDynOff = kHdrBytes;
 constexpr size_t kStaticOff = kDynOff + MOE_MAX_OPS * sizeof(OpDyn);
-constexpr size_t kArraysOff = kStaticOff + MOE_MAX_OPS * sizeof(OpStatic);
+constexpr size_t kXqOff = kStaticOff + MOE_MAX_OPS * sizeof(OpStatic);
+constexpr size_t kArraysOff = kXqOff + MOE_MAX_OPS * kXcds * sizeof(XQueue);
 
 __device__ __forceinline__ Hdr* hdr_of(char* ws) { return (Hdr*)ws; }
 __device__ __forceinline__ OpDyn* dyn_of(char* ws) { return (OpDyn*)(ws + kDynOff); }
 __device__ __forceinline__ OpStatic* static_of(char* ws) { return (OpStatic*)(ws + kStaticOff); }
 __device__ __forceinline__ char* arr_of(char* ws) { return ws + kArraysOff; }
+__device__ __forceinline__ XQueue* xq_of(char* ws, int o, int x) { return (XQueue*)(ws + kXqOff) + o * kXcds + x; }
+
+// Tile t of a queue holding n_mt row tiles starting at m_lo -> (stage, row tile, column block).
+__device__ __forceinline__ void queue_tile(int t, int n_mt, int m_lo, int n1, int n2, int& stage, int& mtile, int& nb) {
+    const int n1x = n_mt * n1;
+    int u = t, nn = n1;
+    stage = 1;
+    if (t >= n1x) { stage = 2; u = t - n1x; nn = n2; }
+    const int group = u / (kGroupM * nn);
+    const int within = u - group * (kGroupM * nn);
+    const int rest = n_mt - group * kGroupM;
+    const int gsz = rest < kGroupM ? rest : kGroupM;
+    nb = within / gsz;
+    mtile = m_lo + group * kGroupM + (within - nb * gsz);
+}
 
 // A row-tile table entry packs everything a claim needs into one 64-bit word:
 // bits 0-9 expert, 10-23 row block, 24-31 valid rows, 32-63 first row.
@@ -148,11 +182,11 @@ template <class S>
 __device__ __forceinline__ void run_tile_cls(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds) {
     const long H = op.H, I = op.I;
     if (stage == 1) {
-        gemm_tile_bf16_rows<S, true>(rows32, op.x + row0 * H, (int)H,
+        gemm_tile_bf16_rows<S, true, true>(rows32, op.x + row0 * H, (int)H,
                                      op.wgu + (long)e * 2 * I * H + (long)nb * (S::BN / 2) * H, (int)H, (int)I,
                                      (int)H, op.h + row0 * I + nb * (S::BN / 2), (int)I, lds);
     } else {
-        gemm_tile_bf16_rows<S, false>(rows32, op.h + row0 * I, (int)I, op.wd + (long)e * H * I + (long)nb * S::BN * I,
+        gemm_tile_bf16_rows<S, false, true>(rows32, op.h + row0 * I, (int)I, op.wd + (long)e * H * I + (long)nb * S::BN * I,
                                       (int)I, 0, (int)I, op.y + row0 * H + nb * S::BN, (int)H, lds);
     }
 }
@@ -220,10 +254,11 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, const Cm
     // 2. poll (all loads independent, issued together)
     const bool has = lane < a.n_ops;
     const int o_l = has ? lane : 0;
+    const int myx = xcc_id();
+    const XQueue* own = xq_of(a.ws, o_l, myx);
     const int state = has ? ld_relaxed_agent(&dyn[o_l].state) : ST_DONE;
-    const int claim = has ? ld_relaxed_agent(&dyn[o_l].claim) : 0;
-    const int total = has ? ld_relaxed_agent(&dyn[o_l].total) : 0;
-    const int n1t = has ? ld_relaxed_agent(&dyn[o_l].n1t) : 0;
+    const int own_claim = has ? ld_relaxed_agent(&own->claim) : 0;
+    const int own_size = has ? ld_relaxed_agent(&own->size) : 0;
     const int phase = has ? sta[o_l].phase : 0;
     int stop = 0, q = 0;
     if (lane == 0) {
@@ -292,10 +327,12 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, const Cm
         }
     }
 
-    // 5. claim: decode first on workgroups below q', prefill first elsewhere
-    const bool avail = state == ST_ACTIVE && claim < total;
-    const uint64_t dmask = __ballot(avail && phase == MOE_DECODE);
-    const uint64_t pmask = __ballot(avail && phase == MOE_PREFILL);
+    // 5. claim: decode first on workgroups below q', prefill first elsewhere;
+    //    within a phase: the own XCD's queue first, then steal from the others
+    const bool active = state == ST_ACTIVE;
+    const uint64_t dmask = __ballot(active && phase == MOE_DECODE);
+    const uint64_t pmask = __ballot(active && phase == MOE_PREFILL);
+    const uint64_t own_avail = __ballot(active && own_claim < own_size);
     const bool prefer_decode = wg < q;
     const uint64_t order[2] = {prefer_decode ? dmask : pmask, prefer_decode ? pmask : dmask};
     for (int p = 0; p < 2; ++p) {
@@ -303,17 +340,38 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, const Cm
         while (m) {                                                  // wave-uniform loop
             const int o = __ffsll((long long)m) - 1;
             m &= m - 1;
-            const int tot = __shfl(total, o, 64);
-            const int o_n1t = __shfl(n1t, o, 64);
-            int t = 0;
-            if (lane == 0) t = atomicAdd(&dyn[o].claim, 1);
-            t = __shfl(t, 0, 64);
-            if (t >= tot) continue;
+            int src = -1, t = 0;
+            if ((own_avail >> o) & 1) {                             // own queue
+                if (lane == 0) t = atomicAdd(&xq_of(a.ws, o, myx)->claim, 1);
+                t = __shfl(t, 0, 64);
+                if (t < __shfl(own_size, o, 64)) src = myx;
+            }
+            if (src < 0) {                                           // steal: the queue with most tiles left
+                const XQueue* qx = xq_of(a.ws, o, lane & (kXcds - 1));
+                int left = 0;
+                if (lane < kXcds) left = ld_relaxed_agent(&qx->size) - ld_relaxed_agent(&qx->claim);
+                int best = left, who = lane;
+#pragma unroll
+                for (int off = 4; off >= 1; off >>= 1) {             // max over lanes 0..7
+                    const int ob = __shfl_xor(best, off, 64), ow = __shfl_xor(who, off, 64);
+                    if (ob > best || (ob == best && ow < who)) { best = ob; who = ow; }
+                }
+                best = __shfl(best, 0, 64);
+                who = __shfl(who, 0, 64);
+                if (best <= 0) continue;
+                if (lane == 0) t = atomicAdd(&xq_of(a.ws, o, who)->claim, 1);
+                t = __shfl(t, 0, 64);
+                int sz = 0;
+                if (lane == 0) sz = ld_relaxed_agent(&xq_of(a.ws, o, who)->size);
+                if (t >= __shfl(sz, 0, 64)) continue;
+                src = who;
+            }
             if (lane == 0) {
                 const OpArg& op = a.op[o];
+                const XQueue* qs = xq_of(a.ws, o, src);
+                const int m_lo = ld_relaxed_agent(&qs->m_lo), n_mt = ld_relaxed_agent(&qs->n_mt);
                 int stage, mtile, nb;
-                if (t < o_n1t) { stage = 1; mtile = t / op.n1; nb = t % op.n1; }
-                else { stage = 2; mtile = (t - o_n1t) / op.n2; nb = (t - o_n1t) % op.n2; }
+                queue_tile(t, n_mt, m_lo, op.n1, op.n2, stage, mtile, nb);
                 const uint64_t* table = (const uint64_t*)(arr_of(a.ws) + op.table_off);
                 const uint64_t ent = ld_relaxed_agent(table + mtile);
                 const int rows = (int)((ent >> 24) & 0xFF);
@@ -322,8 +380,11 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, const Cm
                 cmd->row0 = (int)(ent >> 32); cmd->rows = rows; cmd->rows32 = (rows + 31) & ~31;
                 cmd->nb = nb; cmd->mtile = mtile; cmd->t = t;
                 cmd->t_claim = wall_ticks();
-                if (t == 0)
-                    __hip_atomic_store(&dyn[o].t_first, cmd->t_claim, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (t == 0) {
+                    unsigned long long zero = 0;
+                    __hip_atomic_compare_exchange_strong(&dyn[o].t_first, &zero, cmd->t_claim, __ATOMIC_RELAXED,
+                                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
                 if (stage == 2) {                                     // GEMM-1 of this row tile must be committed
                     const int32_t* g1 = (const int32_t*)(arr_of(a.ws) + op.g1_off) + mtile;
                     int64_t spins = 0;
@@ -393,7 +454,13 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
             __hip_atomic_store(&hdr->quota, qd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         __hip_atomic_store(&d->x_moe, xm, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&d->n1t, xm * op.n1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int x = 0; x < kXcds; ++x) {                      // balanced contiguous row-tile ranges
+            XQueue* qx = xq_of(a.ws, o, x);
+            const int lo = (int)((long)xm * x / kXcds), hi = (int)((long)xm * (x + 1) / kXcds);
+            __hip_atomic_store(&qx->m_lo, lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&qx->n_mt, hi - lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(&qx->size, (hi - lo) * (op.n1 + op.n2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
         __hip_atomic_store(&d->total, xm * (op.n1 + op.n2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(&d->quota, qd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(&d->t_ready, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -520,6 +587,8 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
         const moe_op_desc& d = ops[o];
         if (d.phase != MOE_PREFILL && d.phase != MOE_DECODE) return fail(MOE_ERR_INVALID_ARG, "op %d: bad phase %d", o, d.phase);
         if (d.dtype != MOE_BF16) return fail(MOE_ERR_UNSUPPORTED, "op %d: dtype %d not supported by the FFN kernel", o, d.dtype);
+        if (d.weight_layout != MOE_LAYOUT_PACKED)
+            return fail(MOE_ERR_UNSUPPORTED, "op %d: weights must be in MOE_LAYOUT_PACKED (moe_pack_weights)", o);
         const int cls = d.phase == MOE_PREFILL ? CLS_P_BF16 : CLS_D_BF16;
         const ClassInfo ci = class_info(cls);
         if (d.E_local < 1 || d.E_local > 1024) return fail(MOE_ERR_UNSUPPORTED, "op %d: E_local=%d outside [1,1024]", o, d.E_local);

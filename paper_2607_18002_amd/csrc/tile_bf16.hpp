@@ -8,9 +8,9 @@
 //  * A (activation rows, shared by the four waves) is staged through LDS,
 //    double-buffered, with rows padded by 16 bytes so an operand read is free
 //    of bank conflicts.
-// K order inside a K step: lanes 0-31 take elements [0, BK/2) and lanes 32-63
-// take [BK/2, BK) across the BK/16 MFMAs, so each lane's B reads of a K step
-// are one contiguous BK-byte run (a full cache line at BK = 64 bf16).  A and B
+// K order: K runs in 64-element chunks; in each chunk lanes 0-31 take
+// elements [0, 32) and lanes 32-63 take [32, 64), 8 per MFMA, so MFMA kk of a
+// K step covers chunk kk/4, elements (lane/32)*32 + (kk%4)*8 .. +8.  A and B
 // use the same order; the sum over K is unchanged.
 //
 // GLU tiles (GEMM-1) take BN/2 gate rows and BN/2 up rows of the [2I, H]
@@ -45,11 +45,21 @@ struct TileRegs {
     static constexpr int CA = MACT * 32 / S::RPP;    // A chunks per thread and K step
 };
 
+// Raw buffer loads: the tile's base address lives in an SGPR descriptor, the
+// per-lane offset in one VGPR, the K-step offset in an SGPR and the per-MFMA
+// offset in the instruction, so a load needs no address arithmetic.  The
+// descriptor's size bounds the tile's extent (reads past it return zero).
+constexpr int kBufferWord3 = 0x00020000;   // gfx9-family raw buffer: 32-bit data format, no swizzle
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kBufferWord3);
+}
+
 template <int CA>
-__device__ __forceinline__ void load_a(u32x4 (&ra)[CA], const char* __restrict__ A, const uint32_t (&aoff)[CA],
+__device__ __forceinline__ void load_a(u32x4 (&ra)[CA], __amdgpu_buffer_rsrc_t A, const uint32_t (&aoff)[CA],
                                        int k0b) {
 #pragma unroll
-    for (int i = 0; i < CA; ++i) ra[i] = *(const u32x4*)(A + aoff[i] + k0b);
+    for (int i = 0; i < CA; ++i) ra[i] = __builtin_amdgcn_raw_buffer_load_b128(A, (int)aoff[i], k0b, 0);
 }
 
 template <int CA>
@@ -58,29 +68,49 @@ __device__ __forceinline__ void store_a(char* buf, const u32x4 (&ra)[CA], const 
     for (int i = 0; i < CA; ++i) *(u32x4*)(buf + alds[i]) = ra[i];
 }
 
-template <class S>
-__device__ __forceinline__ void load_b(bf16x8 (&rb)[S::NBW][S::KK], const char* __restrict__ B,
+// Weight fragments of one K step.  Row-major weights: lane reads 16 bytes of
+// its row per MFMA (k0b = step * BK * 2).  Packed weights (moe_pack_weights):
+// each 32-row x 64-element chunk is 4 KB laid out as [kk%4][lane][16 B], so
+// each load instruction reads 1 KB contiguous (k0b = step * BK * 64).
+template <class S, bool PACKED>
+__device__ __forceinline__ void load_b(bf16x8 (&rb)[S::NBW][S::KK], __amdgpu_buffer_rsrc_t B,
                                        const uint32_t (&boff)[S::NBW], int k0b) {
 #pragma unroll
     for (int j = 0; j < S::NBW; ++j)
 #pragma unroll
-        for (int kk = 0; kk < S::KK; ++kk) rb[j][kk] = *(const bf16x8*)(B + boff[j] + k0b + kk * 16);
+        for (int kk = 0; kk < S::KK; ++kk) {
+            const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(
+                B, (int)(boff[j] + (PACKED ? kk * 1024 : (kk >> 2) * 128 + (kk & 3) * 16)), k0b, 0);
+            rb[j][kk] = __builtin_bit_cast(bf16x8, v);
+        }
 }
 
+// One K step of MFMAs.  The A fragments of step kk+1 are read from LDS while
+// the MFMAs of step kk run (two register sets), and the scheduling-group
+// barriers keep that order: each step is {MACT LDS reads, MACT*NBW MFMAs}.
 template <class S, int MACT>
 __device__ __forceinline__ void mma_step(f32x16 (&acc)[MACT][S::NBW], const bf16x8 (&rb)[S::NBW][S::KK],
                                          const char* buf, int lane) {
-    const char* arow = buf + (lane & 31) * S::LDS_ROW + (lane >> 5) * S::BK;   // half-K split: +BK/2 elements
+    const char* arow = buf + (lane & 31) * S::LDS_ROW + (lane >> 5) * 64;   // lanes 32-63: +32 elements
+    bf16x8 af[2][MACT];
+#pragma unroll
+    for (int i = 0; i < MACT; ++i) af[0][i] = *(const bf16x8*)(arow + i * 32 * S::LDS_ROW);
+    __builtin_amdgcn_sched_group_barrier(0x100, MACT, 0);                              // DS reads of step 0
 #pragma unroll
     for (int kk = 0; kk < S::KK; ++kk) {
-        bf16x8 af[MACT];
+        const int cur = kk & 1;
+        if (kk + 1 < S::KK) {
 #pragma unroll
-        for (int i = 0; i < MACT; ++i) af[i] = *(const bf16x8*)(arow + i * 32 * S::LDS_ROW + kk * 16);
+            for (int i = 0; i < MACT; ++i)
+                af[cur ^ 1][i] = *(const bf16x8*)(arow + i * 32 * S::LDS_ROW + ((kk + 1) >> 2) * 128 + ((kk + 1) & 3) * 16);
+        }
 #pragma unroll
         for (int i = 0; i < MACT; ++i)
 #pragma unroll
             for (int j = 0; j < S::NBW; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], rb[j][kk], acc[i][j], 0, 0, 0);
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], rb[j][kk], acc[i][j], 0, 0, 0);
+        if (kk + 1 < S::KK) __builtin_amdgcn_sched_group_barrier(0x100, MACT, 0);   // DS reads of kk+1
+        __builtin_amdgcn_sched_group_barrier(0x008, MACT * S::NBW, 0);                // MFMAs of kk
     }
 }
 
@@ -88,7 +118,7 @@ __device__ __forceinline__ void mma_step(f32x16 (&acc)[MACT][S::NBW], const bf16
 // B   : first B row of the tile (GLU: gate row n0), row stride ldb elements
 // up_rows : GLU only, rows from the gate block to the matching up block (I)
 // out : output tile origin, row stride ldo (bf16); rows [0, 32*MACT) written
-template <class S, bool GLU, int MACT>
+template <class S, bool GLU, int MACT, bool PACKED = false>
 __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, int lda,
                                                const uint16_t* __restrict__ B, int ldb, int up_rows, int K,
                                                uint16_t* __restrict__ out, int ldo, char* lds) {
@@ -106,7 +136,10 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
         } else {
             row = wn * S::WCOLS + 32 * j + (lane & 31);
         }
-        boff[j] = (uint32_t)row * (uint32_t)ldb * 2u + (uint32_t)((lane >> 5) * S::BK);
+        if (PACKED)   // row is 32-aligned minus the lane part; the block starts where row-major row (row & ~31) would
+            boff[j] = (uint32_t)(row - (lane & 31)) * (uint32_t)ldb * 2u + (uint32_t)(lane * 16);
+        else
+            boff[j] = (uint32_t)row * (uint32_t)ldb * 2u + (uint32_t)((lane >> 5) * 64);
     }
     uint32_t aoff[CA], alds[CA];
 #pragma unroll
@@ -115,8 +148,10 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
         aoff[i] = (uint32_t)r * (uint32_t)lda * 2u + c * 16;
         alds[i] = r * S::LDS_ROW + c * 16;
     }
-    const char* Ab = (const char*)A;
-    const char* Bb = (const char*)B;
+    // extents: A rows [0, 32*MACT); B rows [0, BN) or, for GLU, gate rows [0, BN/2) and up rows [up_rows, up_rows + BN/2)
+    const __amdgpu_buffer_rsrc_t Ab = make_rsrc(A, (uint32_t)(MACT * 32) * (uint32_t)lda * 2u);
+    const __amdgpu_buffer_rsrc_t Bb =
+        make_rsrc(B, (uint32_t)(GLU ? up_rows + S::BN / 2 : S::BN) * (uint32_t)ldb * 2u);
     char* lds0 = lds;
     char* lds1 = lds + S::A_STAGE;
 
@@ -131,17 +166,19 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
     u32x4 ra[CA];
     bf16x8 rb0[S::NBW][S::KK], rb1[S::NBW][S::KK];
     const int nk = K / S::BK;
-    constexpr int KB = S::BK * 2;                     // bytes per K step
+    constexpr int KB = S::BK * 2;                     // bytes per K step of a row-major row
+    constexpr int KBB = PACKED ? S::BK * 64 : KB;     // bytes per K step of a weight fragment stream
+    static_assert(S::BK % 64 == 0, "K steps are whole 64-element chunks");
 
     // K is a multiple of 2*BK (checked by the host), so the loop runs whole pairs of K steps.
     // A loads are issued before the B loads of the same K step: staging A into
     // LDS then waits only for A (vmcnt counts in issue order) and leaves the
     // later B loads in flight.
     load_a<CA>(ra, Ab, aoff, 0);
-    load_b<S>(rb0, Bb, boff, 0);
+    load_b<S, PACKED>(rb0, Bb, boff, 0);
     store_a<CA>(lds0, ra, alds);
     load_a<CA>(ra, Ab, aoff, KB);
-    load_b<S>(rb1, Bb, boff, KB);
+    load_b<S, PACKED>(rb1, Bb, boff, KBB);
     __syncthreads();
     for (int s = 0; s < nk; s += 2) {
         const bool more = s + 2 < nk;
@@ -149,14 +186,14 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
         store_a<CA>(lds1, ra, alds);
         if (more) {
             load_a<CA>(ra, Ab, aoff, (s + 2) * KB);
-            load_b<S>(rb0, Bb, boff, (s + 2) * KB);
+            load_b<S, PACKED>(rb0, Bb, boff, (s + 2) * KBB);
         }
         __syncthreads();
         mma_step<S, MACT>(acc, rb1, lds1, lane);
         if (more) {
             store_a<CA>(lds0, ra, alds);
             load_a<CA>(ra, Ab, aoff, (s + 3) * KB);
-            load_b<S>(rb1, Bb, boff, (s + 3) * KB);
+            load_b<S, PACKED>(rb1, Bb, boff, (s + 3) * KBB);
         }
         __syncthreads();
     }
@@ -190,15 +227,15 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
 }
 
 // Dispatch on the number of 32-row blocks holding valid rows (uniform per tile).
-template <class S, bool GLU>
+template <class S, bool GLU, bool PACKED>
 __device__ __forceinline__ void gemm_tile_bf16_rows(int rows32, const uint16_t* A, int lda, const uint16_t* B, int ldb,
                                                     int up_rows, int K, uint16_t* out, int ldo, char* lds) {
     static_assert(S::MB == 4, "dispatch written for 128-row tiles");
     switch (rows32 >> 5) {
-        case 1: gemm_tile_bf16<S, GLU, 1>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
-        case 2: gemm_tile_bf16<S, GLU, 2>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
-        case 3: gemm_tile_bf16<S, GLU, 3>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
-        default: gemm_tile_bf16<S, GLU, 4>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
+        case 1: gemm_tile_bf16<S, GLU, 1, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
+        case 2: gemm_tile_bf16<S, GLU, 2, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
+        case 3: gemm_tile_bf16<S, GLU, 3, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
+        default: gemm_tile_bf16<S, GLU, 4, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
     }
 }
 

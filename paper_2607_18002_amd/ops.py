@@ -112,6 +112,17 @@ def moe_combine(y_perm: torch.Tensor, assign_to_row: torch.Tensor, topk_w: torch
     return y
 
 
+def moe_pack_weights(src: torch.Tensor, dst: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """[E, N, K] bf16 row-major -> the FFN kernel's packed weight layout (same shape and size)."""
+    lib = load_library()
+    E, N, K = src.shape
+    if dst is None:
+        dst = torch.empty_like(src)
+    check(lib.moe_pack_weights(_ptr(src), _ptr(dst), E, N, K, act_dtype_code(src), _stream(stream)),
+          "moe_pack_weights")
+    return dst
+
+
 def moe_x_moe(counts: Sequence[int], M_t: int) -> int:
     lib = load_library()
     arr = (C.c_int32 * len(counts))(*[int(c) for c in counts])
@@ -127,5 +138,5 @@ def status_string(status: int) -> str:
 
 
 __all__ = ["moe_topk_route", "moe_permute_workspace_bytes", "moe_permute", "moe_ffn_row_align", "moe_ffn_tile_shape",
-           "moe_ffn_workspace_bytes", "moe_grouped_ffn_persistent", "moe_combine", "moe_x_moe",
+           "moe_ffn_workspace_bytes", "moe_grouped_ffn_persistent", "moe_combine", "moe_pack_weights", "moe_x_moe",
            "moe_decode_quota", "status_string", "OpDesc", "SchedConfig", "_lib"]

@@ -13,7 +13,8 @@ import numpy as np
 import torch
 
 from . import ops as K
-from ._lib import MOE_BF16, MOE_DECODE, MOE_FP8_E4M3, MOE_PREFILL, OpDesc, OpStats, SchedConfig, TraceRec
+from ._lib import (MOE_BF16, MOE_DECODE, MOE_FP8_E4M3, MOE_LAYOUT_PACKED, MOE_PREFILL, OpDesc, OpStats, SchedConfig,
+                   TraceRec)
 
 TRACE_DTYPE = np.dtype([("op", "<i2"), ("stage", "<i2"), ("wg", "<i2"), ("xcc", "<i2"), ("expert", "<i4"),
                         ("mblk", "<i4"), ("nblk", "<i4"), ("rows", "<i4"), ("t_claim", "<u8"),
@@ -35,18 +36,30 @@ def bits_of(t: torch.Tensor) -> np.ndarray:
 
 @dataclass
 class LayerWeights:
+    """Expert weights of one layer on the device, in the FFN kernel's packed
+    layout (moe_pack_weights); load() converts row-major [E, N, K] tensors."""
     H: int
     I: int
     dtype: int                                  # MOE_BF16 | MOE_FP8_E4M3
-    w_gate_up: torch.Tensor                     # [E_l, 2I, H]
-    w_down: torch.Tensor                        # [E_l, H, I]
+    w_gate_up: torch.Tensor                     # packed [E_l, 2I, H]
+    w_down: torch.Tensor                        # packed [E_l, H, I]
     w_gate_up_scales: Optional[torch.Tensor] = None
     w_down_scales: Optional[torch.Tensor] = None
+    layout: int = MOE_LAYOUT_PACKED
+
+    def load(self, w_gate_up: torch.Tensor, w_down: torch.Tensor) -> None:
+        """Overwrite with new row-major device weights (packed on the device)."""
+        K.moe_pack_weights(w_gate_up, self.w_gate_up)
+        K.moe_pack_weights(w_down, self.w_down)
 
     @staticmethod
     def from_numpy(w: dict, H: int, I: int, device) -> "LayerWeights":
         if w["w_gate_up"].dtype == np.uint16:
-            return LayerWeights(H, I, MOE_BF16, bf16_tensor(w["w_gate_up"], device), bf16_tensor(w["w_down"], device))
+            gu, wd = bf16_tensor(w["w_gate_up"], device), bf16_tensor(w["w_down"], device)
+            lw = LayerWeights(H, I, MOE_BF16, torch.empty_like(gu), torch.empty_like(wd))
+            lw.load(gu, wd)
+            del gu, wd
+            return lw
         return LayerWeights(H, I, MOE_FP8_E4M3, torch.from_numpy(w["w_gate_up"]).to(device),
                             torch.from_numpy(w["w_down"]).to(device),
                             torch.from_numpy(w["w_gate_up_scales"]).to(device),
@@ -155,7 +168,8 @@ class MoEPipeline:
                       w_gate_up_scales=p(w.w_gate_up_scales), w_down=p(w.w_down),
                       w_down_scales=p(w.w_down_scales), h=p(b.h), h_scales=p(b.h_scales), y_perm=p(b.y_perm),
                       release_word=p(s.release_word), release_after_ns=s.release_after_ns,
-                      depends_on_op=s.depends_on_op, gap_ns=s.gap_ns, done_word=p(b.done_word))
+                      depends_on_op=s.depends_on_op, weight_layout=w.layout, gap_ns=s.gap_ns,
+                      done_word=p(b.done_word))
 
     # ---------------------------------------------------------------- the four calls
     def route(self, stream=None):

@@ -298,10 +298,31 @@ def test_buffers_reused_across_launches_with_new_inputs(dev):
         for s, ph in zip(specs, lay.phases):
             s.logits.copy_(torch.from_numpy(ph.logits).to(dev))
             s.x.copy_(bf16_tensor(ph.x, dev))
-        w.w_gate_up.copy_(bf16_tensor(lay.weights["w_gate_up"], dev))
-        w.w_down.copy_(bf16_tensor(lay.weights["w_down"], dev))
+        w.load(bf16_tensor(lay.weights["w_gate_up"], dev), bf16_tensor(lay.weights["w_down"], dev))
         pipe.run()
         torch.cuda.synchronize()
         assert pipe.statuses() == (0, 0)
         for i, ph in enumerate(lay.phases):
             _check_op(pipe, i, cfg, lay, ph)
+
+
+def test_pack_weights_layout(dev):
+    """moe_pack_weights writes the documented layout: chunk c of 32-row block b
+    holds, for q = 0..3 and lane = 0..63, row 32b + lane%32, columns
+    64c + (lane/32)*32 + 8q .. +8 (bit copy)."""
+    from paper_2607_18002_amd import ops
+    from paper_2607_18002_amd.pipeline import bf16_tensor, bits_of
+    rng = np.random.default_rng(31)
+    E, N, K = 3, 96, 192
+    w = rng.integers(0, 65535, size=(E, N, K), dtype=np.uint16)
+    got = bits_of(ops.moe_pack_weights(bf16_tensor(w, dev))).reshape(E, -1)
+    want = np.empty((E, N * K), dtype=np.uint16)
+    pos = 0
+    for b in range(N // 32):
+        for c in range(K // 64):
+            for q in range(4):
+                for lane in range(64):
+                    row, col = 32 * b + lane % 32, 64 * c + (lane // 32) * 32 + 8 * q
+                    want[:, pos:pos + 8] = w[:, row, col:col + 8]
+                    pos += 8
+    np.testing.assert_array_equal(got, want)
