@@ -205,10 +205,13 @@ def main():
     traced = MoEPipeline(specs, decode_quota_wg=args.quota, trace_capacity=1 << 18)
     traced.run()
     torch.cuda.synchronize()
-    lat = decode_latency(traced, specs)
     if args.dump_trace:
         np.save(args.dump_trace, traced.trace_records())
         np.save(args.dump_trace.replace(".npy", "_stats.npy"), traced.op_stats())
+    err, status = traced.statuses()
+    if err or status:
+        raise SystemExit(f"device status of the traced launch: permute={err} ffn={status}")
+    lat = decode_latency(traced, specs)
 
     dtype = cfg.dtype
     t_mfma = flops / (MFMA_PEAK_TFLOPS[dtype] * 1e12)

@@ -48,6 +48,8 @@ typedef int32_t moe_status_t;
 #define MOE_ERR_ABORTED     (-5) /* device: the abort word was set                             */
 #define MOE_ERR_TIMEOUT     (-6) /* device: a bounded wait exceeded its spin limit             */
 #define MOE_ERR_BAD_EXPERT  (-7) /* device: an expert id outside [-1, E_local)                 */
+#define MOE_ERR_INTERNAL    (-8) /* device: a scheduler invariant failed; the kernel stopped
+                                    before touching memory outside the op's buffers         */
 
 typedef int32_t moe_dtype_t;
 #define MOE_F32      0

@@ -17,6 +17,7 @@ MOE_ERR_HIP = -4
 MOE_ERR_ABORTED = -5
 MOE_ERR_TIMEOUT = -6
 MOE_ERR_BAD_EXPERT = -7
+MOE_ERR_INTERNAL = -8
 
 MOE_F32, MOE_BF16, MOE_FP8_E4M3 = 0, 1, 2
 MOE_PREFILL, MOE_DECODE = 0, 1

@@ -71,6 +71,7 @@ const char* moe_status_string(moe_status_t s) {
         case MOE_ERR_ABORTED: return "MOE_ERR_ABORTED";
         case MOE_ERR_TIMEOUT: return "MOE_ERR_TIMEOUT";
         case MOE_ERR_BAD_EXPERT: return "MOE_ERR_BAD_EXPERT";
+        case MOE_ERR_INTERNAL: return "MOE_ERR_INTERNAL";
         default: return "MOE_ERR_UNKNOWN";
     }
 }

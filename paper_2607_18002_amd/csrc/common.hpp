@@ -35,6 +35,11 @@ __device__ __forceinline__ void set_status(int32_t* status, int32_t code) {
 
 __device__ __forceinline__ uint64_t wall_ticks() { return wall_clock64(); }
 
+// Wait until every global store this wave issued has reached the L2 (vmcnt = 0;
+// expcnt and lgkmcnt left at their maxima).  A workgroup barrier alone does not
+// do this, so waves that hand stores to another wave's release call it first.
+__device__ __forceinline__ void wait_own_stores() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Hardware register XCC_ID: the XCD a wave runs on.
 __device__ __forceinline__ int xcc_id() {
     return __builtin_amdgcn_s_getreg((20) | (0 << 6) | (31 << 11)) & 0xF;

@@ -198,6 +198,18 @@ __device__ __forceinline__ void run_tile(const OpArg& op, int stage, int row0, i
 }
 
 // ----------------------------------------------------------------------------- scheduler
+// Per-workgroup LDS copy of each op's own-XCD queue (wave 0 only), taken at the
+// workgroup's first claim from that queue -- after the claim atomic returned, so
+// causally after the op became ACTIVE: the range [lo, lo + cnt) of row tiles and,
+// when cnt <= kTabCache, their table entries.  Later claims cost one atomic and
+// an LDS read.  lo = -1: not taken yet.
+constexpr int kTabCache = 64;
+struct TabCache {
+    uint64_t ent[MOE_MAX_OPS][kTabCache];
+    int32_t lo[MOE_MAX_OPS];
+    int32_t cnt[MOE_MAX_OPS];
+};
+
 // Command block written by wave 0 and read by the whole workgroup.
 struct Cmd {
     int32_t kind, op, stage, e, row0, rows32, nb, mtile, mblk, rows, t, pad;
@@ -231,14 +243,14 @@ __device__ void finish_op(const KArgs& a, int o, int total) {
 // Wave 0 at a tile boundary: commit the previous tile (if any), read the
 // decision words once, and pick the next action for the workgroup.
 __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, const Cmd& prev, bool have_prev,
-                         int64_t& idle) {
+                         int64_t& idle, TabCache* tab) {
     const int lane = threadIdx.x;
     Hdr* hdr = hdr_of(a.ws);
     OpDyn* dyn = dyn_of(a.ws);
     const OpStatic* sta = static_of(a.ws);
 
     // 1. commit: publish the tile's h / y, then count it (the completion count returns later)
-    int done_after = -1, prev_total = -1;
+    int done_after = -1;
     unsigned long long t_end = 0;
     if (have_prev && lane == 0) {
         t_end = wall_ticks();                                  // the tile's last store has completed
@@ -247,8 +259,7 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, const Cm
             int32_t* g1 = (int32_t*)(arr_of(a.ws) + a.op[prev.op].g1_off);
             __hip_atomic_fetch_add(g1 + prev.mtile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        done_after = add_relaxed_agent(&dyn[prev.op].done, 1) + 1;
-        prev_total = ld_relaxed_agent(&dyn[prev.op].total);
+        done_after = add_relaxed_agent(&dyn[prev.op].done, 1) + 1;    // result used after the polls
     }
 
     // 2. poll (all loads independent, issued together)
@@ -259,7 +270,9 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, const Cm
     const int state = has ? ld_relaxed_agent(&dyn[o_l].state) : ST_DONE;
     const int own_claim = has ? ld_relaxed_agent(&own->claim) : 0;
     const int own_size = has ? ld_relaxed_agent(&own->size) : 0;
+    const int total = has ? ld_relaxed_agent(&dyn[o_l].total) : 0;
     const int phase = has ? sta[o_l].phase : 0;
+    const int prev_total = __shfl(total, have_prev ? prev.op : 0, 64);
     int stop = 0, q = 0;
     if (lane == 0) {
         stop = ld_relaxed_agent(&hdr->stop);
@@ -366,18 +379,46 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, const Cm
                 if (t >= __shfl(sz, 0, 64)) continue;
                 src = who;
             }
-            if (lane == 0) {
-                const OpArg& op = a.op[o];
+            const OpArg& op = a.op[o];
+            const uint64_t* table = (const uint64_t*)(arr_of(a.ws) + op.table_off);
+            int m_lo, n_mt;
+            if (src == myx) {
+                if (tab->lo[o] < 0) {                                 // first claim from this op's own queue
+                    const XQueue* qs = xq_of(a.ws, o, myx);
+                    m_lo = ld_relaxed_agent(&qs->m_lo);
+                    n_mt = ld_relaxed_agent(&qs->n_mt);
+                    if (n_mt <= kTabCache && lane < n_mt) tab->ent[o][lane] = ld_relaxed_agent(table + m_lo + lane);
+                    if (lane == 0) { tab->lo[o] = m_lo; tab->cnt[o] = n_mt; }
+                } else {
+                    m_lo = tab->lo[o];
+                    n_mt = tab->cnt[o];
+                }
+            } else {
                 const XQueue* qs = xq_of(a.ws, o, src);
-                const int m_lo = ld_relaxed_agent(&qs->m_lo), n_mt = ld_relaxed_agent(&qs->n_mt);
+                m_lo = ld_relaxed_agent(&qs->m_lo);
+                n_mt = ld_relaxed_agent(&qs->n_mt);
+            }
+            if (lane == 0) {
                 int stage, mtile, nb;
                 queue_tile(t, n_mt, m_lo, op.n1, op.n2, stage, mtile, nb);
-                const uint64_t* table = (const uint64_t*)(arr_of(a.ws) + op.table_off);
-                const uint64_t ent = ld_relaxed_agent(table + mtile);
+                const int lo = tab->lo[o];
+                const int cnt = tab->cnt[o];
+                const uint64_t ent = (lo >= 0 && cnt <= kTabCache && mtile >= lo && mtile < lo + cnt)
+                                         ? tab->ent[o][mtile - lo] : ld_relaxed_agent(table + mtile);
                 const int rows = (int)((ent >> 24) & 0xFF);
+                const int e = (int)(ent & 0x3FF);
+                const int row0 = (int)(ent >> 32);
                 cmd->kind = CMD_TILE; cmd->op = o; cmd->stage = stage;
-                cmd->e = (int)(ent & 0x3FF); cmd->mblk = (int)((ent >> 10) & 0x3FFF);
-                cmd->row0 = (int)(ent >> 32); cmd->rows = rows; cmd->rows32 = (rows + 31) & ~31;
+                cmd->e = e; cmd->mblk = (int)((ent >> 10) & 0x3FFF);
+                cmd->row0 = row0; cmd->rows = rows; cmd->rows32 = (rows + 31) & ~31;
+                // The tile descriptor must address memory inside the op's buffers;
+                // if a scheduler invariant broke, stop instead of running the tile.
+                if (mtile < 0 || mtile >= op.max_mtiles || e >= op.E || rows < 1 || rows > op.mt || row0 < 0 ||
+                    (long)row0 + op.mt > (long)op.capacity || nb < 0 || nb >= (stage == 1 ? op.n1 : op.n2)) {
+                    set_status(a.status, MOE_ERR_INTERNAL);
+                    st_release_agent(&hdr->stop, 1);
+                    cmd->kind = CMD_EXIT;
+                }
                 cmd->nb = nb; cmd->mtile = mtile; cmd->t = t;
                 cmd->t_claim = wall_ticks();
                 if (t == 0) {
@@ -438,6 +479,7 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
             table[pos + mb] = pack_entry(e, mb, rows, off + mb * op.mt);
         }
     }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");       // each wave's entries, before ACTIVE is published
     __syncthreads();
     if (threadIdx.x == 0) {
         Hdr* hdr = hdr_of(a.ws);
@@ -478,8 +520,10 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
     __shared__ Cmd cmd;
     __shared__ int32_t scan[1024];
     __shared__ unsigned long long s_t0;
+    __shared__ TabCache tab;
     const int tid = threadIdx.x;
     const int wg = blockIdx.x;
+    if (tid < MOE_MAX_OPS) { tab.lo[tid] = -1; tab.cnt[tid] = 0; }
     if (tid == 0) {
         const unsigned long long now = wall_ticks();
         const unsigned long long prev = atomicCAS(&hdr_of(a.ws)->t0, 0ull, now);
@@ -491,7 +535,7 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
     Cmd prev;                                   // meaningful in wave 0 only
     bool have_prev = false;
     for (;;) {
-        if (tid < 64) boundary(a, t0, wg, &cmd, prev, have_prev, idle);
+        if (tid < 64) boundary(a, t0, wg, &cmd, prev, have_prev, idle, &tab);
         __syncthreads();
         const int kind = cmd.kind;
         have_prev = false;
@@ -517,7 +561,10 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
         if (tid < 64) prev = cmd;
         __syncthreads();                                      // every thread has read cmd
         run_tile(a.op[o], stage, row0, rows32, nb, e, lds);
-        __syncthreads();                                      // the whole tile is written before the commit
+        // Wave 0's release at the commit writes back this XCD's L2; the barrier does
+        // not wait for global stores, so each wave first lets its own reach the L2.
+        wait_own_stores();
+        __syncthreads();
         have_prev = true;
     }
 }

@@ -52,6 +52,7 @@ def test_status_strings():
     assert ops.status_string(0) == "MOE_OK"
     assert ops.status_string(-3) == "MOE_ERR_CAPACITY"
     assert ops.status_string(-7) == "MOE_ERR_BAD_EXPERT"
+    assert ops.status_string(-8) == "MOE_ERR_INTERNAL"
 
 
 def test_x_moe_matches_oracle():
