@@ -12,10 +12,14 @@ layer is done (+20 us for decode), decode quota 64 of 256 workgroups.
 
 Prints ONE JSON line.  value = routed-expert TFLOP/s of the whole step
 (6*H*I flop per local routed row).  roofline = the persistent FFN kernel
-against the HBM bound (algorithmic bytes: each op's active expert weights
-once plus x_perm in and y_perm out), timed with HIP events on its stream.
-cpu_baseline = the float64 CPU oracle on a bounded sample of the same
-workload, on this host's cores.
+against its bound (algorithmic bytes: each op's active expert weights once
+plus x_perm in and y_perm out; flops 6*H*I per row), its mean duration over
+the timed steps from HIP events on its stream; traffic = HBM bytes per launch
+from the committed rocprofv3 counter record when it was taken on the current
+kernel sources, else null.  decode_tile_latency comes from one extra traced
+launch, and from a launch of the decode ops alone (same inputs and release
+chain) for the latency without prefill load.  cpu_baseline = the float64 CPU
+oracle over the whole workload, on this host's cores.
 """
 from __future__ import annotations
 
@@ -44,6 +48,8 @@ def parse():
     ap.add_argument("--quota", type=int, default=64, help="decode quota q in workgroups")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--dump-trace", default=None, help="write the traced launch's per-tile records (.npy)")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after the run, copy this many MiB device to device 3 times (counter calibration)")
     return ap.parse_args()
 
 
@@ -135,28 +141,59 @@ def decode_latency(pipe, specs):
 
 
 def cpu_baseline(cfg, layers):
-    """The oracle as it stands, on a bounded sample of the same workload:
-    every operation of layer 0 (all of its tokens, every step of the path)."""
+    """The oracle as it stands, on the same workload: every operation of every
+    layer (all tokens, every step of the path), on this host's cores."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
         cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     except Exception:  # pragma: no cover
         cores = len(os.sched_getaffinity(0))
-    lay = layers[0]
     flops, rows, dt = 0.0, 0, 0.0
-    for ph in lay.phases:
-        t = time.perf_counter()
-        res = oracle.moe_local_share(ph.logits, ph.x, lay.weights, cfg.top_k, cfg.local_begin, cfg.E_local, 128,
-                                     x_scales=ph.x_scales)
-        dt += time.perf_counter() - t
-        R = int(res["perm"].counts.sum())
-        rows += R
-        flops += 6.0 * cfg.H * cfg.I * R
-    desc = " + ".join(f"{ph.T} {ph.phase}" for ph in lay.phases)
+    for lay in layers:
+        for ph in lay.phases:
+            t = time.perf_counter()
+            res = oracle.moe_local_share(ph.logits, ph.x, lay.weights, cfg.top_k, cfg.local_begin, cfg.E_local,
+                                         128, x_scales=ph.x_scales)
+            dt += time.perf_counter() - t
+            R = int(res["perm"].counts.sum())
+            rows += R
+            flops += 6.0 * cfg.H * cfg.I * R
+    desc = " + ".join(f"{ph.T} {ph.phase}" for ph in layers[0].phases)
     return {"value": round(flops / dt / 1e12, 5), "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"layer 0 of {cfg.n_layers}: {desc} tokens ({rows} local rows), every step, float64 numpy, "
-                      f"{dt:.1f} s"}
+            "sample": f"the whole workload: {cfg.n_layers} layer(s) x ({desc} tokens), {rows} local rows, every "
+                      f"step of the path, float64 numpy, {dt:.1f} s"}
+
+
+def traffic_record(workload):
+    """HBM bytes per launch recorded by rocprofv3 counters for this workload,
+    or None when no record exists or the kernel sources changed since."""
+    from paper_2607_18002_amd.build import ffn_kernel_hash
+    path = os.path.join(ROOT, "profiles", f"apk_kernel_traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as f:
+        for line in f:
+            if " = " in line:
+                k, v = line.split(" = ", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_hash") != ffn_kernel_hash() or kv.get("workload") != workload:
+        return None
+    return float(kv["traffic_bytes_per_launch"])
+
+
+def phase_subset(specs, phase):
+    """The ops of one phase alone, with dependencies renumbered (same inputs)."""
+    import dataclasses
+    keep = [i for i, s in enumerate(specs) if s.phase == phase]
+    remap = {old: new for new, old in enumerate(keep)}
+    out = []
+    for i in keep:
+        s = specs[i]
+        dep = remap.get(s.depends_on_op, -1)
+        out.append(dataclasses.replace(s, depends_on_op=dep))
+    return out
 
 
 def main():
@@ -197,7 +234,8 @@ def main():
         pipe.combine()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
-    ffn_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    ffn_all = np.array([a.elapsed_time(b) for a, b in ev])
+    ffn_ms = float(np.mean(ffn_all))
     ms_step = wall * 1000.0 / args.steps
 
     flops, abytes, rows = algorithmic_work(pipe, cfg)
@@ -212,6 +250,32 @@ def main():
     if err or status:
         raise SystemExit(f"device status of the traced launch: permute={err} ffn={status}")
     lat = decode_latency(traced, specs)
+    del traced
+    # the decode ops alone (same inputs, same release chain): the latency without prefill load
+    excl = None
+    dec_specs = phase_subset(specs, 1)
+    if lat is not None and dec_specs and len(dec_specs) < len(specs):
+        alone = MoEPipeline(dec_specs, decode_quota_wg=args.quota, trace_capacity=1 << 16)
+        alone.run()
+        alone.run()
+        torch.cuda.synchronize()
+        err, status = alone.statuses()
+        if err or status:
+            raise SystemExit(f"device status of the decode-only launch: permute={err} ffn={status}")
+        excl = decode_latency(alone, dec_specs)
+        del alone
+        lat["exclusive_tile_p50_us"] = excl["tile_p50_us"]
+        lat["exclusive_tile_p99_us"] = excl["tile_p99_us"]
+        lat["exclusive_decode_op_latency_us"] = excl["decode_op_latency_us"]
+        lat["p99_ratio_loaded_vs_exclusive"] = round(lat["tile_p99_us"] / excl["tile_p99_us"], 3)
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     dtype = cfg.dtype
     t_mfma = flops / (MFMA_PEAK_TFLOPS[dtype] * 1e12)
@@ -225,8 +289,13 @@ def main():
         ach = flops / (ffn_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": MFMA_PEAK_TFLOPS[dtype], "unit": "TFLOP/s",
                 "frac": round(ach / MFMA_PEAK_TFLOPS[dtype], 4), "traffic": None}
+    tb = traffic_record(cfg.name)
+    roof["traffic"] = tb
+    if tb is not None:
+        roof["traffic_vs_alg_bytes"] = round(tb / abytes, 3)
     roof["kernel"] = "apk_kernel (moe_grouped_ffn_persistent)"
     roof["kernel_ms"] = round(ffn_ms, 4)
+    roof["kernel_ms_p10_p50_p90"] = [round(float(np.percentile(ffn_all, q)), 4) for q in (10, 50, 90)]
     roof["alg_bytes"] = abytes
     roof["alg_flops"] = flops
 

@@ -20,6 +20,10 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libmoe_apk.so")
 SOURCES = ["api.cpp", "route.hip", "permute.hip", "combine.hip", "ffn.hip", "pack.hip"]
+# Every source file the persistent FFN kernel is compiled from (hashed to tie
+# recorded hardware-counter figures to the kernel they were taken on).
+FFN_KERNEL_SOURCES = ["paper_2607_18002_amd/csrc/ffn.hip", "paper_2607_18002_amd/csrc/tile_bf16.hpp",
+                      "paper_2607_18002_amd/csrc/common.hpp", "include/moe_apk.h"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -46,6 +50,16 @@ def _compile(src: str, verbose: bool) -> str:
     if verbose and lines:
         print("\n".join(lines))
     return obj
+
+
+def ffn_kernel_hash() -> str:
+    """sha256 (first 16 hex digits) over the persistent FFN kernel's sources."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in FFN_KERNEL_SOURCES:
+        with open(os.path.join(ROOT, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
 
 
 def build(verbose: bool = False) -> str:
