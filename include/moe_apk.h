@@ -168,13 +168,17 @@ typedef struct moe_op_desc {
                                      op's last tile has committed                        */
 } moe_op_desc;
 
-/* Per-tile trace record (times in device wall-clock ticks, 100 MHz on gfx950). */
+/* Per-tile trace record (times in device wall-clock ticks, 100 MHz on gfx950).
+ * A tile's life: the scheduling step that picked it began at t_boundary (it
+ * first committed the workgroup's previous tile), its polls of the scheduler
+ * words had returned at t_polled, the tile was claimed at t_claim, its
+ * dependencies were met at t_start, and its outputs were committed at t_end. */
 typedef struct moe_trace_rec {
     int16_t op, stage;        /* stage 1 = GEMM-1 (+activation), 2 = GEMM-2             */
     int16_t wg, xcc;          /* workgroup index and the XCD it ran on                  */
     int32_t expert, mblk;     /* local expert and row-block within its segment          */
     int32_t nblk, rows;       /* column block and valid rows in the tile               */
-    uint64_t t_claim, t_start, t_end; /* claimed, dependencies met, committed           */
+    uint64_t t_boundary, t_polled, t_claim, t_start, t_end;
 } moe_trace_rec;
 
 /* Per-op statistics written by the persistent kernel (times in wall-clock ticks). */

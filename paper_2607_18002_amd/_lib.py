@@ -55,7 +55,8 @@ class TraceRec(C.Structure):
     _fields_ = [
         ("op", C.c_int16), ("stage", C.c_int16), ("wg", C.c_int16), ("xcc", C.c_int16),
         ("expert", _i32), ("mblk", _i32), ("nblk", _i32), ("rows", _i32),
-        ("t_claim", C.c_uint64), ("t_start", C.c_uint64), ("t_end", C.c_uint64),
+        ("t_boundary", C.c_uint64), ("t_polled", C.c_uint64), ("t_claim", C.c_uint64),
+        ("t_start", C.c_uint64), ("t_end", C.c_uint64),
     ]
 
 

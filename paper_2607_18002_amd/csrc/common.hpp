@@ -20,10 +20,9 @@ constexpr int kWave = 64;
 
 // ----------------------------------------------------------------------------- conversions
 // float -> bf16 bits, round to nearest even (finite inputs).
+// float -> bf16 bits, round to nearest even (gfx950's v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t f2bf_bits(float f) {
-    uint32_t u = __float_as_uint(f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return u >> 16;
+    return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)f);
 }
 __device__ __forceinline__ float bf_bits2f(uint32_t h) { return __uint_as_float(h << 16); }
 

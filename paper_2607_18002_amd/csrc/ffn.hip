@@ -17,19 +17,23 @@
 // and broadcasts it through LDS; the whole workgroup runs the tile.  Each
 // operation's tiles are numbered GEMM-1 tiles first (row-tile major), then
 // GEMM-2 tiles; a GEMM-2 tile waits (bounded) on a per-row-tile counter that
-// GEMM-1 tiles bump after an agent-scope release.  Every claimed tile belongs
+// GEMM-1 tiles bump once their h rows are visible.  Every claimed tile belongs
 // to a running workgroup, so the dependency waits cannot deadlock.
 //
 // Coherence across the eight XCD-private L2 caches.  An agent-scope acquire
 // invalidates the whole L2 of the XCD, which would destroy weight reuse if it
 // sat on the polling path.  So every scheduler word is read with relaxed
-// device-scope atomics (coherent loads that invalidate nothing), producers
-// write back their L2 (release fence) before bumping a counter, and consumers
-// of h never invalidate: within one launch a workgroup reads an h row only
-// after the row's GEMM-1 tiles committed and never before, so no L1/L2 can
-// hold a stale copy of it (launch boundaries make earlier launches' copies
-// coherent).  The one acquire per operation is taken by the workgroup that
-// completes it, before it publishes the done word.
+// device-scope atomics (coherent loads that invalidate nothing).  Tile outputs
+// (h, y_perm) are written with device-coherent stores (sc1) that reach the
+// coherence point by themselves, and every wave waits for its own stores
+// before the workgroup barrier that precedes the commit, so bumping a counter
+// needs no L2 write-back of its own.  Consumers of h never invalidate: within
+// one launch a workgroup reads an h row only after the row's GEMM-1 tiles
+// committed and never before, so no L1/L2 can hold a stale copy of it (launch
+// boundaries make earlier launches' copies coherent).  Row-tile tables, which
+// are written with ordinary stores, are published with a release by every
+// wave that wrote them.  The one acquire per operation is taken by the
+// workgroup that completes it, before it publishes the done word.
 #include <cstring>
 
 #include "tile_bf16.hpp"
@@ -213,7 +217,7 @@ struct TabCache {
 // Command block written by wave 0 and read by the whole workgroup.
 struct Cmd {
     int32_t kind, op, stage, e, row0, rows32, nb, mtile, mblk, rows, t, pad;
-    unsigned long long t_claim, t_start;
+    unsigned long long t_boundary, t_polled, t_claim, t_start;
 };
 
 // Lane 0: an op's last tile has committed.  The acquire takes in every other
@@ -242,19 +246,24 @@ __device__ void finish_op(const KArgs& a, int o, int total) {
 
 // Wave 0 at a tile boundary: commit the previous tile (if any), read the
 // decision words once, and pick the next action for the workgroup.
-__device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, const Cmd& prev, bool have_prev,
-                         int64_t& idle, TabCache* tab) {
+__device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool have_prev, int64_t& idle,
+                         TabCache* tab) {
     const int lane = threadIdx.x;
     Hdr* hdr = hdr_of(a.ws);
     OpDyn* dyn = dyn_of(a.ws);
     const OpStatic* sta = static_of(a.ws);
+    // The command block still describes the tile just run (it is rewritten
+    // only below), so the previous tile is read from LDS rather than kept in
+    // registers across the tile.
+    Cmd prev;
+    if (have_prev) prev = *cmd;
+    const unsigned long long t_boundary = wall_ticks();
 
     // 1. commit: publish the tile's h / y, then count it (the completion count returns later)
     int done_after = -1;
     unsigned long long t_end = 0;
     if (have_prev && lane == 0) {
-        t_end = wall_ticks();                                  // the tile's last store has completed
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+        t_end = wall_ticks();   // every wave's device-coherent stores of the tile have completed
         if (prev.stage == 1) {
             int32_t* g1 = (int32_t*)(arr_of(a.ws) + a.op[prev.op].g1_off);
             __hip_atomic_fetch_add(g1 + prev.mtile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -297,7 +306,8 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, const Cm
                     moe_trace_rec r;
                     r.op = (int16_t)prev.op; r.stage = (int16_t)prev.stage; r.wg = (int16_t)wg;
                     r.xcc = (int16_t)xcc_id(); r.expert = prev.e; r.mblk = prev.mblk; r.nblk = prev.nb;
-                    r.rows = prev.rows; r.t_claim = prev.t_claim; r.t_start = prev.t_start; r.t_end = t_end;
+                    r.rows = prev.rows; r.t_boundary = prev.t_boundary; r.t_polled = prev.t_polled;
+                    r.t_claim = prev.t_claim; r.t_start = prev.t_start; r.t_end = t_end;
                     a.trace[idx] = r;
                 }
             }
@@ -420,6 +430,8 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, const Cm
                     cmd->kind = CMD_EXIT;
                 }
                 cmd->nb = nb; cmd->mtile = mtile; cmd->t = t;
+                cmd->t_boundary = t_boundary;
+                cmd->t_polled = now;
                 cmd->t_claim = wall_ticks();
                 if (t == 0) {
                     unsigned long long zero = 0;
@@ -532,10 +544,9 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
     __syncthreads();
     const uint64_t t0 = s_t0;
     int64_t idle = 0;
-    Cmd prev;                                   // meaningful in wave 0 only
     bool have_prev = false;
     for (;;) {
-        if (tid < 64) boundary(a, t0, wg, &cmd, prev, have_prev, idle, &tab);
+        if (tid < 64) boundary(a, t0, wg, &cmd, have_prev, idle, &tab);
         __syncthreads();
         const int kind = cmd.kind;
         have_prev = false;
@@ -558,7 +569,6 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
         const int rows32 = __builtin_amdgcn_readfirstlane(cmd.rows32);
         const int nb = __builtin_amdgcn_readfirstlane(cmd.nb);
         const int e = __builtin_amdgcn_readfirstlane(cmd.e);
-        if (tid < 64) prev = cmd;
         __syncthreads();                                      // every thread has read cmd
         run_tile(a.op[o], stage, row0, rows32, nb, e, lds);
         // Wave 0's release at the commit writes back this XCD's L2; the barrier does

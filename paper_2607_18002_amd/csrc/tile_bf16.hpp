@@ -3,11 +3,14 @@
 // One 256-thread workgroup computes a BM x BN output tile over the full K.
 // The four waves split the BN columns (BN/4 each) and all share the BM rows:
 //  * B (weight rows, K-contiguous) is private to a wave, so it streams from
-//    global memory straight into MFMA operand registers, double-buffered
-//    (two K steps in flight per wave), with no LDS round trip;
-//  * A (activation rows, shared by the four waves) is staged through LDS,
-//    double-buffered, with rows padded by 16 bytes so an operand read is free
-//    of bank conflicts.
+//    global memory straight into MFMA operand registers through a ring of
+//    DEPTH K-step buffers (loads issued DEPTH steps ahead of their MFMAs), with
+//    no LDS round trip.  Tiles with few valid rows do little MFMA work per K
+//    step and have registers to spare, so they run a deeper ring: that is what
+//    keeps enough weight bytes in flight to stream at HBM speed;
+//  * A (activation rows, shared by the four waves) is loaded into registers
+//    two K steps ahead and staged through double-buffered LDS, with rows padded
+//    by 16 bytes so an operand read is free of bank conflicts.
 // K order: K runs in 64-element chunks; in each chunk lanes 0-31 take
 // elements [0, 32) and lanes 32-63 take [32, 64), 8 per MFMA, so MFMA kk of a
 // K step covers chunk kk/4, elements (lane/32)*32 + (kk%4)*8 .. +8.  A and B
@@ -33,7 +36,11 @@ struct TileShape {
     static constexpr int KK = BK / 16;               // MFMAs along K per K step
     static constexpr int LDS_ROW = BK * 2 + 16;      // bytes per LDS row of A
     static constexpr int A_STAGE = BM * LDS_ROW;
-    static constexpr int LDS = 2 * A_STAGE;
+    // Epilogue staging: each wave's bf16 output block, rows padded by 16 bytes
+    // (the widest case, WCOLS columns, is reserved for GLU tiles too).
+    static constexpr int OUT_ROW = WCOLS * 2 + 16;
+    static constexpr int OUT_STAGE = BM * OUT_ROW;
+    static constexpr int LDS = 2 * A_STAGE > 4 * OUT_STAGE ? 2 * A_STAGE : 4 * OUT_STAGE;
     static constexpr int CPR = BK / 8;               // 16-byte chunks per A row and K step
     static constexpr int RPP = 256 / CPR;            // A rows loaded per pass of 256 threads
     static_assert(NBW >= 2 && NBW % 2 == 0, "GLU needs a gate and an up block per wave");
@@ -43,6 +50,9 @@ struct TileShape {
 template <class S, int MACT>
 struct TileRegs {
     static constexpr int CA = MACT * 32 / S::RPP;    // A chunks per thread and K step
+    // K steps of B in flight: 32 VGPRs per step; the MFMA accumulators take
+    // MACT * NBW * 16 registers, so fewer valid rows leave room for more steps.
+    static constexpr int DEPTH = MACT == 1 ? 8 : MACT == 2 ? 6 : 4;
 };
 
 // Raw buffer loads: the tile's base address lives in an SGPR descriptor, the
@@ -50,6 +60,7 @@ struct TileRegs {
 // offset in the instruction, so a load needs no address arithmetic.  The
 // descriptor's size bounds the tile's extent (reads past it return zero).
 constexpr int kBufferWord3 = 0x00020000;   // gfx9-family raw buffer: 32-bit data format, no swizzle
+constexpr int kStoreDevice = 16;           // cache policy sc1: the store is coherent at device scope
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kBufferWord3);
@@ -163,66 +174,82 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    u32x4 ra[CA];
-    bf16x8 rb0[S::NBW][S::KK], rb1[S::NBW][S::KK];
+    constexpr int D = TileRegs<S, MACT>::DEPTH;
+    u32x4 ra[2][CA];                                  // A of steps s+1 and s+2 (slot = step & 1)
+    bf16x8 rb[D][S::NBW][S::KK];                      // B of steps s .. s+D-1 (slot = step % D)
     const int nk = K / S::BK;
     constexpr int KB = S::BK * 2;                     // bytes per K step of a row-major row
     constexpr int KBB = PACKED ? S::BK * 64 : KB;     // bytes per K step of a weight fragment stream
     static_assert(S::BK % 64 == 0, "K steps are whole 64-element chunks");
+    static_assert(D % 2 == 0, "the A slots (step & 1) repeat within one pass of the B ring");
 
-    // K is a multiple of 2*BK (checked by the host), so the loop runs whole pairs of K steps.
-    // A loads are issued before the B loads of the same K step: staging A into
-    // LDS then waits only for A (vmcnt counts in issue order) and leaves the
-    // later B loads in flight.
-    load_a<CA>(ra, Ab, aoff, 0);
-    load_b<S, PACKED>(rb0, Bb, boff, 0);
-    store_a<CA>(lds0, ra, alds);
-    load_a<CA>(ra, Ab, aoff, KB);
-    load_b<S, PACKED>(rb1, Bb, boff, KBB);
+    // Prologue: A of step 0 into LDS stage 0; A of steps 1, 2 and B of steps
+    // 0 .. D-1 in flight.  A loads go before the B loads of the same step, so
+    // waiting for an A slot (vmcnt counts in issue order) leaves later B loads
+    // in flight.
+    load_a<CA>(ra[0], Ab, aoff, 0);
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+        if (d < nk) load_b<S, PACKED>(rb[d], Bb, boff, d * KBB);
+    store_a<CA>(lds0, ra[0], alds);
+    if (1 < nk) load_a<CA>(ra[1], Ab, aoff, KB);
+    if (2 < nk) load_a<CA>(ra[0], Ab, aoff, 2 * KB);
     __syncthreads();
-    for (int s = 0; s < nk; s += 2) {
-        const bool more = s + 2 < nk;
-        mma_step<S, MACT>(acc, rb0, lds0, lane);
-        store_a<CA>(lds1, ra, alds);
-        if (more) {
-            load_a<CA>(ra, Ab, aoff, (s + 2) * KB);
-            load_b<S, PACKED>(rb0, Bb, boff, (s + 2) * KBB);
+    for (int s0 = 0; s0 < nk; s0 += D) {
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            const int s = s0 + d;                     // uniform; d, s & 1 and s % D are compile-time
+            if (s < nk) {
+                mma_step<S, MACT>(acc, rb[d], (d & 1) ? lds1 : lds0, lane);
+                if (s + 1 < nk) store_a<CA>((d & 1) ? lds0 : lds1, ra[(d + 1) & 1], alds);
+                if (s + D < nk) load_b<S, PACKED>(rb[d], Bb, boff, (s + D) * KBB);
+                if (s + 3 < nk) load_a<CA>(ra[(d + 1) & 1], Ab, aoff, (s + 3) * KB);
+                __syncthreads();
+            }
         }
-        __syncthreads();
-        mma_step<S, MACT>(acc, rb1, lds1, lane);
-        if (more) {
-            store_a<CA>(lds0, ra, alds);
-            load_a<CA>(ra, Ab, aoff, (s + 3) * KB);
-            load_b<S, PACKED>(rb1, Bb, boff, (s + 3) * KBB);
-        }
-        __syncthreads();
     }
 
     // Epilogue.  32x32 accumulator layout: lane holds column (lane & 31) and
-    // rows (r/4)*8 + (lane/32)*4 + r%4 of its block, r = 0..15.
+    // rows (r/4)*8 + (lane/32)*4 + r%4 of its block, r = 0..15.  Each wave
+    // writes its bf16 block into its own LDS region (the A stages are free: the
+    // last K step ended with a barrier), reads it back row-wise and writes
+    // whole 16-byte row chunks with device-coherent stores (sc1): the stores
+    // reach the coherence point by themselves, so the tile needs no L2
+    // write-back before it is committed.  A wave reads back only what it wrote
+    // itself, and LDS keeps one wave's operations in order.
+    constexpr int OC = GLU ? S::WCOLS / 2 : S::WCOLS;      // output columns per wave
+    constexpr int ORB = OC * 2 + 16;                       // staged row pitch in bytes
+    char* stg = lds + wn * S::OUT_STAGE;
 #pragma unroll
     for (int i = 0; i < MACT; ++i) {
         const int row_base = 32 * i + (lane >> 5) * 4;
-        if (GLU) {
 #pragma unroll
-            for (int j = 0; j < S::NBW / 2; ++j) {
-                const int col = wn * (S::WCOLS / 2) + 32 * j + (lane & 31);
+        for (int j = 0; j < OC / 32; ++j) {
+            const int col = 32 * j + (lane & 31);
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
+            for (int r = 0; r < 16; ++r) {
+                float v;
+                if (GLU) {
                     const float g = acc[i][j][r], u = acc[i][j + S::NBW / 2][r];
-                    const float hv = g / (1.f + __expf(-g)) * u;
-                    out[(long)(row_base + (r >> 2) * 8 + (r & 3)) * ldo + col] = (uint16_t)f2bf_bits(hv);
+                    v = g / (1.f + __expf(-g)) * u;
+                } else {
+                    v = acc[i][j][r];
                 }
-            }
-        } else {
-#pragma unroll
-            for (int j = 0; j < S::NBW; ++j) {
-                const int col = wn * S::WCOLS + 32 * j + (lane & 31);
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    out[(long)(row_base + (r >> 2) * 8 + (r & 3)) * ldo + col] = (uint16_t)f2bf_bits(acc[i][j][r]);
+                *(uint16_t*)(stg + (row_base + (r >> 2) * 8 + (r & 3)) * ORB + col * 2) = (uint16_t)f2bf_bits(v);
             }
         }
+    }
+    constexpr int CPO = OC * 2 / 16;                       // 16-byte chunks per output row
+    constexpr int RPI = 64 / CPO;                          // rows per store instruction
+    static_assert(64 % CPO == 0 && 32 % RPI == 0, "a store pass stays inside one 32-row block");
+    const __amdgpu_buffer_rsrc_t Ob = make_rsrc(out, (uint32_t)(MACT * 32) * (uint32_t)ldo * 2u);
+    const int orow = lane / CPO, och = lane % CPO;
+    const uint32_t ooff = (uint32_t)orow * (uint32_t)ldo * 2u + (uint32_t)(wn * OC + och * 8) * 2u;
+#pragma unroll
+    for (int p = 0; p < MACT * 32 / RPI; ++p) {
+        const u32x4 v = *(const u32x4*)(stg + (p * RPI + orow) * ORB + och * 16);
+        __builtin_amdgcn_raw_buffer_store_b128(v, Ob, (int)ooff, (int)((uint32_t)(p * RPI) * (uint32_t)ldo * 2u),
+                                               kStoreDevice);
     }
 }
 
