@@ -236,16 +236,20 @@ moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32_t n_ops,
                                         int32_t* status_word, void* stream);
 
 /* Weight layout streamed by the FFN kernel (one-time conversion, outside the
- * hot path).  A bf16 matrix [N, K] (N a multiple of 32, K a multiple of 64) is
- * cut into 32-row blocks; a block is K/64 chunks of 4 KB; chunk c of block b
- * holds, for q = 0..3 and lane = 0..63 in that order, the 8 elements
- *   row 32*b + lane%32,  columns 64*c + (lane/32)*32 + 8*q .. +8,
- * i.e. exactly the 16 bytes lane `lane` feeds to the q-th 32x32x16 MFMA of
- * the chunk, so each 64-lane load reads 1 KB contiguous.  The packed matrix
- * has the same size as the row-major one and block b starts at the same byte
- * offset as row 32*b.
+ * hot path).  A matrix [N, K] is cut into 32-row blocks of 4 KB chunks, each
+ * chunk holding exactly the 16-byte pieces lanes 0..63 feed to the MFMAs of
+ * that chunk, so each 64-lane load reads 1 KB contiguous:
+ *  bf16: chunk c (64 elements of K) of block b holds, for q = 0..3 and
+ *        lane = 0..63 in that order, row 32*b + lane%32, elements
+ *        64*c + (lane/32)*32 + 8*q .. +8 (one 32x32x16 MFMA per q);
+ *  fp8 e4m3: chunk c (128 elements of K, one scale block) holds, for
+ *        kk = 0..1, half = 0..1 and lane = 0..63 in that order, row
+ *        32*b + lane%32, elements 128*c + 64*kk + (lane/32)*32 + 16*half .. +16
+ *        (one 32x32x64 MFMA per kk).
+ * The packed matrix has the same size as the row-major one and block b starts
+ * at the same byte offset as row 32*b.  Scales (fp8) are not moved.
  *  src  [E, N, K] row-major (device);  dst  same size (device, not aliasing src)
- * Limits: dtype MOE_BF16; N % 32 == 0; K % 64 == 0. */
+ * Limits: dtype MOE_BF16 (K % 64 == 0) or MOE_FP8_E4M3 (K % 128 == 0); N % 32 == 0. */
 moe_status_t moe_pack_weights(const void* src, void* dst, int32_t E, int32_t N, int32_t K, moe_dtype_t dtype,
                               void* stream);
 

@@ -9,11 +9,17 @@ of the paper it follows.
 from .moe import (  # noqa: F401
     bf16_to_f64,
     e4m3_to_f64,
+    e4m3_quantize,
+    quantize_rows,
     dequant_rows,
     dequant_weight,
     route,
     permute,
     expert_ffn,
+    expert_hidden,
+    expert_down,
+    grouped_hidden,
+    grouped_down,
     grouped_ffn,
     combine,
     moe_local_share,

@@ -26,6 +26,13 @@ What the paper fixes, and the readings taken where it is silent:
   activation fused into one kernel).  Reading: SwiGLU,
   h = silu(x Wg^T) * (x Wu^T), out = h Wd^T, silu(z) = z / (1 + e^-z), with
   gate rows 0..I-1 and up rows I..2I-1 of the [2I, H] gate/up matrix.
+* fp8 path (Evaluation, "Implementation": the fp8 deployment).  Readings:
+  OCP E4M3FN codes; activations carry one fp32 scale per row and 128
+  columns, weights one per 128 x 128 block; the stored intermediate h is
+  re-quantized per row and 128 columns with scale = max(amax, 1e-4) / 448,
+  rounding to nearest even and saturating at +-448.  By default the oracle
+  keeps h unquantized (the reference the tolerance is stated against); with
+  h_fp8 it applies that quantization (quantize_rows).
 * Combine (Background, "MoE LLM Inference" and "Large-scale MoE LLM
   Serving"): y[t] = sum over local slots j (ascending) of w[t,j] * out[row].
   A token with no local slot gets exactly zero.
@@ -72,6 +79,36 @@ _E4M3 = _e4m3_table()
 
 def e4m3_to_f64(codes: np.ndarray) -> np.ndarray:
     return _E4M3[np.asarray(codes, dtype=np.uint8)]
+
+
+_E4M3_POS = _E4M3[:0x7F]          # the finite non-negative codes 0x00..0x7E, ascending in value
+
+
+def e4m3_quantize(v: np.ndarray) -> np.ndarray:
+    """float64 -> OCP E4M3FN codes: the nearest representable value, ties to
+    the even mantissa, magnitudes beyond 448 saturate to +-448.  Sign from
+    the sign bit of the input (so -0.0 gives the negative-zero code)."""
+    v = np.asarray(v, dtype=np.float64)
+    a = np.minimum(np.abs(v), 448.0)
+    hi = np.clip(np.searchsorted(_E4M3_POS, a, side="left"), 0, 0x7E)   # first code with value >= a
+    lo = np.maximum(hi - 1, 0)
+    d_hi = _E4M3_POS[hi] - a
+    d_lo = a - _E4M3_POS[lo]
+    pick_lo = (d_lo < d_hi) | ((d_lo == d_hi) & (lo % 2 == 0))
+    code = np.where(pick_lo, lo, hi).astype(np.uint8)
+    return np.where(np.signbit(v), code | 0x80, code).astype(np.uint8)
+
+
+def quantize_rows(v: np.ndarray, group: int = 128, floor: float = 1e-4, qmax: float = 448.0):
+    """Per-row, per-`group`-column fp8 quantization of the intermediate h
+    (reading taken for the paper's fp8 path): scale = max(amax, floor) / qmax,
+    code = e4m3(v / scale).  Returns (codes uint8, scales float64)."""
+    v = np.asarray(v, dtype=np.float64)
+    T, n = v.shape
+    g = v.reshape(T, n // group, group)
+    scale = np.maximum(np.abs(g).max(axis=2), floor) / qmax
+    codes = e4m3_quantize(g / scale[:, :, None]).reshape(T, n)
+    return codes, scale
 
 
 def dequant_rows(x: np.ndarray, x_scales: Optional[np.ndarray] = None, group: int = 128) -> np.ndarray:
@@ -177,13 +214,30 @@ def permute(ids: np.ndarray, E_local: int, row_align: int, x: Optional[np.ndarra
 
 # ----------------------------------------------------------------------------- steps 3-5: expert FFN
 
-def expert_ffn(x_rows: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray, w_down: np.ndarray) -> np.ndarray:
-    """SwiGLU expert on float64 rows: x [m,H], Wg/Wu [I,H], Wd [H,I] -> [m,H]."""
+def expert_hidden(x_rows: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray) -> np.ndarray:
+    """GEMM-1 and the activation on float64 rows: h = silu(x Wg^T) * (x Wu^T), [m,I]."""
     g = x_rows @ w_gate.T
     u = x_rows @ w_up.T
     with np.errstate(over="ignore"):
         h = g / (1.0 + np.exp(-g)) * u
+    return h
+
+
+def expert_down(h: np.ndarray, w_down: np.ndarray) -> np.ndarray:
+    """GEMM-2 on float64 rows: h [m,I] . Wd^T -> [m,H]."""
     return h @ w_down.T
+
+
+def expert_ffn(x_rows: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray, w_down: np.ndarray,
+               h_fp8: bool = False) -> np.ndarray:
+    """SwiGLU expert on float64 rows: x [m,H], Wg/Wu [I,H], Wd [H,I] -> [m,H].
+    h_fp8: h passes through the fp8 intermediate format (quantize_rows, then
+    dequantized) before the down projection, as the fp8 path stores it."""
+    h = expert_hidden(x_rows, w_gate, w_up)
+    if h_fp8:
+        codes, sc = quantize_rows(h)
+        h = dequant_rows(codes, sc)
+    return expert_down(h, w_down)
 
 
 def _expert_weights(weights: dict, e: int, I: int):
@@ -194,8 +248,36 @@ def _expert_weights(weights: dict, e: int, I: int):
     return gu[:I], gu[I:], wd
 
 
+def grouped_hidden(x_perm_f64: np.ndarray, counts: np.ndarray, offsets: np.ndarray, weights: dict) -> np.ndarray:
+    """h of every expert's segment (GEMM-1 and the activation); other rows zero."""
+    I = weights["w_down"].shape[2]
+    out = np.zeros((x_perm_f64.shape[0], I), dtype=np.float64)
+    for e in range(len(counts)):
+        m = int(counts[e])
+        if m == 0:
+            continue
+        r0 = int(offsets[e])
+        wg, wu, _ = _expert_weights(weights, e, I)
+        out[r0:r0 + m] = expert_hidden(x_perm_f64[r0:r0 + m], wg, wu)
+    return out
+
+
+def grouped_down(h_rows: np.ndarray, counts: np.ndarray, offsets: np.ndarray, weights: dict) -> np.ndarray:
+    """GEMM-2 of every expert's segment from given h rows; other rows zero."""
+    I = weights["w_down"].shape[2]
+    out = np.zeros((h_rows.shape[0], weights["w_down"].shape[1]), dtype=np.float64)
+    for e in range(len(counts)):
+        m = int(counts[e])
+        if m == 0:
+            continue
+        r0 = int(offsets[e])
+        _, _, wd = _expert_weights(weights, e, I)
+        out[r0:r0 + m] = expert_down(h_rows[r0:r0 + m], wd)
+    return out
+
+
 def grouped_ffn(x_perm_f64: np.ndarray, counts: np.ndarray, offsets: np.ndarray, weights: dict,
-                experts: Optional[list] = None) -> np.ndarray:
+                experts: Optional[list] = None, h_fp8: bool = False) -> np.ndarray:
     """Expert FFN over each expert's segment; padding rows and rows of experts
     not listed stay zero.  x_perm_f64 is the dequantized gathered input."""
     E_local = len(counts)
@@ -207,7 +289,7 @@ def grouped_ffn(x_perm_f64: np.ndarray, counts: np.ndarray, offsets: np.ndarray,
             continue
         r0 = int(offsets[e])
         wg, wu, wd = _expert_weights(weights, e, I)
-        out[r0:r0 + m] = expert_ffn(x_perm_f64[r0:r0 + m], wg, wu, wd)
+        out[r0:r0 + m] = expert_ffn(x_perm_f64[r0:r0 + m], wg, wu, wd, h_fp8)
     return out
 
 
@@ -228,18 +310,18 @@ def combine(y_perm: np.ndarray, assign_to_row: np.ndarray, w: np.ndarray, T: int
 # ----------------------------------------------------------------------------- whole local share
 
 def moe_local_share(logits, x, weights: dict, top_k: int, local_begin: int, E_local: int,
-                    row_align: int, x_scales=None, capacity=None) -> dict:
+                    row_align: int, x_scales=None, capacity=None, h_fp8: bool = False) -> dict:
     """Every step in order; returns all intermediates (float results in float64)."""
     ids, w = route(logits, top_k, local_begin, E_local)
     p = permute(ids, E_local, row_align, x, capacity, x_scales)
     xp = dequant_rows(p.x_perm, p.x_perm_scales)
-    y_perm = grouped_ffn(xp, p.counts, p.offsets, weights)
+    y_perm = grouped_ffn(xp, p.counts, p.offsets, weights, h_fp8=h_fp8)
     y = combine(y_perm, p.assign_to_row, w, ids.shape[0], top_k)
     return dict(ids=ids, w=w, perm=p, y_perm=y_perm, y=y)
 
 
 def token_output(x_row_f64: np.ndarray, ids_row: np.ndarray, w_row: np.ndarray, weights: dict,
-                 cache: Optional[dict] = None) -> np.ndarray:
+                 cache: Optional[dict] = None, h_fp8: bool = False) -> np.ndarray:
     """y for one token, straight from the definition: sum over its local slots
     of w * FFN_e(x).  `cache` may hold dequantized expert weights by id."""
     I = weights["w_down"].shape[2]
@@ -254,7 +336,7 @@ def token_output(x_row_f64: np.ndarray, ids_row: np.ndarray, w_row: np.ndarray, 
             wg, wu, wd = _expert_weights(weights, e, I)
             if cache is not None:
                 cache[e] = (wg, wu, wd)
-        y += w_row[j] * expert_ffn(x_row_f64[None, :], wg, wu, wd)[0]
+        y += w_row[j] * expert_ffn(x_row_f64[None, :], wg, wu, wd, h_fp8)[0]
     return y
 
 

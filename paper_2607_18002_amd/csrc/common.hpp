@@ -15,11 +15,11 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
 
 // ----------------------------------------------------------------------------- conversions
-// float -> bf16 bits, round to nearest even (finite inputs).
 // float -> bf16 bits, round to nearest even (gfx950's v_cvt_pk_bf16_f32).
 __device__ __forceinline__ uint32_t f2bf_bits(float f) {
     return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)f);

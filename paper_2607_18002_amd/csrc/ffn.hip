@@ -37,29 +37,36 @@
 #include <cstring>
 
 #include "tile_bf16.hpp"
+#include "tile_fp8.hpp"
 
 namespace {
 
 using namespace moeapk;
 
-using ShapeP = TileShape<128, 256, 64>;    // prefill: 128 x 256 tile, K step 64
-using ShapeD = TileShape<128, 256, 64>;    // decode : 128 x 256 tile, K step 64
-constexpr int kLdsBytes = ShapeP::LDS > ShapeD::LDS ? ShapeP::LDS : ShapeD::LDS;
+using ShapeP = TileShape<128, 256, 64>;    // bf16 prefill: 128 x 256 tile, K step 64
+using ShapeD = TileShape<128, 256, 64>;    // bf16 decode : 128 x 256 tile, K step 64
+using ShapeF8 = TileShapeF8<64, 256>;      // fp8 (both phases): 64 x 256 tile, K step 128 (one scale block)
+constexpr int kMax2(int a, int b) { return a > b ? a : b; }
+constexpr int kLdsBytes = kMax2(kMax2(ShapeP::LDS, ShapeD::LDS), ShapeF8::LDS);
 constexpr int kRowAlign = 128;             // M_t of both bf16 classes
 constexpr int kMaxRowTiles = 1 << 14;      // per op (14-bit field of a table entry)
 
-enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1 };
+enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1, CLS_FP8 = 2 };
 enum : int32_t { ST_WAIT = 0, ST_INIT = 1, ST_ACTIVE = 2, ST_DONE = 3 };
 enum : int32_t { CMD_EXIT = 0, CMD_TILE = 1, CMD_INST = 2, CMD_IDLE = 3 };
 
 struct OpArg {
     const int32_t* counts;
     const int32_t* offsets;
-    const uint16_t* x;
+    const uint16_t* x;         // bf16 elements, or fp8 codes (bytes) for CLS_FP8
     const uint16_t* wgu;
     const uint16_t* wd;
     uint16_t* h;
     uint16_t* y;
+    const float* xs;           // fp8 scales: x_perm, gate/up weights, down weights, h
+    const float* wgus;
+    const float* wds;
+    float* hs;
     uint32_t* done_word;
     int32_t cls, phase, layer, E, H, I, capacity, mt, n1, n2, max_mtiles, table_off, g1_off, pad;
 };
@@ -195,10 +202,35 @@ __device__ __forceinline__ void run_tile_cls(const OpArg& op, int stage, int row
     }
 }
 
+// fp8: GEMM-1 tiles cover 128 h columns (one h scale group), GEMM-2 tiles 256 y columns.
+__device__ __forceinline__ void run_tile_fp8(const OpArg& op, int stage, int row0, int rows32, int nb, int e,
+                                             char* lds) {
+    using S = ShapeF8;
+    const long H = op.H, I = op.I;
+    const uint8_t* x = (const uint8_t*)op.x;
+    uint8_t* h = (uint8_t*)op.h;
+    if (stage == 1) {
+        const int n0 = nb * (S::BN / 2);
+        gemm_tile_fp8_rows<S, true>(rows32, x + row0 * H, (int)H, op.xs + row0 * (H / 128),
+                                    (const uint8_t*)op.wgu + (long)e * 2 * I * H + (long)n0 * H, n0, (int)I,
+                                    op.wgus + (long)e * (2 * I / 128) * (H / 128), (int)H, h + row0 * I + n0, (int)I,
+                                    op.hs + row0 * (I / 128) + nb, (int)(I / 128), lds);
+    } else {
+        const int n0 = nb * S::BN;
+        gemm_tile_fp8_rows<S, false>(rows32, h + row0 * I, (int)I, op.hs + row0 * (I / 128),
+                                     (const uint8_t*)op.wd + (long)e * H * I + (long)n0 * I, n0, 0,
+                                     op.wds + (long)e * (H / 128) * (I / 128), (int)I, op.y + row0 * H + n0, (int)H,
+                                     nullptr, 0, lds);
+    }
+}
+
 __device__ __forceinline__ void run_tile(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds) {
     // Both bf16 classes currently share one tile shape.
     static_assert(ShapeP::BM == ShapeD::BM && ShapeP::BN == ShapeD::BN && ShapeP::BK == ShapeD::BK, "one shape");
-    run_tile_cls<ShapeP>(op, stage, row0, rows32, nb, e, lds);
+    if (op.cls == CLS_FP8)
+        run_tile_fp8(op, stage, row0, rows32, nb, e, lds);
+    else
+        run_tile_cls<ShapeP>(op, stage, row0, rows32, nb, e, lds);
 }
 
 // ----------------------------------------------------------------------------- scheduler
@@ -580,9 +612,16 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
 }
 
 struct ClassInfo {
-    int bn, bk;
+    int bm, bn, bk;
 };
-ClassInfo class_info(int cls) { return cls == CLS_P_BF16 ? ClassInfo{ShapeP::BN, ShapeP::BK} : ClassInfo{ShapeD::BN, ShapeD::BK}; }
+ClassInfo class_info(int cls) {
+    if (cls == CLS_FP8) return ClassInfo{ShapeF8::BM, ShapeF8::BN, ShapeF8::BK};
+    return cls == CLS_P_BF16 ? ClassInfo{kRowAlign, ShapeP::BN, ShapeP::BK} : ClassInfo{kRowAlign, ShapeD::BN, ShapeD::BK};
+}
+int class_of(int phase, int dtype) {
+    if (dtype == MOE_FP8_E4M3) return CLS_FP8;
+    return phase == MOE_PREFILL ? CLS_P_BF16 : CLS_D_BF16;
+}
 
 // Per op: a row-tile table (8 bytes per row tile) and GEMM-1 counters (4 bytes
 // per row tile), each padded to 256 bytes so no L2 line is shared between ops.
@@ -604,16 +643,16 @@ size_t ws_bytes_for(const moe_op_desc* ops, int n_ops) {
 
 extern "C" int32_t moe_ffn_row_align(moe_phase_t phase, moe_dtype_t dtype) {
     if (phase != MOE_PREFILL && phase != MOE_DECODE) return -1;
-    if (dtype != MOE_BF16) return -2;
-    return kRowAlign;
+    if (dtype != MOE_BF16 && dtype != MOE_FP8_E4M3) return -2;
+    return class_info(class_of(phase, dtype)).bm;
 }
 
 extern "C" moe_status_t moe_ffn_tile_shape(moe_phase_t phase, moe_dtype_t dtype, int32_t* bm, int32_t* bn,
                                            int32_t* bk) {
-    if ((phase != MOE_PREFILL && phase != MOE_DECODE) || dtype != MOE_BF16)
+    if ((phase != MOE_PREFILL && phase != MOE_DECODE) || (dtype != MOE_BF16 && dtype != MOE_FP8_E4M3))
         return moeapk_host::fail(MOE_ERR_UNSUPPORTED, "moe_ffn_tile_shape: phase %d dtype %d", phase, dtype);
-    const ClassInfo ci = class_info(phase == MOE_PREFILL ? CLS_P_BF16 : CLS_D_BF16);
-    if (bm) *bm = kRowAlign;
+    const ClassInfo ci = class_info(class_of(phase, dtype));
+    if (bm) *bm = ci.bm;
     if (bn) *bn = ci.bn;
     if (bk) *bk = ci.bk;
     return MOE_OK;
@@ -643,10 +682,11 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
     for (int o = 0; o < n_ops; ++o) {
         const moe_op_desc& d = ops[o];
         if (d.phase != MOE_PREFILL && d.phase != MOE_DECODE) return fail(MOE_ERR_INVALID_ARG, "op %d: bad phase %d", o, d.phase);
-        if (d.dtype != MOE_BF16) return fail(MOE_ERR_UNSUPPORTED, "op %d: dtype %d not supported by the FFN kernel", o, d.dtype);
+        if (d.dtype != MOE_BF16 && d.dtype != MOE_FP8_E4M3)
+            return fail(MOE_ERR_UNSUPPORTED, "op %d: dtype %d not supported by the FFN kernel", o, d.dtype);
         if (d.weight_layout != MOE_LAYOUT_PACKED)
             return fail(MOE_ERR_UNSUPPORTED, "op %d: weights must be in MOE_LAYOUT_PACKED (moe_pack_weights)", o);
-        const int cls = d.phase == MOE_PREFILL ? CLS_P_BF16 : CLS_D_BF16;
+        const int cls = class_of(d.phase, d.dtype);
         const ClassInfo ci = class_info(cls);
         if (d.E_local < 1 || d.E_local > 1024) return fail(MOE_ERR_UNSUPPORTED, "op %d: E_local=%d outside [1,1024]", o, d.E_local);
         // H and I are the K of a GEMM (whole pairs of K steps) and split into whole output tiles
@@ -654,8 +694,14 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
             return fail(MOE_ERR_UNSUPPORTED, "op %d: H=%d must be a positive multiple of 256", o, d.H);
         if (d.I < ci.bn / 2 || d.I % (ci.bn / 2) != 0 || d.I % (2 * ci.bk) != 0 || d.I % 256 != 0)
             return fail(MOE_ERR_UNSUPPORTED, "op %d: I=%d must be a positive multiple of 256", o, d.I);
-        if (d.row_align != kRowAlign)
-            return fail(MOE_ERR_INVALID_ARG, "op %d: row_align=%d but the FFN tile height is %d", o, d.row_align, kRowAlign);
+        if (cls == CLS_FP8) {
+            if (d.H > 128 * ShapeF8::MAX_KB || d.I > 128 * ShapeF8::MAX_KB)
+                return fail(MOE_ERR_UNSUPPORTED, "op %d: fp8 H, I must be at most %d", o, 128 * ShapeF8::MAX_KB);
+            if (!d.x_perm_scales || !d.w_gate_up_scales || !d.w_down_scales || !d.h_scales)
+                return fail(MOE_ERR_INVALID_ARG, "op %d: fp8 op without its scale buffers", o);
+        }
+        if (d.row_align != ci.bm)
+            return fail(MOE_ERR_INVALID_ARG, "op %d: row_align=%d but the FFN tile height is %d", o, d.row_align, ci.bm);
         if (d.capacity < d.row_align) return fail(MOE_ERR_CAPACITY, "op %d: capacity=%d below one tile", o, d.capacity);
         if ((int64_t)d.capacity * d.H > INT32_MAX || (int64_t)d.capacity * d.I > INT32_MAX)
             return fail(MOE_ERR_UNSUPPORTED, "op %d: capacity*H exceeds 2^31 elements", o);
@@ -674,6 +720,10 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
         p.wd = (const uint16_t*)d.w_down;
         p.h = (uint16_t*)d.h;
         p.y = (uint16_t*)d.y_perm;
+        p.xs = d.x_perm_scales;
+        p.wgus = d.w_gate_up_scales;
+        p.wds = d.w_down_scales;
+        p.hs = d.h_scales;
         p.done_word = d.done_word;
         p.cls = cls;
         p.phase = d.phase;

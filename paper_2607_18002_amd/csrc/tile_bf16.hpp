@@ -50,9 +50,13 @@ struct TileShape {
 template <class S, int MACT>
 struct TileRegs {
     static constexpr int CA = MACT * 32 / S::RPP;    // A chunks per thread and K step
-    // K steps of B in flight: 32 VGPRs per step; the MFMA accumulators take
-    // MACT * NBW * 16 registers, so fewer valid rows leave room for more steps.
-    static constexpr int DEPTH = MACT == 1 ? 8 : MACT == 2 ? 6 : 4;
+    // K steps of B in flight.  One step of B takes NBW * KK * 4 registers; the
+    // MFMA accumulators take MACT * NBW * 16, so fewer valid rows leave room
+    // for more steps (budget: 128 registers at 4 row blocks, 256 at 1).
+    static constexpr int B_STEP_REGS = S::NBW * S::KK * 4;
+    static constexpr int B_BUDGET = MACT == 1 ? 256 : MACT == 2 ? 192 : 128;
+    static constexpr int DEPTH_RAW = B_BUDGET / B_STEP_REGS;
+    static constexpr int DEPTH = DEPTH_RAW >= 8 ? 8 : DEPTH_RAW < 2 ? 2 : (DEPTH_RAW & ~1);
 };
 
 // Raw buffer loads: the tile's base address lives in an SGPR descriptor, the

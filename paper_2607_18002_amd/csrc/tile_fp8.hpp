@@ -1,0 +1,280 @@
+// fp8 (OCP E4M3FN) grouped-GEMM tile on gfx950 with fp32 block scales.
+//
+// Block-scaled product (weights in 128 x 128 blocks, activations in 1 x 128
+// groups along K):
+//   out[t][n] = sum_kb sx[t][kb] * sw[n/128][kb] * sum_{k in block kb} xq[t][k] * wq[n][k].
+// The inner sum of each 128-element K block is two v_mfma_scale_f32_32x32x64_f8f6f4
+// with unit E8M0 scales (127), i.e. a plain fp8 product accumulated in fp32,
+// into a fresh accumulator; the block is then added to the running fp32 total
+// with its two exact fp32 scales.  The scales are arbitrary fp32 values, which
+// the MFMA's power-of-two block scales cannot express.
+//
+// Orientation: the MFMA's A operand is weight rows (output features) and its B
+// operand is activation rows (tokens).  A lane's 32x32 accumulator then holds
+// one token (column lane % 32) and 16 features of one 32-feature block, which
+// all share one activation scale and one weight scale: folding a block into
+// the total costs one multiply and 16 FMAs per lane.
+//
+// Workgroup: 4 waves; wave w owns features [w*WCOLS, (w+1)*WCOLS) (NBW blocks
+// of 32) for all BM tokens.  Weights stream global -> registers through a ring
+// of DEPTH K steps (moe_pack_weights' fp8 layout: per 32-row block and 128-K
+// chunk, [kk][half][lane][16 B]); activations are staged through double-
+// buffered LDS (rows padded by 16 bytes); the tile's activation scales are
+// staged in LDS once, as [K/128][BM].  MFMA K order: MFMA kk of a step covers
+// elements kk*64 + (lane/32)*32 + [0, 32) of the block, in both operands.
+#pragma once
+
+#include "tile_bf16.hpp"
+
+namespace moeapk {
+
+template <int BM_, int BN_>
+struct TileShapeF8 {
+    static constexpr int BM = BM_, BN = BN_, BK = 128;
+    static constexpr int MB = BM / 32;                // 32-token blocks
+    static constexpr int WCOLS = BN / 4;              // features per wave
+    static constexpr int NBW = WCOLS / 32;            // 32-feature blocks per wave
+    static constexpr int KK = BK / 64;                // MFMAs along K per step
+    static constexpr int LDS_ROW = BK + 16;           // bytes per staged activation row
+    static constexpr int A_STAGE = BM * LDS_ROW;
+    static constexpr int MAX_KB = 64;                 // K <= 8192
+    static constexpr int SX_OFF = 2 * A_STAGE;        // activation scales [kb][BM] (f32)
+    static constexpr int SX_BYTES = MAX_KB * BM * 4;
+    static constexpr int H_ROW = (BN / 2) * 4 + 16;   // GLU epilogue: fp32 h row of BN/2 features
+    static constexpr int OUT_ROW = WCOLS * 2 + 16;    // GEMM-2 epilogue: per-wave bf16 row
+    static constexpr int EPI = BM * H_ROW > 4 * BM * OUT_ROW ? BM * H_ROW : 4 * BM * OUT_ROW;
+    static constexpr int LDS = SX_OFF + SX_BYTES > EPI ? SX_OFF + SX_BYTES : EPI;
+    static constexpr int CPR = BK / 16;               // 16-byte chunks per activation row and step
+    static constexpr int RPP = 256 / CPR;             // activation rows per load pass
+    static_assert(NBW == 2, "GLU pairs one gate and one up block per wave");
+    static_assert(RPP <= 32 && 32 % RPP == 0, "a load pass stays inside one 32-row block");
+};
+
+template <class S, int MACT>
+struct TileRegsF8 {
+    static constexpr int CA = MACT * 32 / S::RPP;     // activation chunks per thread and step
+    static constexpr int DEPTH = MACT == 1 ? 4 : 2;   // weight steps in flight (32 VGPRs each)
+};
+
+// Weight operands of one K step: per block j and MFMA kk, 32 bytes per lane
+// (two 16-byte halves, each a 1 KB contiguous wave load).
+template <class S>
+__device__ __forceinline__ void load_w8(i32x8 (&rw)[S::NBW][S::KK], __amdgpu_buffer_rsrc_t B,
+                                        const uint32_t (&boff)[S::NBW], int k0b) {
+#pragma unroll
+    for (int j = 0; j < S::NBW; ++j)
+#pragma unroll
+        for (int kk = 0; kk < S::KK; ++kk) {
+            const u32x4 lo = __builtin_amdgcn_raw_buffer_load_b128(B, (int)(boff[j] + kk * 2048), k0b, 0);
+            const u32x4 hi = __builtin_amdgcn_raw_buffer_load_b128(B, (int)(boff[j] + kk * 2048 + 1024), k0b, 0);
+            rw[j][kk] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+        }
+}
+
+// A   : activation codes of tile row 0, lda bytes per row; rows [0, 32*MACT) are read
+// asc : activation scales of tile row 0 (f32), K/128 per row
+// B   : packed weight codes, first row n0 of the tile (a multiple of 32);
+//       GLU: gate rows n0 + [0, BN/2) and up rows n0 + up_rows + [0, BN/2)
+// wsc : weight scales of the expert, [N/128][K/128]
+// GLU : out = h codes (ldo bytes per row), osc = h scales (ldsc floats per row);
+//       else out = bf16 rows (ldo elements per row)
+template <class S, bool GLU, int MACT>
+__device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int lda, const float* __restrict__ asc,
+                                              const uint8_t* __restrict__ B, int n0, int up_rows,
+                                              const float* __restrict__ wsc, int K, void* __restrict__ out, int ldo,
+                                              float* __restrict__ osc, int ldsc, char* lds) {
+    constexpr int CA = TileRegsF8<S, MACT>::CA;
+    constexpr int D = TileRegsF8<S, MACT>::DEPTH;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wn = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int nkb = K / S::BK;
+
+    // weight rows of this wave's feature blocks, and their scale rows
+    uint32_t boff[S::NBW];
+    const float* sw[S::NBW];
+#pragma unroll
+    for (int j = 0; j < S::NBW; ++j) {
+        const int row = GLU ? (j == 0 ? 0 : up_rows) + wn * (S::WCOLS / 2) : wn * S::WCOLS + 32 * j;
+        boff[j] = (uint32_t)row * (uint32_t)K + (uint32_t)(lane * 16);
+        sw[j] = wsc + (long)((n0 + row) / 128) * nkb;
+    }
+    uint32_t aoff[CA], alds[CA];
+#pragma unroll
+    for (int i = 0; i < CA; ++i) {
+        const int idx = tid + 256 * i, r = idx / S::CPR, c = idx % S::CPR;
+        aoff[i] = (uint32_t)r * (uint32_t)lda + c * 16;
+        alds[i] = r * S::LDS_ROW + c * 16;
+    }
+    const __amdgpu_buffer_rsrc_t Ab = make_rsrc(A, (uint32_t)(MACT * 32) * (uint32_t)lda);
+    const __amdgpu_buffer_rsrc_t Bb =
+        make_rsrc(B, (uint32_t)(GLU ? up_rows + S::BN / 2 : S::BN) * (uint32_t)K);
+    char* lds0 = lds;
+    char* lds1 = lds + S::A_STAGE;
+    float* sx = (float*)(lds + S::SX_OFF);
+
+    // activation scales of the tile, transposed to [kb][token]
+    for (int idx = tid; idx < MACT * 32 * nkb; idx += 256) {
+        const int r = idx / nkb, kb = idx - r * nkb;
+        sx[kb * S::BM + r] = asc[(long)r * nkb + kb];
+    }
+
+    f32x16 tot[S::NBW][MACT];
+#pragma unroll
+    for (int j = 0; j < S::NBW; ++j)
+#pragma unroll
+        for (int i = 0; i < MACT; ++i)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) tot[j][i][r] = 0.f;
+
+    u32x4 ra[CA];
+    i32x8 rw[D][S::NBW][S::KK];
+    const int arow = (lane & 31) * S::LDS_ROW + (lane >> 5) * 32;      // lanes 32-63: +32 bytes
+    constexpr int KBW = 32 * S::BK;                                   // bytes per K step of a 32-row block
+
+    load_a<CA>(ra, Ab, aoff, 0);
+#pragma unroll
+    for (int d = 0; d < D; ++d)
+        if (d < nkb) load_w8<S>(rw[d], Bb, boff, d * KBW);
+    store_a<CA>(lds0, ra, alds);
+    if (1 < nkb) load_a<CA>(ra, Ab, aoff, S::BK);
+    __syncthreads();
+    for (int s0 = 0; s0 < nkb; s0 += D) {
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            const int s = s0 + d;                                      // uniform; d and s & 1 are compile-time
+            if (s < nkb) {
+                const char* cur = (d & 1) ? lds1 : lds0;
+                f32x16 part[S::NBW][MACT];
+#pragma unroll
+                for (int kk = 0; kk < S::KK; ++kk) {
+                    i32x8 xa[MACT];
+#pragma unroll
+                    for (int i = 0; i < MACT; ++i) {
+                        const char* p = cur + arow + i * 32 * S::LDS_ROW + kk * 64;
+                        const u32x4 lo = *(const u32x4*)p, hi = *(const u32x4*)(p + 16);
+                        xa[i] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+                    }
+#pragma unroll
+                    for (int j = 0; j < S::NBW; ++j)
+#pragma unroll
+                        for (int i = 0; i < MACT; ++i) {
+                            const f32x16 c0 = {};
+                            part[j][i] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                                rw[d][j][kk], xa[i], kk == 0 ? c0 : part[j][i], 0, 0, 0, 127, 0, 127);
+                        }
+                }
+                if (s + 1 < nkb) store_a<CA>((d & 1) ? lds0 : lds1, ra, alds);
+                if (s + D < nkb) load_w8<S>(rw[d], Bb, boff, (s + D) * KBW);
+                if (s + 2 < nkb) load_a<CA>(ra, Ab, aoff, (s + 2) * S::BK);
+                // fold the block in: one scale per (feature block, token) pair
+#pragma unroll
+                for (int i = 0; i < MACT; ++i) {
+                    const float xs = sx[s * S::BM + 32 * i + (lane & 31)];
+#pragma unroll
+                    for (int j = 0; j < S::NBW; ++j) {
+                        const float c = xs * sw[j][s];
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) tot[j][i][r] = __builtin_fmaf(part[j][i][r], c, tot[j][i][r]);
+                    }
+                }
+                __syncthreads();
+            }
+        }
+    }
+
+    // Accumulator layout: lane holds token 32*i + (lane & 31) and features
+    // 32*j + (r/4)*8 + (lane/32)*4 + r%4 of its wave's columns, r = 0..15.
+    if (GLU) {
+        // h = silu(g) * u in fp32 -> LDS [token][BN/2]; then each token row's
+        // BN/2 = 128 values (one scale group) are quantized with
+        // scale = max(amax, 1e-4) / 448, clamped to +-448 before the convert
+        // (the hardware convert does not saturate).
+        static_assert(S::BN / 2 == 128, "one h scale group per GEMM-1 tile");
+        char* hb = lds;
+#pragma unroll
+        for (int i = 0; i < MACT; ++i) {
+            const int t = 32 * i + (lane & 31);
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                f32x4 v;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const float gt = tot[0][i][g * 4 + q], up = tot[1][i][g * 4 + q];
+                    v[q] = gt / (1.f + __expf(-gt)) * up;
+                }
+                *(f32x4*)(hb + t * S::H_ROW + (wn * 32 + g * 8 + (lane >> 5) * 4) * 4) = v;
+            }
+        }
+        __syncthreads();
+        const int t = tid >> 2, qq = tid & 3;                       // 4 threads per token row, 32 values each
+        if (t < MACT * 32) {
+            const f32x4* src = (const f32x4*)(hb + t * S::H_ROW + qq * 128);
+            f32x4 v[8];
+            float amax = 0.f;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                v[k] = src[k];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) amax = fmaxf(amax, fabsf(v[k][q]));
+            }
+            amax = fmaxf(amax, __shfl_xor(amax, 1, 64));
+            amax = fmaxf(amax, __shfl_xor(amax, 2, 64));
+            const float m = fmaxf(amax, 1e-4f);
+            const float inv = 448.f / m;
+            u32x4 code[2];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                float c4[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) c4[q] = fminf(fmaxf(v[k][q] * inv, -448.f), 448.f);
+                int w = __builtin_amdgcn_cvt_pk_fp8_f32(c4[0], c4[1], 0, false);
+                w = __builtin_amdgcn_cvt_pk_fp8_f32(c4[2], c4[3], w, true);
+                code[k >> 2][k & 3] = (uint32_t)w;
+            }
+            const __amdgpu_buffer_rsrc_t Ob = make_rsrc(out, (uint32_t)(MACT * 32) * (uint32_t)ldo);
+            const int o = t * ldo + qq * 32;
+            __builtin_amdgcn_raw_buffer_store_b128(code[0], Ob, o, 0, kStoreDevice);
+            __builtin_amdgcn_raw_buffer_store_b128(code[1], Ob, o + 16, 0, kStoreDevice);
+            if (qq == 0) __hip_atomic_store(osc + (long)t * ldsc, m / 448.f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    } else {
+        // bf16 rows through per-wave LDS staging, written as 16-byte row chunks
+        char* stg = lds + wn * (S::BM * S::OUT_ROW);
+#pragma unroll
+        for (int i = 0; i < MACT; ++i) {
+            const int t = 32 * i + (lane & 31);
+#pragma unroll
+            for (int j = 0; j < S::NBW; ++j)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const uint32_t p0 = f2bf_bits(tot[j][i][g * 4 + 0]) | (f2bf_bits(tot[j][i][g * 4 + 1]) << 16);
+                    const uint32_t p1 = f2bf_bits(tot[j][i][g * 4 + 2]) | (f2bf_bits(tot[j][i][g * 4 + 3]) << 16);
+                    *(u32x2*)(stg + t * S::OUT_ROW + (32 * j + g * 8 + (lane >> 5) * 4) * 2) = u32x2{p0, p1};
+                }
+        }
+        constexpr int CPO = S::WCOLS * 2 / 16;                     // 16-byte chunks per staged row
+        constexpr int RPI = 64 / CPO;                              // rows per store instruction
+        const __amdgpu_buffer_rsrc_t Ob = make_rsrc(out, (uint32_t)(MACT * 32) * (uint32_t)ldo * 2u);
+        const int orow = lane / CPO, och = lane % CPO;
+        const uint32_t ooff = (uint32_t)orow * (uint32_t)ldo * 2u + (uint32_t)(wn * S::WCOLS + och * 8) * 2u;
+#pragma unroll
+        for (int p = 0; p < MACT * 32 / RPI; ++p) {
+            const u32x4 v = *(const u32x4*)(stg + (p * RPI + orow) * S::OUT_ROW + och * 16);
+            __builtin_amdgcn_raw_buffer_store_b128(v, Ob, (int)ooff, (int)((uint32_t)(p * RPI) * (uint32_t)ldo * 2u),
+                                                   kStoreDevice);
+        }
+    }
+}
+
+template <class S, bool GLU>
+__device__ __forceinline__ void gemm_tile_fp8_rows(int rows32, const uint8_t* A, int lda, const float* asc,
+                                                   const uint8_t* B, int n0, int up_rows, const float* wsc, int K,
+                                                   void* out, int ldo, float* osc, int ldsc, char* lds) {
+    static_assert(S::MB == 2, "dispatch written for 64-row tiles");
+    if (rows32 > 32)
+        gemm_tile_fp8<S, GLU, 2>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds);
+    else
+        gemm_tile_fp8<S, GLU, 1>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds);
+}
+
+}  // namespace moeapk

@@ -113,7 +113,8 @@ def moe_combine(y_perm: torch.Tensor, assign_to_row: torch.Tensor, topk_w: torch
 
 
 def moe_pack_weights(src: torch.Tensor, dst: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """[E, N, K] bf16 row-major -> the FFN kernel's packed weight layout (same shape and size)."""
+    """[E, N, K] bf16 or fp8-code (uint8) row-major -> the FFN kernel's packed
+    weight layout (same shape and size)."""
     lib = load_library()
     E, N, K = src.shape
     if dst is None:

@@ -60,10 +60,13 @@ class LayerWeights:
             lw.load(gu, wd)
             del gu, wd
             return lw
-        return LayerWeights(H, I, MOE_FP8_E4M3, torch.from_numpy(w["w_gate_up"]).to(device),
-                            torch.from_numpy(w["w_down"]).to(device),
-                            torch.from_numpy(w["w_gate_up_scales"]).to(device),
-                            torch.from_numpy(w["w_down_scales"]).to(device))
+        gu, wd = torch.from_numpy(w["w_gate_up"]).to(device), torch.from_numpy(w["w_down"]).to(device)
+        lw = LayerWeights(H, I, MOE_FP8_E4M3, torch.empty_like(gu), torch.empty_like(wd),
+                          torch.from_numpy(np.ascontiguousarray(w["w_gate_up_scales"], dtype=np.float32)).to(device),
+                          torch.from_numpy(np.ascontiguousarray(w["w_down_scales"], dtype=np.float32)).to(device))
+        lw.load(gu, wd)
+        del gu, wd
+        return lw
 
 
 @dataclass

@@ -81,6 +81,9 @@ def test_row_align_and_workspace_queries():
     from paper_2607_18002_amd import _lib, ops
     assert ops.moe_ffn_row_align(_lib.MOE_PREFILL, _lib.MOE_BF16) == 128
     assert ops.moe_ffn_row_align(_lib.MOE_DECODE, _lib.MOE_BF16) == 128
+    assert ops.moe_ffn_row_align(_lib.MOE_PREFILL, _lib.MOE_FP8_E4M3) == 64
+    assert ops.moe_ffn_row_align(_lib.MOE_DECODE, _lib.MOE_FP8_E4M3) == 64
+    assert ops.moe_ffn_tile_shape(_lib.MOE_PREFILL, _lib.MOE_FP8_E4M3) == (64, 256, 128)
     assert ops.moe_ffn_row_align(7, _lib.MOE_BF16) < 0
     for ph in (_lib.MOE_PREFILL, _lib.MOE_DECODE):
         bm, bn, bk = ops.moe_ffn_tile_shape(ph, _lib.MOE_BF16)

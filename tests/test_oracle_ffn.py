@@ -158,3 +158,19 @@ def test_fp8_path_dequantizes_same_codes():
     h = g / (1 + np.exp(-g)) * g
     y = I * h * 0.125
     np.testing.assert_allclose(r8["y"], np.full((T, H), y), rtol=1e-13)
+
+
+def test_two_stage_split_composes_to_the_ffn():
+    """grouped_down(grouped_hidden(x)) is grouped_ffn(x), segment by segment,
+    with rows outside the segments zero in both stages."""
+    rng = np.random.default_rng(21)
+    E, H, I = 3, 64, 96
+    counts = np.array([5, 0, 7])
+    offsets = np.array([0, 8, 8, 16])
+    x = rng.standard_normal((16, H))
+    w = {"w_gate_up": bf16_bits((rng.standard_normal((E, 2 * I, H)) * 0.1).astype(np.float32)),
+         "w_down": bf16_bits((rng.standard_normal((E, H, I)) * 0.1).astype(np.float32))}
+    h = oracle.grouped_hidden(x, counts, offsets, w)
+    y = oracle.grouped_down(h, counts, offsets, w)
+    np.testing.assert_allclose(y, oracle.grouped_ffn(x, counts, offsets, w), rtol=1e-12, atol=1e-12)
+    assert np.all(h[5:8] == 0) and np.all(y[5:8] == 0) and np.all(y[15:] == 0)

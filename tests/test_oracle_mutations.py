@@ -26,12 +26,13 @@ def _load(path, name):
     return mod
 
 
-PINS = {n: _load(os.path.join(HERE, f"test_oracle_{n}.py"), f"_pins_{n}") for n in ("route", "permute", "ffn", "policy")}
+PINS = {n: _load(os.path.join(HERE, f"test_oracle_{n}.py"), f"_pins_{n}")
+        for n in ("route", "permute", "ffn", "policy", "quant")}
 GOLDEN = os.path.join(HERE, "golden")
 
 
 def _run_pins():
-    r, p, f, q = PINS["route"], PINS["permute"], PINS["ffn"], PINS["policy"]
+    r, p, f, q, z = PINS["route"], PINS["permute"], PINS["ffn"], PINS["policy"], PINS["quant"]
     calls = [
         lambda: r.test_worked_example(GOLDEN), lambda: r.test_brute_force(8, 3, "ties"),
         lambda: r.test_brute_force(16, 8, "normal"), r.test_invariants,
@@ -41,6 +42,8 @@ def _run_pins():
         f.test_dense_gate_matrix_form, f.test_identical_experts_reduce_to_dense_ffn, f.test_combine_properties,
         f.test_permute_combine_round_trip_is_identity, f.test_fp8_path_dequantizes_same_codes,
         q.test_x_moe_eq3, q.test_quota_eq4,
+        z.test_e4m3_round_trip_every_finite_code, z.test_e4m3_midpoints_round_to_even_and_neighbours_to_nearest,
+        z.test_e4m3_hand_derived_values, z.test_quantize_rows_closed_forms, z.test_h_fp8_option_closed_form,
     ]
     failed = 0
     for c in calls:
@@ -76,6 +79,11 @@ MUTANTS = [
     ("quota: Q_max cap dropped", "return min(int(q_max), rounded)", "return rounded"),
     ("quota: ratio inverted", "num, den = int(q) * int(x_moe_now), int(x_moe_star)",
      "num, den = int(q) * int(x_moe_star), max(1, int(x_moe_now))"),
+    ("e4m3 encode: ties to the odd code", "(d_lo == d_hi) & (lo % 2 == 0)", "(d_lo == d_hi) & (lo % 2 == 1)"),
+    ("e4m3 encode: saturates at 240", "np.minimum(np.abs(v), 448.0)", "np.minimum(np.abs(v), 240.0)"),
+    ("h quant: scale floor dropped", "np.maximum(np.abs(g).max(axis=2), floor)", "np.abs(g).max(axis=2)"),
+    ("h quant: wrong full-scale code", "floor) / qmax", "floor) / (qmax / 2)"),
+    ("h quant: option ignored", "    if h_fp8:\n        codes, sc", "    if False:\n        codes, sc"),
     ("quota: no rounding to the multiple", "rounded = c * (-(-num // (den * c)))", "rounded = -(-num // den)"),
 ]
 
