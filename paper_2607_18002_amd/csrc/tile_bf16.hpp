@@ -133,7 +133,7 @@ __device__ __forceinline__ void mma_step(f32x16 (&acc)[MACT][S::NBW], const bf16
 // B   : first B row of the tile (GLU: gate row n0), row stride ldb elements
 // up_rows : GLU only, rows from the gate block to the matching up block (I)
 // out : output tile origin, row stride ldo (bf16); rows [0, 32*MACT) written
-template <class S, bool GLU, int MACT, bool PACKED = false>
+template <class S, bool GLU, int MACT, bool PACKED = false, int D = TileRegs<S, MACT>::DEPTH>
 __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, int lda,
                                                const uint16_t* __restrict__ B, int ldb, int up_rows, int K,
                                                uint16_t* __restrict__ out, int ldo, char* lds) {
@@ -178,38 +178,41 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    constexpr int D = TileRegs<S, MACT>::DEPTH;
     u32x4 ra[2][CA];                                  // A of steps s+1 and s+2 (slot = step & 1)
     bf16x8 rb[D][S::NBW][S::KK];                      // B of steps s .. s+D-1 (slot = step % D)
-    const int nk = K / S::BK;
+    const int nk = K / S::BK;                         // a multiple of D (see gemm_tile_bf16_rows)
     constexpr int KB = S::BK * 2;                     // bytes per K step of a row-major row
     constexpr int KBB = PACKED ? S::BK * 64 : KB;     // bytes per K step of a weight fragment stream
     static_assert(S::BK % 64 == 0, "K steps are whole 64-element chunks");
     static_assert(D % 2 == 0, "the A slots (step & 1) repeat within one pass of the B ring");
 
+    // The K loop has no branches: a step's loads are clamped to the last K
+    // step instead of skipped (the spare loads are re-reads of data just
+    // loaded, never consumed).  With no path-dependent loads the compiler's
+    // wait counts stay exact, so the waits for one step's operands leave the
+    // later steps' loads in flight.
     // Prologue: A of step 0 into LDS stage 0; A of steps 1, 2 and B of steps
     // 0 .. D-1 in flight.  A loads go before the B loads of the same step, so
     // waiting for an A slot (vmcnt counts in issue order) leaves later B loads
     // in flight.
+    const int last = nk - 1;
     load_a<CA>(ra[0], Ab, aoff, 0);
 #pragma unroll
-    for (int d = 0; d < D; ++d)
-        if (d < nk) load_b<S, PACKED>(rb[d], Bb, boff, d * KBB);
+    for (int d = 0; d < D; ++d) load_b<S, PACKED>(rb[d], Bb, boff, d * KBB);
     store_a<CA>(lds0, ra[0], alds);
-    if (1 < nk) load_a<CA>(ra[1], Ab, aoff, KB);
-    if (2 < nk) load_a<CA>(ra[0], Ab, aoff, 2 * KB);
+    load_a<CA>(ra[1], Ab, aoff, (1 < last ? 1 : last) * KB);
+    load_a<CA>(ra[0], Ab, aoff, (2 < last ? 2 : last) * KB);
     __syncthreads();
     for (int s0 = 0; s0 < nk; s0 += D) {
 #pragma unroll
         for (int d = 0; d < D; ++d) {
             const int s = s0 + d;                     // uniform; d, s & 1 and s % D are compile-time
-            if (s < nk) {
-                mma_step<S, MACT>(acc, rb[d], (d & 1) ? lds1 : lds0, lane);
-                if (s + 1 < nk) store_a<CA>((d & 1) ? lds0 : lds1, ra[(d + 1) & 1], alds);
-                if (s + D < nk) load_b<S, PACKED>(rb[d], Bb, boff, (s + D) * KBB);
-                if (s + 3 < nk) load_a<CA>(ra[(d + 1) & 1], Ab, aoff, (s + 3) * KB);
-                __syncthreads();
-            }
+            mma_step<S, MACT>(acc, rb[d], (d & 1) ? lds1 : lds0, lane);
+            store_a<CA>((d & 1) ? lds0 : lds1, ra[(d + 1) & 1], alds);
+            const int sb = s + D < last ? s + D : last, sa = s + 3 < last ? s + 3 : last;
+            load_b<S, PACKED>(rb[d], Bb, boff, sb * KBB);
+            load_a<CA>(ra[(d + 1) & 1], Ab, aoff, sa * KB);
+            __syncthreads();
         }
     }
 
@@ -257,16 +260,29 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
     }
 }
 
+// The K loop runs whole passes of the B ring: the ring depth for the tile's
+// row count when it divides the number of K steps, else 2 (K is a multiple
+// of 2 * BK).
+template <class S, bool GLU, int MACT, bool PACKED>
+__device__ __forceinline__ void gemm_tile_bf16_depth(const uint16_t* A, int lda, const uint16_t* B, int ldb,
+                                                     int up_rows, int K, uint16_t* out, int ldo, char* lds) {
+    constexpr int D = TileRegs<S, MACT>::DEPTH;
+    if ((K / S::BK) % D == 0)
+        gemm_tile_bf16<S, GLU, MACT, PACKED, D>(A, lda, B, ldb, up_rows, K, out, ldo, lds);
+    else
+        gemm_tile_bf16<S, GLU, MACT, PACKED, 2>(A, lda, B, ldb, up_rows, K, out, ldo, lds);
+}
+
 // Dispatch on the number of 32-row blocks holding valid rows (uniform per tile).
 template <class S, bool GLU, bool PACKED>
 __device__ __forceinline__ void gemm_tile_bf16_rows(int rows32, const uint16_t* A, int lda, const uint16_t* B, int ldb,
                                                     int up_rows, int K, uint16_t* out, int ldo, char* lds) {
     static_assert(S::MB == 4, "dispatch written for 128-row tiles");
     switch (rows32 >> 5) {
-        case 1: gemm_tile_bf16<S, GLU, 1, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
-        case 2: gemm_tile_bf16<S, GLU, 2, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
-        case 3: gemm_tile_bf16<S, GLU, 3, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
-        default: gemm_tile_bf16<S, GLU, 4, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
+        case 1: gemm_tile_bf16_depth<S, GLU, 1, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
+        case 2: gemm_tile_bf16_depth<S, GLU, 2, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
+        case 3: gemm_tile_bf16_depth<S, GLU, 3, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
+        default: gemm_tile_bf16_depth<S, GLU, 4, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
     }
 }
 
