@@ -78,13 +78,12 @@ __device__ __forceinline__ void load_w8(i32x8 (&rw)[S::NBW][S::KK], __amdgpu_buf
 // wsc : weight scales of the expert, [N/128][K/128]
 // GLU : out = h codes (ldo bytes per row), osc = h scales (ldsc floats per row);
 //       else out = bf16 rows (ldo elements per row)
-template <class S, bool GLU, int MACT>
+template <class S, bool GLU, int MACT, int D = TileRegsF8<S, MACT>::DEPTH>
 __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int lda, const float* __restrict__ asc,
                                               const uint8_t* __restrict__ B, int n0, int up_rows,
                                               const float* __restrict__ wsc, int K, void* __restrict__ out, int ldo,
                                               float* __restrict__ osc, int ldsc, char* lds) {
     constexpr int CA = TileRegsF8<S, MACT>::CA;
-    constexpr int D = TileRegsF8<S, MACT>::DEPTH;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wn = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nkb = K / S::BK;
@@ -131,54 +130,56 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
     const int arow = (lane & 31) * S::LDS_ROW + (lane >> 5) * 32;      // lanes 32-63: +32 bytes
     constexpr int KBW = 32 * S::BK;                                   // bytes per K step of a 32-row block
 
+    // Branch-free K loop (K/128 is a multiple of D): loads are clamped to the
+    // last step instead of skipped, so the compiler's wait counts stay exact
+    // and a step's waits leave the later steps' weight loads in flight.
+    const int last = nkb - 1;
     load_a<CA>(ra, Ab, aoff, 0);
 #pragma unroll
-    for (int d = 0; d < D; ++d)
-        if (d < nkb) load_w8<S>(rw[d], Bb, boff, d * KBW);
+    for (int d = 0; d < D; ++d) load_w8<S>(rw[d], Bb, boff, d * KBW);
     store_a<CA>(lds0, ra, alds);
-    if (1 < nkb) load_a<CA>(ra, Ab, aoff, S::BK);
+    load_a<CA>(ra, Ab, aoff, (1 < last ? 1 : last) * S::BK);
     __syncthreads();
     for (int s0 = 0; s0 < nkb; s0 += D) {
 #pragma unroll
         for (int d = 0; d < D; ++d) {
             const int s = s0 + d;                                      // uniform; d and s & 1 are compile-time
-            if (s < nkb) {
-                const char* cur = (d & 1) ? lds1 : lds0;
-                f32x16 part[S::NBW][MACT];
+            const char* cur = (d & 1) ? lds1 : lds0;
+            f32x16 part[S::NBW][MACT];
 #pragma unroll
-                for (int kk = 0; kk < S::KK; ++kk) {
-                    i32x8 xa[MACT];
-#pragma unroll
-                    for (int i = 0; i < MACT; ++i) {
-                        const char* p = cur + arow + i * 32 * S::LDS_ROW + kk * 64;
-                        const u32x4 lo = *(const u32x4*)p, hi = *(const u32x4*)(p + 16);
-                        xa[i] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
-                    }
-#pragma unroll
-                    for (int j = 0; j < S::NBW; ++j)
-#pragma unroll
-                        for (int i = 0; i < MACT; ++i) {
-                            const f32x16 c0 = {};
-                            part[j][i] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                                rw[d][j][kk], xa[i], kk == 0 ? c0 : part[j][i], 0, 0, 0, 127, 0, 127);
-                        }
-                }
-                if (s + 1 < nkb) store_a<CA>((d & 1) ? lds0 : lds1, ra, alds);
-                if (s + D < nkb) load_w8<S>(rw[d], Bb, boff, (s + D) * KBW);
-                if (s + 2 < nkb) load_a<CA>(ra, Ab, aoff, (s + 2) * S::BK);
-                // fold the block in: one scale per (feature block, token) pair
+            for (int kk = 0; kk < S::KK; ++kk) {
+                i32x8 xa[MACT];
 #pragma unroll
                 for (int i = 0; i < MACT; ++i) {
-                    const float xs = sx[s * S::BM + 32 * i + (lane & 31)];
-#pragma unroll
-                    for (int j = 0; j < S::NBW; ++j) {
-                        const float c = xs * sw[j][s];
-#pragma unroll
-                        for (int r = 0; r < 16; ++r) tot[j][i][r] = __builtin_fmaf(part[j][i][r], c, tot[j][i][r]);
-                    }
+                    const char* p = cur + arow + i * 32 * S::LDS_ROW + kk * 64;
+                    const u32x4 lo = *(const u32x4*)p, hi = *(const u32x4*)(p + 16);
+                    xa[i] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
                 }
-                __syncthreads();
+#pragma unroll
+                for (int j = 0; j < S::NBW; ++j)
+#pragma unroll
+                    for (int i = 0; i < MACT; ++i) {
+                        const f32x16 c0 = {};
+                        part[j][i] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                            rw[d][j][kk], xa[i], kk == 0 ? c0 : part[j][i], 0, 0, 0, 127, 0, 127);
+                    }
             }
+            store_a<CA>((d & 1) ? lds0 : lds1, ra, alds);
+            const int sw_ = s + D < last ? s + D : last, sa = s + 2 < last ? s + 2 : last;
+            load_w8<S>(rw[d], Bb, boff, sw_ * KBW);
+            load_a<CA>(ra, Ab, aoff, sa * S::BK);
+            // fold the block in: one scale per (feature block, token) pair
+#pragma unroll
+            for (int i = 0; i < MACT; ++i) {
+                const float xs = sx[s * S::BM + 32 * i + (lane & 31)];
+#pragma unroll
+                for (int j = 0; j < S::NBW; ++j) {
+                    const float c = xs * sw[j][s];
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) tot[j][i][r] = __builtin_fmaf(part[j][i][r], c, tot[j][i][r]);
+                }
+            }
+            __syncthreads();
         }
     }
 
@@ -266,15 +267,28 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
     }
 }
 
+// The K loop runs whole passes of the weight ring: the ring depth for the
+// tile's row count when it divides K/128, else 2 (K is a multiple of 256).
+template <class S, bool GLU, int MACT>
+__device__ __forceinline__ void gemm_tile_fp8_depth(const uint8_t* A, int lda, const float* asc, const uint8_t* B,
+                                                    int n0, int up_rows, const float* wsc, int K, void* out, int ldo,
+                                                    float* osc, int ldsc, char* lds) {
+    constexpr int D = TileRegsF8<S, MACT>::DEPTH;
+    if ((K / S::BK) % D == 0)
+        gemm_tile_fp8<S, GLU, MACT, D>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds);
+    else
+        gemm_tile_fp8<S, GLU, MACT, 2>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds);
+}
+
 template <class S, bool GLU>
 __device__ __forceinline__ void gemm_tile_fp8_rows(int rows32, const uint8_t* A, int lda, const float* asc,
                                                    const uint8_t* B, int n0, int up_rows, const float* wsc, int K,
                                                    void* out, int ldo, float* osc, int ldsc, char* lds) {
     static_assert(S::MB == 2, "dispatch written for 64-row tiles");
     if (rows32 > 32)
-        gemm_tile_fp8<S, GLU, 2>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds);
+        gemm_tile_fp8_depth<S, GLU, 2>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds);
     else
-        gemm_tile_fp8<S, GLU, 1>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds);
+        gemm_tile_fp8_depth<S, GLU, 1>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds);
 }
 
 }  // namespace moeapk
