@@ -4,8 +4,9 @@
 // are fixed after routing, before the activations are written).
 //
 // Four launches on the caller's stream:
-//   count   : per-chunk expert histogram in LDS (4096 assignments per block)
-//   scan    : expert counts, padded segment offsets, per-(chunk, expert) bases
+//   count   : per-chunk expert histogram in LDS (512 assignments per block)
+//   scan    : expert counts, padded segment offsets, per-(chunk, expert) bases;
+//             each expert's prefix over chunks is split across 1024/E threads
 //   scatter : stable rank of every assignment inside its chunk, built from
 //             wave ballots (rank = popcount(match & lanes-below)) plus per-wave
 //             and per-iteration running counts -> row_to_assign / assign_to_row.
@@ -20,7 +21,7 @@ namespace {
 using moeapk::set_status;
 
 constexpr int kThreads = 256;
-constexpr int kIters = 16;
+constexpr int kIters = 2;
 constexpr int kChunk = kThreads * kIters;   // assignments per block
 
 __global__ __launch_bounds__(256) void permute_count_kernel(const int32_t* __restrict__ ids, int A, int E,
@@ -47,35 +48,51 @@ __global__ __launch_bounds__(1024) void permute_scan_kernel(int NB, int E, int a
                                                            int32_t* __restrict__ counts,
                                                            int32_t* __restrict__ offsets,
                                                            int32_t* __restrict__ err) {
+    __shared__ int32_t part[1024];       // per thread: the sum of its run of chunks, then its run's base
     __shared__ int32_t padded[1024];
     __shared__ int32_t scan[1024];
-    const int e = threadIdx.x;
-    int total = 0;
-    if (e < E) {
-        for (int b = 0; b < NB; ++b) {
-            const int c = blk_cnt[(size_t)b * E + e];
-            blk_cnt[(size_t)b * E + e] = total;              // exclusive prefix over chunks
-            total += c;
-        }
-        counts[e] = total;
-    }
-    padded[e] = (e < E) ? ((total + align - 1) / align) * align : 0;
-    scan[e] = padded[e];
+    // P threads per expert (P = 1024 / E rounded down to a power of two); thread
+    // (e, j) owns chunks [j*R, (j+1)*R) of expert e, R = ceil(NB / P).
+    int P = 1;
+    while (P * 2 * E <= 1024) P *= 2;
+    const int R = (NB + P - 1) / P;
+    const int t = threadIdx.x, e = t / P, j = t - e * P;
+    const bool mine = e < E;
+    const int b0 = mine ? j * R : 0, b1 = mine ? min(NB, b0 + R) : 0;
+    int sum = 0;
+    for (int b = b0; b < b1; ++b) sum += blk_cnt[(size_t)b * E + e];
+    part[t] = sum;
     __syncthreads();
-    for (int off = 1; off < 1024; off <<= 1) {               // inclusive Hillis-Steele scan
-        const int v = (e >= off) ? scan[e - off] : 0;
+    if (mine && j == 0) {                                      // exclusive prefix over the expert's P runs
+        int run = 0;
+        for (int q = 0; q < P; ++q) { const int v = part[t + q]; part[t + q] = run; run += v; }
+        scan[e] = run;                                         // total rows of expert e (temporarily)
+    }
+    __syncthreads();
+    const int tot = (t < E) ? scan[t] : 0;
+    if (t < E) counts[t] = tot;
+    padded[t] = (t < E) ? ((tot + align - 1) / align) * align : 0;
+    __syncthreads();
+    scan[t] = padded[t];
+    __syncthreads();
+    for (int off = 1; off < 1024; off <<= 1) {                 // inclusive Hillis-Steele scan over experts
+        const int v = (t >= off) ? scan[t - off] : 0;
         __syncthreads();
-        scan[e] += v;
+        scan[t] += v;
         __syncthreads();
     }
-    const int start = scan[e] - padded[e];
-    if (e < E) {
-        offsets[e] = start;
-        for (int b = 0; b < NB; ++b) blk_cnt[(size_t)b * E + e] += start;
+    if (t < E) offsets[t] = scan[t] - padded[t];
+    if (t == E - 1) {
+        offsets[E] = scan[t];
+        if (scan[t] > capacity) set_status(err, MOE_ERR_CAPACITY);
     }
-    if (e == E - 1) {
-        offsets[E] = scan[e];
-        if (scan[e] > capacity) set_status(err, MOE_ERR_CAPACITY);
+    if (mine) {                                                // bases of this thread's chunks
+        int run = scan[e] - padded[e] + part[t];
+        for (int b = b0; b < b1; ++b) {
+            const int c = blk_cnt[(size_t)b * E + e];
+            blk_cnt[(size_t)b * E + e] = run;
+            run += c;
+        }
     }
 }
 
