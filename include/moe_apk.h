@@ -111,7 +111,10 @@ moe_status_t moe_topk_route(const float* logits, int32_t T, int32_t E_global, in
  *  row_to_assign  [capacity] i32 out (rows >= offsets[E_local] untouched)
  *  assign_to_row  [T*top_k] i32 out (-1 for non-local slots)
  *  x_perm         [capacity, H] out, same dtype as x (rows >= offsets[E_local]
- *                 untouched);  x_perm_scales [capacity, H/128] f32 out (fp8)
+ *                 untouched);  x_perm_scales [capacity, H/128] f32 out (fp8).
+ *                 x_perm NULL: only the maps are built (padding rows of
+ *                 row_to_assign still set to -1); x and x_scales may then be
+ *                 NULL -- the FFN gathers its rows from x itself (moe_op_desc.x)
  *  workspace      moe_permute_workspace_bytes(T, top_k, E_local) bytes
  *  error_flag     device i32 status word (data errors; not cleared here)
  * Limits: 1 <= E_local <= 1024, H a multiple of 128.
@@ -166,6 +169,15 @@ typedef struct moe_op_desc {
     int64_t gap_ns;               /* ...for at least gap_ns                              */
     uint32_t* done_word;          /* NULL, or set to 1 (system-scope release) when the
                                      op's last tile has committed                        */
+    /* Fused gather (Evaluation, "Implementation": the MoE data pre-processing
+     * fused into the persistent kernel).  With x_perm NULL and x set, GEMM-1
+     * reads row r of a segment straight from x[row_to_assign[r] / top_k]
+     * (padding rows, row_to_assign -1, read as zero) and, for fp8, its scales
+     * from x_scales; moe_permute then only builds the maps (x_perm NULL).   */
+    const void*  x;               /* [T, H] activations (bf16 or fp8 codes), or NULL    */
+    const float* x_scales;        /* [T, H/128]                   fp8 only            */
+    const int32_t* row_to_assign; /* [capacity] from moe_permute                       */
+    int32_t T, top_k;             /* rows of x; slots per token                         */
 } moe_op_desc;
 
 /* Per-tile trace record (times in device wall-clock ticks, 100 MHz on gfx950).

@@ -39,6 +39,7 @@ class OpDesc(C.Structure):
         ("release_word", _p), ("release_after_ns", _i64),
         ("depends_on_op", _i32), ("weight_layout", _i32), ("gap_ns", _i64),
         ("done_word", _p),
+        ("x", _p), ("x_scales", _p), ("row_to_assign", _p), ("T", _i32), ("top_k", _i32),
     ]
 
 

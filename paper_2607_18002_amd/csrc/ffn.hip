@@ -58,7 +58,7 @@ enum : int32_t { CMD_EXIT = 0, CMD_TILE = 1, CMD_INST = 2, CMD_IDLE = 3 };
 struct OpArg {
     const int32_t* counts;
     const int32_t* offsets;
-    const uint16_t* x;         // bf16 elements, or fp8 codes (bytes) for CLS_FP8
+    const uint16_t* x;         // bf16 elements, or fp8 codes (bytes) for CLS_FP8: x_perm, or x when gathered
     const uint16_t* wgu;
     const uint16_t* wd;
     uint16_t* h;
@@ -68,7 +68,8 @@ struct OpArg {
     const float* wds;
     float* hs;
     uint32_t* done_word;
-    int32_t cls, phase, layer, E, H, I, capacity, mt, n1, n2, max_mtiles, table_off, g1_off, pad;
+    const int32_t* rmap;       // gathered GEMM-1 operand: row -> assignment (x row = assignment / top_k), else NULL
+    int32_t cls, phase, layer, E, H, I, capacity, mt, n1, n2, max_mtiles, table_off, g1_off, T, top_k, pad;
 };
 
 struct KArgs {
@@ -193,9 +194,11 @@ template <class S>
 __device__ __forceinline__ void run_tile_cls(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds) {
     const long H = op.H, I = op.I;
     if (stage == 1) {
-        gemm_tile_bf16_rows<S, true, true>(rows32, op.x + row0 * H, (int)H,
+        const bool g = op.rmap != nullptr;
+        gemm_tile_bf16_rows<S, true, true>(rows32, g ? op.x : op.x + row0 * H, (int)H,
                                      op.wgu + (long)e * 2 * I * H + (long)nb * (S::BN / 2) * H, (int)H, (int)I,
-                                     (int)H, op.h + row0 * I + nb * (S::BN / 2), (int)I, lds);
+                                     (int)H, op.h + row0 * I + nb * (S::BN / 2), (int)I, lds,
+                                     g ? op.rmap + row0 : nullptr, op.top_k, op.T);
     } else {
         gemm_tile_bf16_rows<S, false, true>(rows32, op.h + row0 * I, (int)I, op.wd + (long)e * H * I + (long)nb * S::BN * I,
                                       (int)I, 0, (int)I, op.y + row0 * H + nb * S::BN, (int)H, lds);
@@ -211,10 +214,12 @@ __device__ __forceinline__ void run_tile_fp8(const OpArg& op, int stage, int row
     uint8_t* h = (uint8_t*)op.h;
     if (stage == 1) {
         const int n0 = nb * (S::BN / 2);
-        gemm_tile_fp8_rows<S, true>(rows32, x + row0 * H, (int)H, op.xs + row0 * (H / 128),
+        const bool g = op.rmap != nullptr;
+        gemm_tile_fp8_rows<S, true>(rows32, g ? x : x + row0 * H, (int)H, g ? op.xs : op.xs + row0 * (H / 128),
                                     (const uint8_t*)op.wgu + (long)e * 2 * I * H + (long)n0 * H, n0, (int)I,
                                     op.wgus + (long)e * (2 * I / 128) * (H / 128), (int)H, h + row0 * I + n0, (int)I,
-                                    op.hs + row0 * (I / 128) + nb, (int)(I / 128), lds);
+                                    op.hs + row0 * (I / 128) + nb, (int)(I / 128), lds,
+                                    g ? op.rmap + row0 : nullptr, op.top_k, op.T);
     } else {
         const int n0 = nb * S::BN;
         gemm_tile_fp8_rows<S, false>(rows32, h + row0 * I, (int)I, op.hs + row0 * (I / 128),
@@ -697,7 +702,7 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
         if (cls == CLS_FP8) {
             if (d.H > 128 * ShapeF8::MAX_KB || d.I > 128 * ShapeF8::MAX_KB)
                 return fail(MOE_ERR_UNSUPPORTED, "op %d: fp8 H, I must be at most %d", o, 128 * ShapeF8::MAX_KB);
-            if (!d.x_perm_scales || !d.w_gate_up_scales || !d.w_down_scales || !d.h_scales)
+            if (!(d.x ? d.x_scales : d.x_perm_scales) || !d.w_gate_up_scales || !d.w_down_scales || !d.h_scales)
                 return fail(MOE_ERR_INVALID_ARG, "op %d: fp8 op without its scale buffers", o);
         }
         if (d.row_align != ci.bm)
@@ -707,20 +712,32 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
             return fail(MOE_ERR_UNSUPPORTED, "op %d: capacity*H exceeds 2^31 elements", o);
         if (d.capacity / d.row_align >= kMaxRowTiles)
             return fail(MOE_ERR_UNSUPPORTED, "op %d: capacity=%d exceeds %d row tiles", o, d.capacity, kMaxRowTiles);
-        if (!d.counts || !d.offsets || !d.x_perm || !d.w_gate_up || !d.w_down || !d.h || !d.y_perm)
+        if (!d.counts || !d.offsets || !d.w_gate_up || !d.w_down || !d.h || !d.y_perm)
             return fail(MOE_ERR_INVALID_ARG, "op %d: null buffer", o);
+        // GEMM-1 operand: x_perm, or x gathered through row_to_assign (exactly one of the two)
+        if ((d.x_perm != nullptr) == (d.x != nullptr))
+            return fail(MOE_ERR_INVALID_ARG, "op %d: give exactly one of x_perm and x", o);
+        if (d.x) {
+            if (!d.row_to_assign || d.T < 1 || d.top_k < 1)
+                return fail(MOE_ERR_INVALID_ARG, "op %d: gathered operand needs row_to_assign, T >= 1, top_k >= 1", o);
+            if ((int64_t)d.T * d.H * (cls == CLS_FP8 ? 1 : 2) >= ((int64_t)1 << 31))
+                return fail(MOE_ERR_UNSUPPORTED, "op %d: T*H of the gathered operand exceeds 2^31 bytes", o);
+        }
         if (d.depends_on_op >= o || d.depends_on_op < -1)
             return fail(MOE_ERR_INVALID_ARG, "op %d: depends_on_op=%d must be -1 or an earlier op", o, d.depends_on_op);
         if (d.gap_ns < 0) return fail(MOE_ERR_INVALID_ARG, "op %d: gap_ns < 0", o);
         OpArg& p = a.op[o];
         p.counts = d.counts;
         p.offsets = d.offsets;
-        p.x = (const uint16_t*)d.x_perm;
+        p.x = (const uint16_t*)(d.x ? d.x : d.x_perm);
         p.wgu = (const uint16_t*)d.w_gate_up;
         p.wd = (const uint16_t*)d.w_down;
         p.h = (uint16_t*)d.h;
         p.y = (uint16_t*)d.y_perm;
-        p.xs = d.x_perm_scales;
+        p.xs = d.x ? d.x_scales : d.x_perm_scales;
+        p.rmap = d.x ? d.row_to_assign : nullptr;
+        p.T = d.x ? d.T : 0;
+        p.top_k = d.x ? d.top_k : 1;
         p.wgus = d.w_gate_up_scales;
         p.wds = d.w_down_scales;
         p.hs = d.h_scales;

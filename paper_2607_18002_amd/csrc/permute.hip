@@ -13,7 +13,8 @@
 //             The result is the unique order "ascending assignment a = t*k+j",
 //             so it is bit-exact and independent of scheduling.
 //   gather  : one wave per row copies x[a / k] (16-byte vectors) into x_perm,
-//             zero-fills padding rows and marks them -1.
+//             zero-fills padding rows and marks them -1; without x_perm (the
+//             FFN then gathers its rows itself) it only marks padding rows.
 #include "common.hpp"
 
 namespace {
@@ -170,6 +171,10 @@ __global__ __launch_bounds__(256) void permute_gather_kernel(const int32_t* __re
         }
         const bool valid = (r - soff[lo]) < soff[E + 1 + lo];
         const int a = valid ? row_to_assign[r] : -1;
+        if (!x_perm) {                                        // maps only
+            if (a < 0 && lane == 0) row_to_assign[r] = -1;
+            continue;
+        }
         uint4* dst = x_perm + (size_t)r * row_vecs;
         if (a >= 0) {
             const uint4* src = x + (size_t)(a / k) * row_vecs;
@@ -217,10 +222,10 @@ extern "C" moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t 
         return fail(MOE_ERR_CAPACITY, "moe_permute: capacity %d < T*min(k,E_local) + E_local*(row_align-1) = %lld",
                     capacity, (long long)need);
     if ((int64_t)T * top_k > (int64_t)INT32_MAX / 2) return fail(MOE_ERR_UNSUPPORTED, "moe_permute: T*top_k too large");
-    if (!counts || !offsets || !row_to_assign || !assign_to_row || !x || !x_perm || !workspace || !error_flag ||
-        (T > 0 && !topk_ids))
+    if (!counts || !offsets || !row_to_assign || !assign_to_row || !workspace || !error_flag ||
+        (T > 0 && !topk_ids) || (x_perm && !x))
         return fail(MOE_ERR_INVALID_ARG, "moe_permute: null pointer");
-    if (fp8 && (!x_scales || !x_perm_scales))
+    if (fp8 && x_perm && (!x_scales || !x_perm_scales))
         return fail(MOE_ERR_INVALID_ARG, "moe_permute: fp8 activations need x_scales and x_perm_scales");
     moe_status_t st = moeapk_host::check_device();
     if (st != MOE_OK) return st;
@@ -246,7 +251,7 @@ extern "C" moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t 
     if (grid < 1) grid = 1;
     hipLaunchKernelGGL(permute_gather_kernel, dim3(grid), dim3(256), (2 * E_local + 1) * sizeof(int32_t), s, counts,
                        offsets, E_local, top_k, capacity, (const uint4*)x, row_bytes / 16, x_scales,
-                       fp8 ? H / 128 : 0, row_to_assign, (uint4*)x_perm, fp8 ? x_perm_scales : nullptr);
+                       fp8 ? H / 128 : 0, row_to_assign, (uint4*)x_perm, (fp8 && x_perm) ? x_perm_scales : nullptr);
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(MOE_ERR_HIP, "moe_permute: launch failed: %s", hipGetErrorString(err));
     return MOE_OK;

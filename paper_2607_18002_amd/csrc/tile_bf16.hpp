@@ -129,14 +129,18 @@ __device__ __forceinline__ void mma_step(f32x16 (&acc)[MACT][S::NBW], const bf16
     }
 }
 
-// A   : tile row 0 at k = 0, row stride lda elements; rows [0, 32*MACT) are read
+// A   : tile row 0 at k = 0, row stride lda elements; rows [0, 32*MACT) are read.
+//       With a row map (gathered operand): A is row 0 of a matrix of a_rows
+//       rows, and tile row r is A's row rowmap[r] / k (rowmap[r] < 0: zero).
 // B   : first B row of the tile (GLU: gate row n0), row stride ldb elements
 // up_rows : GLU only, rows from the gate block to the matching up block (I)
 // out : output tile origin, row stride ldo (bf16); rows [0, 32*MACT) written
 template <class S, bool GLU, int MACT, bool PACKED = false, int D = TileRegs<S, MACT>::DEPTH>
 __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, int lda,
                                                const uint16_t* __restrict__ B, int ldb, int up_rows, int K,
-                                               uint16_t* __restrict__ out, int ldo, char* lds) {
+                                               uint16_t* __restrict__ out, int ldo, char* lds,
+                                               const int32_t* __restrict__ rowmap = nullptr, int k = 1,
+                                               int a_rows = 0) {
     constexpr int CA = TileRegs<S, MACT>::CA;
     const int tid = threadIdx.x, lane = tid & 63, wn = tid >> 6;
 
@@ -160,11 +164,19 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
 #pragma unroll
     for (int i = 0; i < CA; ++i) {
         const int idx = tid + 256 * i, r = idx / S::CPR, c = idx % S::CPR;
-        aoff[i] = (uint32_t)r * (uint32_t)lda * 2u + c * 16;
+        int src = r;
+        if (rowmap) {
+            const int a = rowmap[r];
+            src = (a >= 0 && a / k < a_rows) ? a / k : -1;
+        }
+        // a gathered padding row gets an offset past the buffer's extent, which reads as zero
+        aoff[i] = src >= 0 ? (uint32_t)src * (uint32_t)lda * 2u + c * 16 : 0x80000000u;
         alds[i] = r * S::LDS_ROW + c * 16;
     }
-    // extents: A rows [0, 32*MACT); B rows [0, BN) or, for GLU, gate rows [0, BN/2) and up rows [up_rows, up_rows + BN/2)
-    const __amdgpu_buffer_rsrc_t Ab = make_rsrc(A, (uint32_t)(MACT * 32) * (uint32_t)lda * 2u);
+    // extents: A rows [0, 32*MACT) (gathered: [0, a_rows)); B rows [0, BN) or, for GLU,
+    // gate rows [0, BN/2) and up rows [up_rows, up_rows + BN/2)
+    const __amdgpu_buffer_rsrc_t Ab =
+        make_rsrc(A, (uint32_t)(rowmap ? a_rows : MACT * 32) * (uint32_t)lda * 2u);
     const __amdgpu_buffer_rsrc_t Bb =
         make_rsrc(B, (uint32_t)(GLU ? up_rows + S::BN / 2 : S::BN) * (uint32_t)ldb * 2u);
     char* lds0 = lds;
@@ -265,24 +277,26 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
 // of 2 * BK).
 template <class S, bool GLU, int MACT, bool PACKED>
 __device__ __forceinline__ void gemm_tile_bf16_depth(const uint16_t* A, int lda, const uint16_t* B, int ldb,
-                                                     int up_rows, int K, uint16_t* out, int ldo, char* lds) {
+                                                     int up_rows, int K, uint16_t* out, int ldo, char* lds,
+                                                     const int32_t* rowmap, int k, int a_rows) {
     constexpr int D = TileRegs<S, MACT>::DEPTH;
     if ((K / S::BK) % D == 0)
-        gemm_tile_bf16<S, GLU, MACT, PACKED, D>(A, lda, B, ldb, up_rows, K, out, ldo, lds);
+        gemm_tile_bf16<S, GLU, MACT, PACKED, D>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows);
     else
-        gemm_tile_bf16<S, GLU, MACT, PACKED, 2>(A, lda, B, ldb, up_rows, K, out, ldo, lds);
+        gemm_tile_bf16<S, GLU, MACT, PACKED, 2>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows);
 }
 
 // Dispatch on the number of 32-row blocks holding valid rows (uniform per tile).
 template <class S, bool GLU, bool PACKED>
 __device__ __forceinline__ void gemm_tile_bf16_rows(int rows32, const uint16_t* A, int lda, const uint16_t* B, int ldb,
-                                                    int up_rows, int K, uint16_t* out, int ldo, char* lds) {
+                                                    int up_rows, int K, uint16_t* out, int ldo, char* lds,
+                                                    const int32_t* rowmap = nullptr, int k = 1, int a_rows = 0) {
     static_assert(S::MB == 4, "dispatch written for 128-row tiles");
     switch (rows32 >> 5) {
-        case 1: gemm_tile_bf16_depth<S, GLU, 1, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
-        case 2: gemm_tile_bf16_depth<S, GLU, 2, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
-        case 3: gemm_tile_bf16_depth<S, GLU, 3, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
-        default: gemm_tile_bf16_depth<S, GLU, 4, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds); break;
+        case 1: gemm_tile_bf16_depth<S, GLU, 1, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows); break;
+        case 2: gemm_tile_bf16_depth<S, GLU, 2, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows); break;
+        case 3: gemm_tile_bf16_depth<S, GLU, 3, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows); break;
+        default: gemm_tile_bf16_depth<S, GLU, 4, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows); break;
     }
 }
 

@@ -76,13 +76,17 @@ __device__ __forceinline__ void load_w8(i32x8 (&rw)[S::NBW][S::KK], __amdgpu_buf
 // B   : packed weight codes, first row n0 of the tile (a multiple of 32);
 //       GLU: gate rows n0 + [0, BN/2) and up rows n0 + up_rows + [0, BN/2)
 // wsc : weight scales of the expert, [N/128][K/128]
+// rowmap (optional, gathered operand): A and asc start at row 0 of a matrix of
+//       a_rows rows; tile row r is its row rowmap[r] / k (rowmap[r] < 0: zero)
 // GLU : out = h codes (ldo bytes per row), osc = h scales (ldsc floats per row);
 //       else out = bf16 rows (ldo elements per row)
 template <class S, bool GLU, int MACT, int D = TileRegsF8<S, MACT>::DEPTH>
 __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int lda, const float* __restrict__ asc,
                                               const uint8_t* __restrict__ B, int n0, int up_rows,
                                               const float* __restrict__ wsc, int K, void* __restrict__ out, int ldo,
-                                              float* __restrict__ osc, int ldsc, char* lds) {
+                                              float* __restrict__ osc, int ldsc, char* lds,
+                                              const int32_t* __restrict__ rowmap = nullptr, int k = 1,
+                                              int a_rows = 0) {
     constexpr int CA = TileRegsF8<S, MACT>::CA;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wn = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -101,10 +105,16 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
 #pragma unroll
     for (int i = 0; i < CA; ++i) {
         const int idx = tid + 256 * i, r = idx / S::CPR, c = idx % S::CPR;
-        aoff[i] = (uint32_t)r * (uint32_t)lda + c * 16;
+        int src = r;
+        if (rowmap) {
+            const int a = rowmap[r];
+            src = (a >= 0 && a / k < a_rows) ? a / k : -1;
+        }
+        // a gathered padding row gets an offset past the buffer's extent, which reads as zero
+        aoff[i] = src >= 0 ? (uint32_t)src * (uint32_t)lda + c * 16 : 0x80000000u;
         alds[i] = r * S::LDS_ROW + c * 16;
     }
-    const __amdgpu_buffer_rsrc_t Ab = make_rsrc(A, (uint32_t)(MACT * 32) * (uint32_t)lda);
+    const __amdgpu_buffer_rsrc_t Ab = make_rsrc(A, (uint32_t)(rowmap ? a_rows : MACT * 32) * (uint32_t)lda);
     const __amdgpu_buffer_rsrc_t Bb =
         make_rsrc(B, (uint32_t)(GLU ? up_rows + S::BN / 2 : S::BN) * (uint32_t)K);
     char* lds0 = lds;
@@ -114,7 +124,12 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
     // activation scales of the tile, transposed to [kb][token]
     for (int idx = tid; idx < MACT * 32 * nkb; idx += 256) {
         const int r = idx / nkb, kb = idx - r * nkb;
-        sx[kb * S::BM + r] = asc[(long)r * nkb + kb];
+        int src = r;
+        if (rowmap) {
+            const int a = rowmap[r];
+            src = (a >= 0 && a / k < a_rows) ? a / k : -1;
+        }
+        sx[kb * S::BM + r] = src >= 0 ? asc[(long)src * nkb + kb] : 0.f;
     }
 
     f32x16 tot[S::NBW][MACT];
@@ -272,23 +287,29 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
 template <class S, bool GLU, int MACT>
 __device__ __forceinline__ void gemm_tile_fp8_depth(const uint8_t* A, int lda, const float* asc, const uint8_t* B,
                                                     int n0, int up_rows, const float* wsc, int K, void* out, int ldo,
-                                                    float* osc, int ldsc, char* lds) {
+                                                    float* osc, int ldsc, char* lds, const int32_t* rowmap,
+                                                    int k, int a_rows) {
     constexpr int D = TileRegsF8<S, MACT>::DEPTH;
     if ((K / S::BK) % D == 0)
-        gemm_tile_fp8<S, GLU, MACT, D>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds);
+        gemm_tile_fp8<S, GLU, MACT, D>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap, k,
+                                       a_rows);
     else
-        gemm_tile_fp8<S, GLU, MACT, 2>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds);
+        gemm_tile_fp8<S, GLU, MACT, 2>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap, k,
+                                       a_rows);
 }
 
 template <class S, bool GLU>
 __device__ __forceinline__ void gemm_tile_fp8_rows(int rows32, const uint8_t* A, int lda, const float* asc,
                                                    const uint8_t* B, int n0, int up_rows, const float* wsc, int K,
-                                                   void* out, int ldo, float* osc, int ldsc, char* lds) {
+                                                   void* out, int ldo, float* osc, int ldsc, char* lds,
+                                                   const int32_t* rowmap = nullptr, int k = 1, int a_rows = 0) {
     static_assert(S::MB == 2, "dispatch written for 64-row tiles");
     if (rows32 > 32)
-        gemm_tile_fp8_depth<S, GLU, 2>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds);
+        gemm_tile_fp8_depth<S, GLU, 2>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap, k,
+                                       a_rows);
     else
-        gemm_tile_fp8_depth<S, GLU, 1>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds);
+        gemm_tile_fp8_depth<S, GLU, 1>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap, k,
+                                       a_rows);
 }
 
 }  // namespace moeapk

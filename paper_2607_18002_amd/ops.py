@@ -55,7 +55,7 @@ def moe_permute_workspace_bytes(T: int, top_k: int, E_local: int) -> int:
 
 def moe_permute(topk_ids: torch.Tensor, E_local: int, x: torch.Tensor, x_scales: Optional[torch.Tensor],
                 row_align: int, capacity: int, counts: torch.Tensor, offsets: torch.Tensor,
-                row_to_assign: torch.Tensor, assign_to_row: torch.Tensor, x_perm: torch.Tensor,
+                row_to_assign: torch.Tensor, assign_to_row: torch.Tensor, x_perm: Optional[torch.Tensor],
                 x_perm_scales: Optional[torch.Tensor], workspace: torch.Tensor, error_flag: torch.Tensor,
                 stream=None) -> None:
     lib = load_library()

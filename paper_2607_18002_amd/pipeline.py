@@ -98,7 +98,7 @@ class OpBuffers:
     offsets: torch.Tensor
     row_to_assign: torch.Tensor
     assign_to_row: torch.Tensor
-    x_perm: torch.Tensor
+    x_perm: Optional[torch.Tensor]              # None when the FFN gathers x rows itself
     x_perm_scales: Optional[torch.Tensor]
     h: torch.Tensor
     h_scales: Optional[torch.Tensor]
@@ -112,10 +112,13 @@ class MoEPipeline:
     def __init__(self, specs: List[OpSpec], n_workgroups: int = 0, decode_quota_wg: int = 64,
                  decode_quota_max_wg: int = 0, x_moe_expected: int = 0, round_multiple: int = 8,
                  trace_capacity: int = 0, spin_limit: int = 0, abort_word: Optional[torch.Tensor] = None,
-                 y_dtype: torch.dtype = torch.bfloat16):
+                 y_dtype: torch.dtype = torch.bfloat16, fused_gather: bool = False):
+        """fused_gather: GEMM-1 reads its rows straight from x through row_to_assign
+        (permute then only builds the maps), instead of from a permuted copy x_perm."""
         if not specs:
             raise ValueError("no operations")
         self.device = specs[0].logits.device
+        self.fused_gather = fused_gather
         dev = self.device
         self.bufs: List[OpBuffers] = []
         for s in specs:
@@ -135,8 +138,9 @@ class MoEPipeline:
                 offsets=torch.zeros(s.E_local + 1, dtype=torch.int32, device=dev),
                 row_to_assign=torch.full((cap,), -1, dtype=torch.int32, device=dev),
                 assign_to_row=torch.empty((T * s.top_k,), dtype=torch.int32, device=dev),
-                x_perm=torch.zeros((cap, H), dtype=act, device=dev),
-                x_perm_scales=torch.zeros((cap, H // 128), dtype=torch.float32, device=dev) if fp8 else None,
+                x_perm=None if fused_gather else torch.zeros((cap, H), dtype=act, device=dev),
+                x_perm_scales=(torch.zeros((cap, H // 128), dtype=torch.float32, device=dev)
+                               if fp8 and not fused_gather else None),
                 h=torch.zeros((cap, I), dtype=act, device=dev),
                 h_scales=torch.zeros((cap, I // 128), dtype=torch.float32, device=dev) if fp8 else None,
                 y_perm=torch.zeros((cap, H), dtype=torch.bfloat16, device=dev),
@@ -158,14 +162,18 @@ class MoEPipeline:
                                trace=self.trace.data_ptr() if trace_capacity > 0 else None,
                                trace_capacity=trace_capacity, op_stats=self.stats.data_ptr(),
                                spin_limit=spin_limit)
-        self.descs = [self._desc(i, b) for i, b in enumerate(self.bufs)]
+        self.descs = [self._desc(i, b, fused_gather) for i, b in enumerate(self.bufs)]
         self.ffn_ws = torch.zeros((K.moe_ffn_workspace_bytes(self.descs, self.cfg),), dtype=torch.uint8, device=dev)
 
     @staticmethod
-    def _desc(i: int, b: OpBuffers) -> OpDesc:
+    def _desc(i: int, b: OpBuffers, fused_gather: bool = False) -> OpDesc:
         s, w = b.spec, b.spec.weights
         p = lambda t: None if t is None else t.data_ptr()  # noqa: E731
-        return OpDesc(phase=s.phase, layer=s.layer, E_local=s.E_local, H=w.H, I=w.I, capacity=b.capacity,
+        gathered = {}
+        if fused_gather:
+            gathered = dict(x=p(s.x), x_scales=p(s.x_scales), row_to_assign=p(b.row_to_assign), T=b.T,
+                            top_k=s.top_k)
+        return OpDesc(**gathered, phase=s.phase, layer=s.layer, E_local=s.E_local, H=w.H, I=w.I, capacity=b.capacity,
                       row_align=b.row_align, dtype=w.dtype, counts=p(b.counts), offsets=p(b.offsets),
                       x_perm=p(b.x_perm), x_perm_scales=p(b.x_perm_scales), w_gate_up=p(w.w_gate_up),
                       w_gate_up_scales=p(w.w_gate_up_scales), w_down=p(w.w_down),

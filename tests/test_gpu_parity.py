@@ -4,6 +4,7 @@ Indices bit-exact; routing weights within 1e-6 relative; expert and combined
 outputs per row/token normwise within 1e-2 (bf16) or 3e-2 (fp8).  Small shapes span several
 tiles and ragged tails; the full-size configurations are checked on every
 index and on sampled tokens the oracle evaluates one by one."""
+import ctypes as C
 import json
 import os
 
@@ -73,7 +74,7 @@ def test_route_empty(dev):
 
 
 # ----------------------------------------------------------------------------- a2 permutation
-def _permute(dev, ids, E, align, x, x_scales=None, capacity=None):
+def _permute(dev, ids, E, align, x, x_scales=None, capacity=None, maps_only=False):
     from paper_2607_18002_amd import ops
     from paper_2607_18002_amd.pipeline import bf16_tensor
     T, k = ids.shape
@@ -91,11 +92,13 @@ def _permute(dev, ids, E, align, x, x_scales=None, capacity=None):
                ws=torch.empty(ops.moe_permute_workspace_bytes(T, k, E), dtype=torch.uint8, device=dev),
                err=torch.zeros(1, dtype=torch.int32, device=dev))
     xp_arg = out["xp"] if fp8 else out["xp"].view(torch.bfloat16)
+    if maps_only:                                            # the copy buffers are not passed
+        xp_arg = out["xps"] = None
     ops.moe_permute(torch.from_numpy(ids).to(dev), E, xd, xs, align, cap, out["counts"], out["offsets"],
                     out["r2a"], out["a2r"], xp_arg, out["xps"], out["ws"], out["err"])
     torch.cuda.synchronize()
     res = {n: (t.cpu().numpy() if t is not None else None) for n, t in out.items()}
-    if not fp8:
+    if not fp8 and not maps_only:
         res["xp"] = res["xp"].view(np.uint16)
     return res, cap
 
@@ -119,6 +122,31 @@ def test_permute_bit_exact(dev, T, k, E, align):
     np.testing.assert_array_equal(got["xp"][:used], ref.x_perm[:used])
     assert np.all(got["r2a"][used:] == -5), "rows past the last segment are left untouched"
     assert got["err"][0] == 0
+
+
+@pytest.mark.parametrize("fp8", [False, True])
+def test_permute_maps_only(dev, fp8):
+    """Without x_perm the call builds the same maps (bit-exact), including the
+    -1 of every padding row inside the segments."""
+    rng = np.random.default_rng(12)
+    T, k, E, align = 900, 8, 24, 64
+    L = rng.standard_normal((T, 2 * E)).astype(np.float32)
+    L[:, 1] += 1.0
+    ids, _ = oracle.route(L, k, 0, E)
+    if fp8:
+        x = rng.integers(0, 255, size=(T, 256), dtype=np.uint8)
+        xs = rng.random((T, 2), dtype=np.float32)
+    else:
+        x, xs = rng.integers(0, 1 << 15, size=(T, 256), dtype=np.uint16), None
+    got, cap = _permute(dev, ids, E, align, x, xs, maps_only=True)
+    ref = oracle.permute(ids, E, align, capacity=cap)
+    used = int(ref.offsets[-1])
+    assert got["err"][0] == 0
+    assert (ref.row_to_assign[:used] == -1).any()
+    np.testing.assert_array_equal(got["counts"], ref.counts)
+    np.testing.assert_array_equal(got["offsets"], ref.offsets)
+    np.testing.assert_array_equal(got["r2a"][:used], ref.row_to_assign[:used])
+    np.testing.assert_array_equal(got["a2r"], ref.assign_to_row)
 
 
 def test_permute_fp8_rows_and_scales(dev):
@@ -238,8 +266,9 @@ def _check_fp8_op(pipe, i, cfg, lay, ph, tol=BF16_TOL):
     np.testing.assert_array_equal(b.counts.cpu().numpy(), p.counts)
     np.testing.assert_array_equal(b.offsets.cpu().numpy(), p.offsets)
     valid = p.row_to_assign >= 0
-    np.testing.assert_array_equal(b.x_perm.cpu().numpy()[valid], p.x_perm[valid])
-    np.testing.assert_array_equal(b.x_perm_scales.cpu().numpy()[valid], p.x_perm_scales[valid])
+    if b.x_perm is not None:                                 # else the FFN gathered x rows itself
+        np.testing.assert_array_equal(b.x_perm.cpu().numpy()[valid], p.x_perm[valid])
+        np.testing.assert_array_equal(b.x_perm_scales.cpu().numpy()[valid], p.x_perm_scales[valid])
     h = oracle.grouped_hidden(oracle.dequant_rows(p.x_perm, p.x_perm_scales), p.counts, p.offsets, lay.weights)
     codes, sc = oracle.quantize_rows(h[valid])
     g_codes, g_sc = b.h.cpu().numpy()[valid], b.h_scales.cpu().numpy()[valid].astype(np.float64)
@@ -271,17 +300,38 @@ def test_tiny_config_both_phases_one_launch(dev):
 
 @pytest.mark.parametrize("H,I,T_p,T_d,E_g,E_l,k", [(512, 256, 700, 90, 64, 8, 4), (256, 768, 300, 300, 16, 16, 2),
                                                    (768, 512, 1100, 45, 128, 12, 8)])
-def test_small_ragged_configs(dev, H, I, T_p, T_d, E_g, E_l, k):
+@pytest.mark.parametrize("fused", [False, True], ids=["x_perm", "gathered"])
+def test_small_ragged_configs(dev, H, I, T_p, T_d, E_g, E_l, k, fused):
     cfg = custom_config(2, cfg_id=200 + H + I, H=H, I=I, prefill_tokens=T_p, decode_tokens=T_d,
                         E_global=E_g, E_local=E_l, top_k=k, zipf_s=(1.3,))
     lay = make_layer(cfg, 0)
     lay.phases[0].logits[:, 3] = -100.0                      # local expert 3 receives no prefill row
     specs, lay, _ = layer_specs(cfg, 0, dev, lay=lay)
-    pipe = _run_pipeline(dev, specs, trace_capacity=1 << 16)
+    pipe = _run_pipeline(dev, specs, trace_capacity=1 << 16, fused_gather=fused)
     assert pipe.statuses() == (0, 0)
     assert pipe.bufs[0].counts.cpu().numpy()[3] == 0
     for i, ph in enumerate(lay.phases):
         _check_op(pipe, i, cfg, lay, ph)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_gathered_operand_matches_the_copy_bitwise(dev, dtype):
+    """GEMM-1 reading x through row_to_assign performs the same arithmetic as
+    reading the permuted copy: h and y_perm are bit-identical."""
+    base = 2 if dtype == "bf16" else 5
+    cfg = custom_config(base, cfg_id=700 + base, H=512, I=512, prefill_tokens=500, decode_tokens=37,
+                        E_global=64, E_local=8, top_k=4, zipf_s=(1.3,))
+    specs, lay, _ = layer_specs(cfg, 0, dev)
+    a = _run_pipeline(dev, specs)
+    b = _run_pipeline(dev, specs, fused_gather=True)
+    assert a.statuses() == (0, 0) and b.statuses() == (0, 0)
+    for ba, bb in zip(a.bufs, b.bufs):
+        valid = (ba.row_to_assign >= 0).cpu().numpy()
+        assert torch.equal(ba.row_to_assign, bb.row_to_assign)
+        assert np.array_equal(ba.h.view(torch.uint8).cpu().numpy()[valid], bb.h.view(torch.uint8).cpu().numpy()[valid])
+        assert np.array_equal(ba.y_perm.view(torch.int16).cpu().numpy()[valid],
+                              bb.y_perm.view(torch.int16).cpu().numpy()[valid])
+        assert torch.equal(ba.y.view(torch.int16), bb.y.view(torch.int16))
 
 
 def test_token_without_local_expert_is_exact_zero(dev):
@@ -296,7 +346,7 @@ def test_token_without_local_expert_is_exact_zero(dev):
     _check_op(pipe, 0, cfg, lay, lay.phases[0])
 
 
-def _sampled_full_size(dev, cfg_id, layers=(0,), n_sample=10, tol=BF16_TOL, h_fp8_tol=None):
+def _sampled_full_size(dev, cfg_id, layers=(0,), n_sample=10, tol=BF16_TOL, h_fp8_tol=None, fused_gather=False):
     """Full-size configuration: every index bit-exact, sampled tokens' outputs
     against the oracle evaluated token by token."""
     from paper_2607_18002_amd.pipeline import bits_of
@@ -306,7 +356,7 @@ def _sampled_full_size(dev, cfg_id, layers=(0,), n_sample=10, tol=BF16_TOL, h_fp
         s, lay, _ = layer_specs(cfg, layer, dev)
         specs += s
         lays += [(lay, ph) for ph in lay.phases]
-    pipe = _run_pipeline(dev, specs, trace_capacity=0)
+    pipe = _run_pipeline(dev, specs, trace_capacity=0, fused_gather=fused_gather)
     assert pipe.statuses() == (0, 0)
     rng = np.random.default_rng(cfg_id)
     worst = 0.0
@@ -356,6 +406,15 @@ def test_full_size_mixed_config_two_layers(dev):
     _sampled_full_size(dev, 4, layers=(0, 1), n_sample=6)
 
 
+def test_full_size_mixed_config_gathered(dev):
+    """The mixed configuration with GEMM-1 reading x through row_to_assign."""
+    _sampled_full_size(dev, 4, n_sample=6, fused_gather=True)
+
+
+def test_full_size_fp8_mixed_config_gathered(dev):
+    _sampled_full_size(dev, 5, n_sample=6, tol=FP8_TOL, fused_gather=True)
+
+
 def test_full_size_fp8_mixed_config(dev):
     """fp8 e4m3 with 128 x 128 weight scales and 1 x 128 activation scales,
     H 6144, I 2048, 4096 prefill + 1024 decode tokens in one launch: within
@@ -365,7 +424,8 @@ def test_full_size_fp8_mixed_config(dev):
 
 @pytest.mark.parametrize("H,I,T_p,T_d,E_g,E_l,k", [(512, 256, 600, 70, 64, 8, 4), (256, 512, 200, 200, 16, 16, 2),
                                                    (768, 768, 900, 33, 128, 12, 8)])
-def test_fp8_small_configs(dev, H, I, T_p, T_d, E_g, E_l, k):
+@pytest.mark.parametrize("fused", [False, True], ids=["x_perm", "gathered"])
+def test_fp8_small_configs(dev, H, I, T_p, T_d, E_g, E_l, k, fused):
     """fp8 path on ragged shapes: 32- and 64-row tiles, several row tiles per
     expert, an expert without rows; checked stage by stage (_check_fp8_op).
     At these small widths the fp8 rounding of h alone can exceed 3e-2 against
@@ -376,7 +436,7 @@ def test_fp8_small_configs(dev, H, I, T_p, T_d, E_g, E_l, k):
     lay = make_layer(cfg, 0)
     lay.phases[0].logits[:, 2] = -100.0                      # local expert 2 receives no prefill row
     specs, lay, _ = layer_specs(cfg, 0, dev, lay=lay)
-    pipe = _run_pipeline(dev, specs, trace_capacity=1 << 16)
+    pipe = _run_pipeline(dev, specs, trace_capacity=1 << 16, fused_gather=fused)
     assert pipe.statuses() == (0, 0)
     assert pipe.bufs[0].counts.cpu().numpy()[2] == 0
     assert pipe.bufs[0].row_align == 64
@@ -449,3 +509,31 @@ def test_pack_weights_layout(dev):
                     want[:, pos:pos + 8] = w[:, row, col:col + 8]
                     pos += 8
     np.testing.assert_array_equal(got, want)
+
+
+def test_gathered_operand_argument_errors(dev):
+    """The GEMM-1 operand is exactly one of x_perm and x; a gathered operand
+    needs its row map, T and top_k.  Rejected on the host, nothing launched."""
+    from paper_2607_18002_amd import _lib
+    from paper_2607_18002_amd.pipeline import MoEPipeline
+    cfg = custom_config(2, cfg_id=710, H=256, I=256, prefill_tokens=64, decode_tokens=0, E_global=16, E_local=8,
+                        top_k=2)
+    specs, _, _ = layer_specs(cfg, 0, dev)
+    pipe = MoEPipeline(specs)
+    lib = _lib.load_library()
+    d = pipe.descs[0]
+    cases = [dict(x=specs[0].x.data_ptr()),                                            # both operands
+             dict(x_perm=None, x=specs[0].x.data_ptr()),                              # no row map
+             dict(x_perm=None, x=specs[0].x.data_ptr(), row_to_assign=pipe.bufs[0].row_to_assign.data_ptr(),
+                  T=64, top_k=0),
+             dict(x_perm=None)]                                                        # neither
+    for kw in cases:
+        bad = _lib.OpDesc.from_buffer_copy(d)
+        for k, v in kw.items():
+            setattr(bad, k, v)
+        arr = (_lib.OpDesc * 1)(bad)
+        rc = lib.moe_grouped_ffn_persistent(arr, 1, C.byref(pipe.cfg), pipe.ffn_ws.data_ptr(),
+                                            pipe.status.data_ptr(), None)
+        assert rc == _lib.MOE_ERR_INVALID_ARG, (kw, rc)
+    torch.cuda.synchronize()
+    assert int(pipe.status.item()) == 0
