@@ -115,7 +115,10 @@ moe_status_t moe_topk_route(const float* logits, int32_t T, int32_t E_global, in
  *                 x_perm NULL: only the maps are built (padding rows of
  *                 row_to_assign still set to -1); x and x_scales may then be
  *                 NULL -- the FFN gathers its rows from x itself (moe_op_desc.x)
- *  workspace      moe_permute_workspace_bytes(T, top_k, E_local) bytes
+ *  workspace      moe_permute_workspace_bytes(T, top_k, E_local) bytes of
+ *                 device memory, zero before its first use (allocate it
+ *                 zeroed); every call leaves its first 256 bytes zero again.
+ *                 Calls that share a workspace must not overlap in time.
  *  error_flag     device i32 status word (data errors; not cleared here)
  * Limits: 1 <= E_local <= 1024, H a multiple of 128.
  */

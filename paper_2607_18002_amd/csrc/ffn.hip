@@ -406,7 +406,11 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
                 t = __shfl(t, 0, 64);
                 if (t < __shfl(own_size, o, 64)) src = myx;
             }
-            if (src < 0) {                                           // steal: the queue with most tiles left
+            // steal: the queue with most tiles left; a lost race tries again,
+            // so the op is left only once every one of its queues is empty.
+            // A failed claim means that queue's counter passed its size for
+            // good, so there are at most kXcds failures: the loop ends.
+            while (src < 0) {
                 const XQueue* qx = xq_of(a.ws, o, lane & (kXcds - 1));
                 int left = 0;
                 if (lane < kXcds) left = ld_relaxed_agent(&qx->size) - ld_relaxed_agent(&qx->claim);
@@ -418,14 +422,14 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
                 }
                 best = __shfl(best, 0, 64);
                 who = __shfl(who, 0, 64);
-                if (best <= 0) continue;
+                if (best <= 0) break;
                 if (lane == 0) t = atomicAdd(&xq_of(a.ws, o, who)->claim, 1);
                 t = __shfl(t, 0, 64);
                 int sz = 0;
                 if (lane == 0) sz = ld_relaxed_agent(&xq_of(a.ws, o, who)->size);
-                if (t >= __shfl(sz, 0, 64)) continue;
-                src = who;
+                if (t < __shfl(sz, 0, 64)) src = who;
             }
+            if (src < 0) continue;
             const OpArg& op = a.op[o];
             const uint64_t* table = (const uint64_t*)(arr_of(a.ws) + op.table_off);
             int m_lo, n_mt;

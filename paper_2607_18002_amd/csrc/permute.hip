@@ -3,18 +3,20 @@
 // "One-Sided Dispatch and Combine": each expert's destination and final offset
 // are fixed after routing, before the activations are written).
 //
-// Four launches on the caller's stream:
-//   count   : per-chunk expert histogram in LDS (512 assignments per block)
-//   scan    : expert counts, padded segment offsets, per-(chunk, expert) bases;
-//             each expert's prefix over chunks is split across 1024/E threads
+// Two launches on the caller's stream, three with the activation copy:
+//   count   : per-chunk expert histogram in LDS (512 assignments per block);
+//             the last block to finish (a ticket counter in the workspace)
+//             runs the scan: expert counts, padded segment offsets and the
+//             per-(chunk, expert) bases, each expert's prefix over chunks
+//             split across 256/E threads
 //   scatter : stable rank of every assignment inside its chunk, built from
 //             wave ballots (rank = popcount(match & lanes-below)) plus per-wave
 //             and per-iteration running counts -> row_to_assign / assign_to_row.
 //             The result is the unique order "ascending assignment a = t*k+j",
-//             so it is bit-exact and independent of scheduling.
-//   gather  : one wave per row copies x[a / k] (16-byte vectors) into x_perm,
-//             zero-fills padding rows and marks them -1; without x_perm (the
-//             FFN then gathers its rows itself) it only marks padding rows.
+//             so it is bit-exact and independent of scheduling.  The same
+//             launch marks every padding row of the segments -1.
+//   gather  : only with x_perm: one wave per row copies x[a / k] (16-byte
+//             vectors) into x_perm and zero-fills padding rows.
 #include "common.hpp"
 
 namespace {
@@ -25,10 +27,47 @@ constexpr int kThreads = 256;
 constexpr int kIters = 2;
 constexpr int kChunk = kThreads * kIters;   // assignments per block
 
-__global__ __launch_bounds__(256) void permute_count_kernel(const int32_t* __restrict__ ids, int A, int E,
-                                                           int32_t* __restrict__ blk_cnt,
+// Exclusive prefix over the E padded segment sizes by one 256-thread block:
+// each thread scans a run of up to 4 experts, the run totals are scanned in LDS.
+__device__ void block_offsets(int E, int align, int capacity, const int32_t* tot, int32_t* padded_off,
+                              int32_t* counts, int32_t* offsets, int32_t* err) {
+    __shared__ int32_t run_sum[kThreads];
+    const int t = threadIdx.x;
+    const int per = (E + kThreads - 1) / kThreads;             // 1..4 experts per thread
+    const int e0 = t * per, e1 = min(E, e0 + per);
+    int sum = 0;
+    for (int e = e0; e < e1; ++e) sum += ((tot[e] + align - 1) / align) * align;
+    run_sum[t] = sum;
+    __syncthreads();
+    for (int off = 1; off < kThreads; off <<= 1) {             // inclusive Hillis-Steele scan of the runs
+        const int v = (t >= off) ? run_sum[t - off] : 0;
+        __syncthreads();
+        run_sum[t] += v;
+        __syncthreads();
+    }
+    int base = run_sum[t] - sum;
+    for (int e = e0; e < e1; ++e) {
+        counts[e] = tot[e];
+        offsets[e] = base;
+        padded_off[e] = base;
+        base += ((tot[e] + align - 1) / align) * align;
+    }
+    if (t == kThreads - 1) {
+        offsets[E] = run_sum[t];
+        if (run_sum[t] > capacity) set_status(err, MOE_ERR_CAPACITY);
+    }
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(256) void permute_count_kernel(const int32_t* __restrict__ ids, int A, int E, int NB,
+                                                           int align, int capacity, unsigned* __restrict__ ticket,
+                                                           int32_t* __restrict__ blk_cnt,   // counts, then bases
+                                                           int32_t* __restrict__ counts,
+                                                           int32_t* __restrict__ offsets,
                                                            int32_t* __restrict__ err) {
-    extern __shared__ int32_t hist[];
+    extern __shared__ int32_t hist[];                          // [E] histogram, later [E] totals + [E] offsets
+    __shared__ int32_t part[kThreads * 4];                     // per (expert, run): run sum, then run base
+    __shared__ int s_last;
     for (int e = threadIdx.x; e < E; e += kThreads) hist[e] = 0;
     __syncthreads();
     const int base = blockIdx.x * kChunk;
@@ -42,54 +81,59 @@ __global__ __launch_bounds__(256) void permute_count_kernel(const int32_t* __res
     }
     __syncthreads();
     for (int e = threadIdx.x; e < E; e += kThreads) blk_cnt[(size_t)blockIdx.x * E + e] = hist[e];
-}
+    // Publish this block's counts, then take a ticket; the last block scans.
+    // atomicInc wraps to 0 on the last ticket, so the counter is ready for the next call.
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) s_last = atomicInc(ticket, (unsigned)(NB - 1)) == (unsigned)(NB - 1);
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
 
-__global__ __launch_bounds__(1024) void permute_scan_kernel(int NB, int E, int align, int capacity,
-                                                           int32_t* __restrict__ blk_cnt,   // in: counts; out: bases
-                                                           int32_t* __restrict__ counts,
-                                                           int32_t* __restrict__ offsets,
-                                                           int32_t* __restrict__ err) {
-    __shared__ int32_t part[1024];       // per thread: the sum of its run of chunks, then its run's base
-    __shared__ int32_t padded[1024];
-    __shared__ int32_t scan[1024];
-    // P threads per expert (P = 1024 / E rounded down to a power of two); thread
-    // (e, j) owns chunks [j*R, (j+1)*R) of expert e, R = ceil(NB / P).
+    // Scan.  P threads per expert (the largest power of two with P*E <= 256, at
+    // least 1); unit u = (e, j) sums chunks [j*R, (j+1)*R) of expert e.
     int P = 1;
-    while (P * 2 * E <= 1024) P *= 2;
+    while (P * 2 * E <= kThreads) P *= 2;
+    const int U = P * E;                                        // <= 1024
     const int R = (NB + P - 1) / P;
-    const int t = threadIdx.x, e = t / P, j = t - e * P;
-    const bool mine = e < E;
-    const int b0 = mine ? j * R : 0, b1 = mine ? min(NB, b0 + R) : 0;
-    int sum = 0;
-    for (int b = b0; b < b1; ++b) sum += blk_cnt[(size_t)b * E + e];
-    part[t] = sum;
+    for (int u = threadIdx.x; u < U; u += kThreads) {
+        const int e = u / P, j = u - e * P;
+        const int b0 = j * R, b1 = min(NB, b0 + R);
+        int sum = 0;
+        int b = b0;
+        for (; b + 8 <= b1; b += 8) {                          // eight independent loads in flight
+            int c[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) c[i] = blk_cnt[(size_t)(b + i) * E + e];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) sum += c[i];
+        }
+        for (; b < b1; ++b) sum += blk_cnt[(size_t)b * E + e];
+        part[u] = sum;
+    }
     __syncthreads();
-    if (mine && j == 0) {                                      // exclusive prefix over the expert's P runs
+    int32_t* tot = hist;                                        // reuse: E totals
+    int32_t* poff = hist + E;                                   // E padded offsets
+    for (int e = threadIdx.x; e < E; e += kThreads) {           // exclusive prefix over the expert's P runs
         int run = 0;
-        for (int q = 0; q < P; ++q) { const int v = part[t + q]; part[t + q] = run; run += v; }
-        scan[e] = run;                                         // total rows of expert e (temporarily)
+        for (int q = 0; q < P; ++q) { const int v = part[e * P + q]; part[e * P + q] = run; run += v; }
+        tot[e] = run;
     }
     __syncthreads();
-    const int tot = (t < E) ? scan[t] : 0;
-    if (t < E) counts[t] = tot;
-    padded[t] = (t < E) ? ((tot + align - 1) / align) * align : 0;
-    __syncthreads();
-    scan[t] = padded[t];
-    __syncthreads();
-    for (int off = 1; off < 1024; off <<= 1) {                 // inclusive Hillis-Steele scan over experts
-        const int v = (t >= off) ? scan[t - off] : 0;
-        __syncthreads();
-        scan[t] += v;
-        __syncthreads();
-    }
-    if (t < E) offsets[t] = scan[t] - padded[t];
-    if (t == E - 1) {
-        offsets[E] = scan[t];
-        if (scan[t] > capacity) set_status(err, MOE_ERR_CAPACITY);
-    }
-    if (mine) {                                                // bases of this thread's chunks
-        int run = scan[e] - padded[e] + part[t];
-        for (int b = b0; b < b1; ++b) {
+    block_offsets(E, align, capacity, tot, poff, counts, offsets, err);
+    for (int u = threadIdx.x; u < U; u += kThreads) {           // bases of the unit's chunks
+        const int e = u / P, j = u - e * P;
+        const int b0 = j * R, b1 = min(NB, b0 + R);
+        int run = poff[e] + part[u];
+        int b = b0;
+        for (; b + 8 <= b1; b += 8) {
+            int c[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) c[i] = blk_cnt[(size_t)(b + i) * E + e];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) { blk_cnt[(size_t)(b + i) * E + e] = run; run += c[i]; }
+        }
+        for (; b < b1; ++b) {
             const int c = blk_cnt[(size_t)b * E + e];
             blk_cnt[(size_t)b * E + e] = run;
             run += c;
@@ -99,9 +143,16 @@ __global__ __launch_bounds__(1024) void permute_scan_kernel(int NB, int E, int a
 
 __global__ __launch_bounds__(256) void permute_scatter_kernel(const int32_t* __restrict__ ids, int A, int E,
                                                              int capacity, const int32_t* __restrict__ blk_base,
+                                                             const int32_t* __restrict__ counts,
+                                                             const int32_t* __restrict__ offsets,
                                                              int32_t* __restrict__ row_to_assign,
                                                              int32_t* __restrict__ assign_to_row,
                                                              int32_t* __restrict__ err) {
+    // padding rows [offsets[e] + counts[e], offsets[e+1]) of experts e = block, block + grid, ...
+    for (int e = blockIdx.x; e < E; e += gridDim.x) {
+        const int r0 = offsets[e] + counts[e], r1 = min(offsets[e + 1], capacity);
+        for (int r = r0 + (int)threadIdx.x; r < r1; r += kThreads) row_to_assign[r] = -1;
+    }
     extern __shared__ int32_t sm[];
     int32_t* running = sm;           // [E]   rows handed out in earlier iterations
     int32_t* wcnt = sm + E;          // [4][E] per-wave counts of the current iteration
@@ -171,10 +222,6 @@ __global__ __launch_bounds__(256) void permute_gather_kernel(const int32_t* __re
         }
         const bool valid = (r - soff[lo]) < soff[E + 1 + lo];
         const int a = valid ? row_to_assign[r] : -1;
-        if (!x_perm) {                                        // maps only
-            if (a < 0 && lane == 0) row_to_assign[r] = -1;
-            continue;
-        }
         uint4* dst = x_perm + (size_t)r * row_vecs;
         if (a >= 0) {
             const uint4* src = x + (size_t)(a / k) * row_vecs;
@@ -186,10 +233,13 @@ __global__ __launch_bounds__(256) void permute_gather_kernel(const int32_t* __re
             for (int v = lane; v < row_vecs; v += 64) dst[v] = z;
             if (xs_perm)
                 for (int v = lane; v < n_scales; v += 64) xs_perm[(size_t)r * n_scales + v] = 0.f;
-            if (lane == 0) row_to_assign[r] = -1;
         }
     }
 }
+
+// Workspace: a 256-byte header (word 0: the count kernel's ticket counter),
+// then the [chunks][E] counts / bases.
+constexpr size_t kWsHeader = 256;
 
 int num_chunks(int32_t T, int32_t top_k) {
     const int64_t A = (int64_t)T * top_k;
@@ -201,7 +251,7 @@ int num_chunks(int32_t T, int32_t top_k) {
 extern "C" size_t moe_permute_workspace_bytes(int32_t T, int32_t top_k, int32_t E_local) {
     if (T < 0 || top_k < 1 || E_local < 1) return 0;
     const int nb = num_chunks(T, top_k);
-    return (size_t)(nb > 0 ? nb : 1) * (size_t)E_local * sizeof(int32_t) + 256;
+    return kWsHeader + (size_t)(nb > 0 ? nb : 1) * (size_t)E_local * sizeof(int32_t);
 }
 
 extern "C" moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t top_k, int32_t E_local,
@@ -233,16 +283,17 @@ extern "C" moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t 
     hipStream_t s = (hipStream_t)stream;
     const int A = T * top_k;
     const int nb = num_chunks(T, top_k);
-    int32_t* blk = (int32_t*)workspace;
-    if (nb > 0) {
-        hipLaunchKernelGGL(permute_count_kernel, dim3(nb), dim3(kThreads), E_local * sizeof(int32_t), s, topk_ids, A,
-                           E_local, blk, error_flag);
-    }
-    hipLaunchKernelGGL(permute_scan_kernel, dim3(1), dim3(1024), 0, s, nb, E_local, row_align, capacity, blk, counts,
-                       offsets, error_flag);
-    if (nb > 0) {
-        hipLaunchKernelGGL(permute_scatter_kernel, dim3(nb), dim3(kThreads), 5 * E_local * sizeof(int32_t), s, topk_ids,
-                           A, E_local, capacity, blk, row_to_assign, assign_to_row, error_flag);
+    const int nb1 = nb > 0 ? nb : 1;                           // T == 0: one block writes zero counts
+    unsigned* ticket = (unsigned*)workspace;
+    int32_t* blk = (int32_t*)((char*)workspace + kWsHeader);
+    hipLaunchKernelGGL(permute_count_kernel, dim3(nb1), dim3(kThreads), 2 * E_local * sizeof(int32_t), s, topk_ids,
+                       A, E_local, nb1, row_align, capacity, ticket, blk, counts, offsets, error_flag);
+    hipLaunchKernelGGL(permute_scatter_kernel, dim3(nb1), dim3(kThreads), 5 * E_local * sizeof(int32_t), s, topk_ids,
+                       A, E_local, capacity, blk, counts, offsets, row_to_assign, assign_to_row, error_flag);
+    if (!x_perm) {
+        const hipError_t err = hipGetLastError();
+        if (err != hipSuccess) return fail(MOE_ERR_HIP, "moe_permute: launch failed: %s", hipGetErrorString(err));
+        return MOE_OK;
     }
     const int row_bytes = fp8 ? H : 2 * H;
     const int rows_max = capacity;
@@ -251,7 +302,7 @@ extern "C" moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t 
     if (grid < 1) grid = 1;
     hipLaunchKernelGGL(permute_gather_kernel, dim3(grid), dim3(256), (2 * E_local + 1) * sizeof(int32_t), s, counts,
                        offsets, E_local, top_k, capacity, (const uint4*)x, row_bytes / 16, x_scales,
-                       fp8 ? H / 128 : 0, row_to_assign, (uint4*)x_perm, (fp8 && x_perm) ? x_perm_scales : nullptr);
+                       fp8 ? H / 128 : 0, row_to_assign, (uint4*)x_perm, fp8 ? x_perm_scales : nullptr);
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(MOE_ERR_HIP, "moe_permute: launch failed: %s", hipGetErrorString(err));
     return MOE_OK;

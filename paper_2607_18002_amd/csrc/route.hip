@@ -4,7 +4,9 @@
 // order keys: high half = the fp32 logit mapped to an unsigned integer that
 // orders like the float (-0.0 folded onto +0.0), low half = ~expert so that
 // equal logits prefer the lower expert index.  Each of the k rounds takes a
-// wave-wide max with xor-shuffles and retires the winner; lane j keeps slot j.
+// wave-wide max and retires the winner; lane j keeps slot j.  The wave-wide
+// reductions stay in the vector ALU: DPP quad permutes and row mirrors give
+// every lane its 16-lane row's result, four lane reads combine the rows.
 #include "common.hpp"
 
 namespace {
@@ -24,6 +26,44 @@ __device__ __forceinline__ float key_value(uint64_t key) {
     return __uint_as_float(u);
 }
 
+// DPP controls: quad permutes [1,0,3,2] and [2,3,0,1], half-row and row mirrors.
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
+
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+    const int lo = __builtin_amdgcn_mov_dpp((int)(uint32_t)v, CTRL, 0xF, 0xF, false);
+    const int hi = __builtin_amdgcn_mov_dpp((int)(uint32_t)(v >> 32), CTRL, 0xF, 0xF, false);
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+__device__ __forceinline__ uint64_t max64(uint64_t a, uint64_t b) { return a > b ? a : b; }
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Maximum of v over the wave, the same value in every lane.
+__device__ __forceinline__ uint64_t wave_max64(uint64_t v) {
+    v = max64(v, dpp64<kDppXor1>(v));
+    v = max64(v, dpp64<kDppXor2>(v));
+    v = max64(v, dpp64<kDppHalfMirror>(v));
+    v = max64(v, dpp64<kDppMirror>(v));                  // every lane: its row's maximum
+    return max64(max64(readlane64(v, 0), readlane64(v, 16)), max64(readlane64(v, 32), readlane64(v, 48)));
+}
+
+// Sum of v over the wave, the same value in every lane.
+__device__ __forceinline__ float wave_sum(float v) {
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kDppXor1, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kDppXor2, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kDppHalfMirror, 0xF, 0xF, false));
+    v += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), kDppMirror, 0xF, 0xF, false));
+    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return (r0 + r1) + (r2 + r3);
+}
+
 template <int EPL>
 __global__ __launch_bounds__(256) void topk_route_kernel(const float* __restrict__ logits, int T, int E, int k,
                                                         int local_begin, int E_local, int32_t* __restrict__ ids,
@@ -32,11 +72,15 @@ __global__ __launch_bounds__(256) void topk_route_kernel(const float* __restrict
     const int t = blockIdx.x * kTokensPerBlock + (threadIdx.x >> 6);
     if (t >= T) return;  // wave-uniform
     const float* row = logits + (size_t)t * E;
+    // all loads first (clamped in-row indices, no branches), so they are in flight together
+    float v[EPL];
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) v[i] = row[min(lane + 64 * i, E - 1)];
     uint64_t key[EPL];
 #pragma unroll
     for (int i = 0; i < EPL; ++i) {
         const int e = lane + 64 * i;
-        key[i] = (e < E) ? order_key(row[e], (uint32_t)e) : 0ull;
+        key[i] = (e < E) ? order_key(v[i], (uint32_t)e) : 0ull;
     }
     int my_e = -1;
     float my_v = 0.f;
@@ -44,11 +88,7 @@ __global__ __launch_bounds__(256) void topk_route_kernel(const float* __restrict
         uint64_t best = 0;
 #pragma unroll
         for (int i = 0; i < EPL; ++i) best = key[i] > best ? key[i] : best;
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-            const uint64_t o = __shfl_xor(best, off, 64);
-            best = o > best ? o : best;
-        }
+        best = wave_max64(best);
         const int e = (int)(0xFFFFFFFFu - (uint32_t)best);
 #pragma unroll
         for (int i = 0; i < EPL; ++i)
@@ -58,11 +98,9 @@ __global__ __launch_bounds__(256) void topk_route_kernel(const float* __restrict
             my_v = key_value(best);
         }
     }
-    const float m = __shfl(my_v, 0, 64);                 // the largest selected logit
+    const float m = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_v), 0));   // the largest selected logit
     const float ex = (lane < k) ? expf(my_v - m) : 0.f;
-    float s = ex;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+    const float s = wave_sum(ex);
     if (lane < k) {
         const int loc = my_e - local_begin;
         ids[(size_t)t * k + lane] = (loc >= 0 && loc < E_local) ? loc : -1;

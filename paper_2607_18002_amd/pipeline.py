@@ -145,7 +145,7 @@ class MoEPipeline:
                 h_scales=torch.zeros((cap, I // 128), dtype=torch.float32, device=dev) if fp8 else None,
                 y_perm=torch.zeros((cap, H), dtype=torch.bfloat16, device=dev),
                 y=torch.empty((T, H), dtype=y_dtype, device=dev),
-                perm_ws=torch.empty((max(1, K.moe_permute_workspace_bytes(T, s.top_k, s.E_local)),),
+                perm_ws=torch.zeros((max(1, K.moe_permute_workspace_bytes(T, s.top_k, s.E_local)),),
                                     dtype=torch.uint8, device=dev),
                 done_word=torch.zeros(1, dtype=torch.int32, device=dev),
             ))

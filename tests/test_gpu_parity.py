@@ -89,7 +89,7 @@ def _permute(dev, ids, E, align, x, x_scales=None, capacity=None, maps_only=Fals
                a2r=torch.full((T * k,), -5, dtype=torch.int32, device=dev),
                xp=torch.full((cap, H), 7, dtype=torch.uint8 if fp8 else torch.int16, device=dev),
                xps=torch.full((cap, H // 128), 7.0, device=dev) if fp8 else None,
-               ws=torch.empty(ops.moe_permute_workspace_bytes(T, k, E), dtype=torch.uint8, device=dev),
+               ws=torch.zeros(ops.moe_permute_workspace_bytes(T, k, E), dtype=torch.uint8, device=dev),
                err=torch.zeros(1, dtype=torch.int32, device=dev))
     xp_arg = out["xp"] if fp8 else out["xp"].view(torch.bfloat16)
     if maps_only:                                            # the copy buffers are not passed
@@ -122,6 +122,36 @@ def test_permute_bit_exact(dev, T, k, E, align):
     np.testing.assert_array_equal(got["xp"][:used], ref.x_perm[:used])
     assert np.all(got["r2a"][used:] == -5), "rows past the last segment are left untouched"
     assert got["err"][0] == 0
+
+
+def test_permute_workspace_reused_across_sizes(dev):
+    """One zeroed workspace serves calls of different sizes in turn: the
+    last-block ticket returns to zero after every call."""
+    from paper_2607_18002_amd import ops
+    rng = np.random.default_rng(21)
+    E, k, align, H = 16, 4, 32, 128
+    ws = torch.zeros(ops.moe_permute_workspace_bytes(3000, k, E), dtype=torch.uint8, device=dev)
+    for T in (3000, 7, 1, 0, 1500, 3000):
+        L = rng.standard_normal((max(T, 1), 2 * E)).astype(np.float32)[:T]
+        ids, _ = oracle.route(L, k, 0, E) if T else (np.zeros((0, k), np.int32), None)
+        cap = T * min(k, E) + E * (align - 1)
+        counts = torch.full((E,), -5, dtype=torch.int32, device=dev)
+        offsets = torch.full((E + 1,), -5, dtype=torch.int32, device=dev)
+        r2a = torch.full((cap,), -5, dtype=torch.int32, device=dev)
+        a2r = torch.full((max(T * k, 1),), -5, dtype=torch.int32, device=dev)
+        err = torch.zeros(1, dtype=torch.int32, device=dev)
+        x = torch.zeros((max(T, 1), H), dtype=torch.bfloat16, device=dev)[:T]
+        ops.moe_permute(torch.from_numpy(ids).to(dev), E, x, None, align, cap, counts, offsets, r2a, a2r, None,
+                        None, ws, err)
+        torch.cuda.synchronize()
+        ref = oracle.permute(ids, E, align, capacity=cap)
+        used = int(ref.offsets[-1])
+        assert int(err.item()) == 0
+        np.testing.assert_array_equal(counts.cpu().numpy(), ref.counts)
+        np.testing.assert_array_equal(offsets.cpu().numpy(), ref.offsets)
+        np.testing.assert_array_equal(r2a.cpu().numpy()[:used], ref.row_to_assign[:used])
+        np.testing.assert_array_equal(a2r.cpu().numpy()[:T * k], ref.assign_to_row)
+        assert int(ws[:256].view(torch.int32).abs().sum().item()) == 0
 
 
 @pytest.mark.parametrize("fp8", [False, True])
