@@ -190,24 +190,27 @@ __global__ __launch_bounds__(256) void apk_init_kernel(const InitArgs a) {
 }
 
 // ----------------------------------------------------------------------------- tiles
-template <class S>
-__device__ __forceinline__ void run_tile_cls(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds) {
+template <class S, class Hook>
+__device__ __forceinline__ void run_tile_cls(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds,
+                                             Hook hook) {
     const long H = op.H, I = op.I;
     if (stage == 1) {
         const bool g = op.rmap != nullptr;
         gemm_tile_bf16_rows<S, true, true>(rows32, g ? op.x : op.x + row0 * H, (int)H,
                                      op.wgu + (long)e * 2 * I * H + (long)nb * (S::BN / 2) * H, (int)H, (int)I,
                                      (int)H, op.h + row0 * I + nb * (S::BN / 2), (int)I, lds,
-                                     g ? op.rmap + row0 : nullptr, op.top_k, op.T);
+                                     g ? op.rmap + row0 : nullptr, op.top_k, op.T, hook);
     } else {
         gemm_tile_bf16_rows<S, false, true>(rows32, op.h + row0 * I, (int)I, op.wd + (long)e * H * I + (long)nb * S::BN * I,
-                                      (int)I, 0, (int)I, op.y + row0 * H + nb * S::BN, (int)H, lds);
+                                      (int)I, 0, (int)I, op.y + row0 * H + nb * S::BN, (int)H, lds, nullptr, 1, 0,
+                                      hook);
     }
 }
 
 // fp8: GEMM-1 tiles cover 128 h columns (one h scale group), GEMM-2 tiles 256 y columns.
+template <class Hook>
 __device__ __forceinline__ void run_tile_fp8(const OpArg& op, int stage, int row0, int rows32, int nb, int e,
-                                             char* lds) {
+                                             char* lds, Hook hook) {
     using S = ShapeF8;
     const long H = op.H, I = op.I;
     const uint8_t* x = (const uint8_t*)op.x;
@@ -219,23 +222,25 @@ __device__ __forceinline__ void run_tile_fp8(const OpArg& op, int stage, int row
                                     (const uint8_t*)op.wgu + (long)e * 2 * I * H + (long)n0 * H, n0, (int)I,
                                     op.wgus + (long)e * (2 * I / 128) * (H / 128), (int)H, h + row0 * I + n0, (int)I,
                                     op.hs + row0 * (I / 128) + nb, (int)(I / 128), lds,
-                                    g ? op.rmap + row0 : nullptr, op.top_k, op.T);
+                                    g ? op.rmap + row0 : nullptr, op.top_k, op.T, hook);
     } else {
         const int n0 = nb * S::BN;
         gemm_tile_fp8_rows<S, false>(rows32, h + row0 * I, (int)I, op.hs + row0 * (I / 128),
                                      (const uint8_t*)op.wd + (long)e * H * I + (long)n0 * I, n0, 0,
                                      op.wds + (long)e * (H / 128) * (I / 128), (int)I, op.y + row0 * H + n0, (int)H,
-                                     nullptr, 0, lds);
+                                     nullptr, 0, lds, nullptr, 1, 0, hook);
     }
 }
 
-__device__ __forceinline__ void run_tile(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds) {
+template <class Hook>
+__device__ __forceinline__ void run_tile(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds,
+                                         Hook hook) {
     // Both bf16 classes currently share one tile shape.
     static_assert(ShapeP::BM == ShapeD::BM && ShapeP::BN == ShapeD::BN && ShapeP::BK == ShapeD::BK, "one shape");
     if (op.cls == CLS_FP8)
-        run_tile_fp8(op, stage, row0, rows32, nb, e, lds);
+        run_tile_fp8(op, stage, row0, rows32, nb, e, lds, hook);
     else
-        run_tile_cls<ShapeP>(op, stage, row0, rows32, nb, e, lds);
+        run_tile_cls<ShapeP>(op, stage, row0, rows32, nb, e, lds, hook);
 }
 
 // ----------------------------------------------------------------------------- scheduler
@@ -281,10 +286,47 @@ __device__ void finish_op(const KArgs& a, int o, int total) {
     add_relaxed_agent(&hdr->ops_done, 1);
 }
 
-// Wave 0 at a tile boundary: commit the previous tile (if any), read the
-// decision words once, and pick the next action for the workgroup.
+// The words a workgroup reads at a tile boundary to pick its next action
+// (wave 0, one op per lane; lane 0 also the header words).  A workgroup
+// coming out of a tile issues them right after its K loop, so that their
+// round trip overlaps the epilogue; they are then older than the boundary by
+// the epilogue's duration.
+struct Polls {
+    int state, own_claim, own_size, total, phase, stop, q;
+    uint32_t abort_v;
+};
+
+__device__ __forceinline__ Polls issue_polls(const KArgs& a) {
+    const int lane = threadIdx.x;
+    const bool has = lane < a.n_ops;
+    const int o_l = has ? lane : 0;
+    const OpDyn* dyn = dyn_of(a.ws);
+    const XQueue* own = xq_of(a.ws, o_l, xcc_id());
+    const Hdr* hdr = hdr_of(a.ws);
+    // every load unconditional (lanes past n_ops read op 0), results selected after
+    const int st = ld_relaxed_agent(&dyn[o_l].state);
+    const int cl = ld_relaxed_agent(&own->claim);
+    const int sz = ld_relaxed_agent(&own->size);
+    const int tot = ld_relaxed_agent(&dyn[o_l].total);
+    const int ph = static_of(a.ws)[o_l].phase;
+    Polls p;
+    p.stop = ld_relaxed_agent(&hdr->stop);
+    p.q = ld_relaxed_agent(&hdr->quota);
+    p.abort_v = a.abort_word ? __hip_atomic_load(a.abort_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) : 0u;
+    p.state = has ? st : ST_DONE;
+    p.own_claim = has ? cl : 0;
+    p.own_size = has ? sz : 0;
+    p.total = has ? tot : 0;
+    p.phase = has ? ph : 0;
+    return p;
+}
+
+// Wave 0 at a tile boundary: commit the previous tile (if any), decide with
+// the polled words (pre, issued after the previous tile's K loop, when
+// have_pre; else read now), claim, and only then wait for the commit's
+// completion count, so the commit and the claim share one round trip.
 __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool have_prev, int64_t& idle,
-                         TabCache* tab) {
+                         TabCache* tab, bool have_pre, Polls pre) {
     const int lane = threadIdx.x;
     Hdr* hdr = hdr_of(a.ws);
     OpDyn* dyn = dyn_of(a.ws);
@@ -295,47 +337,24 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
     Cmd prev;
     if (have_prev) prev = *cmd;
     const unsigned long long t_boundary = wall_ticks();
+    const Polls pl = have_pre ? pre : issue_polls(a);
 
-    // 1. commit: publish the tile's h / y, then count it (the completion count returns later)
+    // 1. commit: count the tile (its device-coherent stores have completed);
+    //    the completion count is read in finish_prev, after the claim
     int done_after = -1;
     unsigned long long t_end = 0;
     if (have_prev && lane == 0) {
-        t_end = wall_ticks();   // every wave's device-coherent stores of the tile have completed
+        t_end = wall_ticks();
         if (prev.stage == 1) {
             int32_t* g1 = (int32_t*)(arr_of(a.ws) + a.op[prev.op].g1_off);
             __hip_atomic_fetch_add(g1 + prev.mtile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        done_after = add_relaxed_agent(&dyn[prev.op].done, 1) + 1;    // result used after the polls
+        done_after = add_relaxed_agent(&dyn[prev.op].done, 1) + 1;
     }
-
-    // 2. poll (all loads independent, issued together)
-    const bool has = lane < a.n_ops;
-    const int o_l = has ? lane : 0;
-    const int myx = xcc_id();
-    const XQueue* own = xq_of(a.ws, o_l, myx);
-    const int state = has ? ld_relaxed_agent(&dyn[o_l].state) : ST_DONE;
-    const int own_claim = has ? ld_relaxed_agent(&own->claim) : 0;
-    const int own_size = has ? ld_relaxed_agent(&own->size) : 0;
-    const int total = has ? ld_relaxed_agent(&dyn[o_l].total) : 0;
-    const int phase = has ? sta[o_l].phase : 0;
-    const int prev_total = __shfl(total, have_prev ? prev.op : 0, 64);
-    int stop = 0, q = 0;
-    if (lane == 0) {
-        stop = ld_relaxed_agent(&hdr->stop);
-        q = ld_relaxed_agent(&hdr->quota);
-        if (!stop && a.abort_word &&
-            __hip_atomic_load(a.abort_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != 0u) {
-            set_status(a.status, MOE_ERR_ABORTED);
-            st_release_agent(&hdr->stop, 1);
-            stop = 1;
-        }
-        if (!stop && idle > a.spin_limit) {                    // nothing claimable for too long
-            set_status(a.status, MOE_ERR_TIMEOUT);
-            st_release_agent(&hdr->stop, 1);
-            stop = 1;
-        }
-        // 3. finish the previous tile's op if that tile was its last; trace it
-        if (have_prev) {
+    const int prev_total = __shfl(pl.total, have_prev ? prev.op : 0, 64);
+    // 3. finish the previous tile's op if that tile was its last; trace it
+    auto finish_prev = [&]() {
+        if (have_prev && lane == 0) {
             if (done_after == prev_total) finish_op(a, prev.op, prev_total);
             if (a.trace) {
                 const int idx = add_relaxed_agent(&hdr->trace_count, 1);
@@ -349,14 +368,36 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
                 }
             }
         }
+    };
+
+    // 2. stop conditions (polled)
+    const int state = pl.state, own_claim = pl.own_claim, own_size = pl.own_size;
+    const int o_l = lane < a.n_ops ? lane : 0;
+    const int phase = pl.phase;
+    const int myx = xcc_id();
+    int stop = 0;
+    if (lane == 0) {
+        stop = pl.stop;
+        if (!stop && pl.abort_v != 0u) {
+            set_status(a.status, MOE_ERR_ABORTED);
+            st_release_agent(&hdr->stop, 1);
+            stop = 1;
+        }
+        if (!stop && idle > a.spin_limit) {                    // nothing claimable for too long
+            set_status(a.status, MOE_ERR_TIMEOUT);
+            st_release_agent(&hdr->stop, 1);
+            stop = 1;
+        }
     }
     if (__shfl(stop, 0, 64)) {
+        finish_prev();
         if (lane == 0) cmd->kind = CMD_EXIT;
         return;
     }
-    q = __shfl(q, 0, 64);
+    const int q = __shfl(pl.q, 0, 64);
     if (__ballot(state != ST_DONE) == 0) {
-        // every op was DONE when polled; ops finished in step 3 are DONE too
+        // every op was DONE when polled; an op the previous tile completes is finished below
+        finish_prev();
         if (lane == 0) cmd->kind = CMD_EXIT;
         return;
     }
@@ -381,6 +422,7 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
         int won = 0;
         if (lane == o) won = atomicCAS(&dyn[o].state, ST_WAIT, ST_INIT) == ST_WAIT;
         if (__ballot(won)) {
+            finish_prev();
             if (lane == 0) { cmd->kind = CMD_INST; cmd->op = o; }
             idle = 0;
             return;
@@ -430,6 +472,7 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
                 if (t < __shfl(sz, 0, 64)) src = who;
             }
             if (src < 0) continue;
+            finish_prev();
             const OpArg& op = a.op[o];
             const uint64_t* table = (const uint64_t*)(arr_of(a.ws) + op.table_off);
             int m_lo, n_mt;
@@ -498,6 +541,7 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
             return;
         }
     }
+    finish_prev();
     if (lane == 0) cmd->kind = CMD_IDLE;
     ++idle;
 }
@@ -586,8 +630,9 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
     const uint64_t t0 = s_t0;
     int64_t idle = 0;
     bool have_prev = false;
+    Polls polls = {};                                         // wave 0: issued after the last tile's K loop
     for (;;) {
-        if (tid < 64) boundary(a, t0, wg, &cmd, have_prev, idle, &tab);
+        if (tid < 64) boundary(a, t0, wg, &cmd, have_prev, idle, &tab, have_prev, polls);
         __syncthreads();
         const int kind = cmd.kind;
         have_prev = false;
@@ -611,7 +656,9 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
         const int nb = __builtin_amdgcn_readfirstlane(cmd.nb);
         const int e = __builtin_amdgcn_readfirstlane(cmd.e);
         __syncthreads();                                      // every thread has read cmd
-        run_tile(a.op[o], stage, row0, rows32, nb, e, lds);
+        run_tile(a.op[o], stage, row0, rows32, nb, e, lds, [&]() {
+            if (tid < 64) polls = issue_polls(a);
+        });
         // Wave 0's release at the commit writes back this XCD's L2; the barrier does
         // not wait for global stores, so each wave first lets its own reach the L2.
         wait_own_stores();

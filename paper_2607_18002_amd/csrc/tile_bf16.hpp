@@ -27,6 +27,13 @@
 
 namespace moeapk {
 
+// A tile calls hook() once, after its K loop and before its epilogue: the
+// caller's chance to issue memory requests whose latency then overlaps the
+// epilogue's stores (NoHook: nothing).
+struct NoHook {
+    __device__ __forceinline__ void operator()() const {}
+};
+
 template <int BM_, int BN_, int BK_>
 struct TileShape {
     static constexpr int BM = BM_, BN = BN_, BK = BK_;
@@ -135,12 +142,13 @@ __device__ __forceinline__ void mma_step(f32x16 (&acc)[MACT][S::NBW], const bf16
 // B   : first B row of the tile (GLU: gate row n0), row stride ldb elements
 // up_rows : GLU only, rows from the gate block to the matching up block (I)
 // out : output tile origin, row stride ldo (bf16); rows [0, 32*MACT) written
-template <class S, bool GLU, int MACT, bool PACKED = false, int D = TileRegs<S, MACT>::DEPTH>
+template <class S, bool GLU, int MACT, bool PACKED = false, int D = TileRegs<S, MACT>::DEPTH,
+          class Hook = NoHook>
 __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, int lda,
                                                const uint16_t* __restrict__ B, int ldb, int up_rows, int K,
                                                uint16_t* __restrict__ out, int ldo, char* lds,
                                                const int32_t* __restrict__ rowmap = nullptr, int k = 1,
-                                               int a_rows = 0) {
+                                               int a_rows = 0, Hook hook = Hook{}) {
     constexpr int CA = TileRegs<S, MACT>::CA;
     const int tid = threadIdx.x, lane = tid & 63, wn = tid >> 6;
 
@@ -227,6 +235,7 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
             __syncthreads();
         }
     }
+    hook();
 
     // Epilogue.  32x32 accumulator layout: lane holds column (lane & 31) and
     // rows (r/4)*8 + (lane/32)*4 + r%4 of its block, r = 0..15.  Each wave
@@ -275,28 +284,29 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
 // The K loop runs whole passes of the B ring: the ring depth for the tile's
 // row count when it divides the number of K steps, else 2 (K is a multiple
 // of 2 * BK).
-template <class S, bool GLU, int MACT, bool PACKED>
+template <class S, bool GLU, int MACT, bool PACKED, class Hook>
 __device__ __forceinline__ void gemm_tile_bf16_depth(const uint16_t* A, int lda, const uint16_t* B, int ldb,
                                                      int up_rows, int K, uint16_t* out, int ldo, char* lds,
-                                                     const int32_t* rowmap, int k, int a_rows) {
+                                                     const int32_t* rowmap, int k, int a_rows, Hook hook) {
     constexpr int D = TileRegs<S, MACT>::DEPTH;
     if ((K / S::BK) % D == 0)
-        gemm_tile_bf16<S, GLU, MACT, PACKED, D>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows);
+        gemm_tile_bf16<S, GLU, MACT, PACKED, D>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows, hook);
     else
-        gemm_tile_bf16<S, GLU, MACT, PACKED, 2>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows);
+        gemm_tile_bf16<S, GLU, MACT, PACKED, 2>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows, hook);
 }
 
 // Dispatch on the number of 32-row blocks holding valid rows (uniform per tile).
-template <class S, bool GLU, bool PACKED>
+template <class S, bool GLU, bool PACKED, class Hook = NoHook>
 __device__ __forceinline__ void gemm_tile_bf16_rows(int rows32, const uint16_t* A, int lda, const uint16_t* B, int ldb,
                                                     int up_rows, int K, uint16_t* out, int ldo, char* lds,
-                                                    const int32_t* rowmap = nullptr, int k = 1, int a_rows = 0) {
+                                                    const int32_t* rowmap = nullptr, int k = 1, int a_rows = 0,
+                                                    Hook hook = Hook{}) {
     static_assert(S::MB == 4, "dispatch written for 128-row tiles");
     switch (rows32 >> 5) {
-        case 1: gemm_tile_bf16_depth<S, GLU, 1, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows); break;
-        case 2: gemm_tile_bf16_depth<S, GLU, 2, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows); break;
-        case 3: gemm_tile_bf16_depth<S, GLU, 3, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows); break;
-        default: gemm_tile_bf16_depth<S, GLU, 4, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows); break;
+        case 1: gemm_tile_bf16_depth<S, GLU, 1, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows, hook); break;
+        case 2: gemm_tile_bf16_depth<S, GLU, 2, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows, hook); break;
+        case 3: gemm_tile_bf16_depth<S, GLU, 3, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows, hook); break;
+        default: gemm_tile_bf16_depth<S, GLU, 4, PACKED>(A, lda, B, ldb, up_rows, K, out, ldo, lds, rowmap, k, a_rows, hook); break;
     }
 }
 

@@ -80,13 +80,13 @@ __device__ __forceinline__ void load_w8(i32x8 (&rw)[S::NBW][S::KK], __amdgpu_buf
 //       a_rows rows; tile row r is its row rowmap[r] / k (rowmap[r] < 0: zero)
 // GLU : out = h codes (ldo bytes per row), osc = h scales (ldsc floats per row);
 //       else out = bf16 rows (ldo elements per row)
-template <class S, bool GLU, int MACT, int D = TileRegsF8<S, MACT>::DEPTH>
+template <class S, bool GLU, int MACT, int D = TileRegsF8<S, MACT>::DEPTH, class Hook = NoHook>
 __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int lda, const float* __restrict__ asc,
                                               const uint8_t* __restrict__ B, int n0, int up_rows,
                                               const float* __restrict__ wsc, int K, void* __restrict__ out, int ldo,
                                               float* __restrict__ osc, int ldsc, char* lds,
                                               const int32_t* __restrict__ rowmap = nullptr, int k = 1,
-                                              int a_rows = 0) {
+                                              int a_rows = 0, Hook hook = Hook{}) {
     constexpr int CA = TileRegsF8<S, MACT>::CA;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wn = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -197,6 +197,7 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
             __syncthreads();
         }
     }
+    hook();
 
     // Accumulator layout: lane holds token 32*i + (lane & 31) and features
     // 32*j + (r/4)*8 + (lane/32)*4 + r%4 of its wave's columns, r = 0..15.
@@ -284,32 +285,33 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
 
 // The K loop runs whole passes of the weight ring: the ring depth for the
 // tile's row count when it divides K/128, else 2 (K is a multiple of 256).
-template <class S, bool GLU, int MACT>
+template <class S, bool GLU, int MACT, class Hook>
 __device__ __forceinline__ void gemm_tile_fp8_depth(const uint8_t* A, int lda, const float* asc, const uint8_t* B,
                                                     int n0, int up_rows, const float* wsc, int K, void* out, int ldo,
                                                     float* osc, int ldsc, char* lds, const int32_t* rowmap,
-                                                    int k, int a_rows) {
+                                                    int k, int a_rows, Hook hook) {
     constexpr int D = TileRegsF8<S, MACT>::DEPTH;
     if ((K / S::BK) % D == 0)
         gemm_tile_fp8<S, GLU, MACT, D>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap, k,
-                                       a_rows);
+                                       a_rows, hook);
     else
         gemm_tile_fp8<S, GLU, MACT, 2>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap, k,
-                                       a_rows);
+                                       a_rows, hook);
 }
 
-template <class S, bool GLU>
+template <class S, bool GLU, class Hook = NoHook>
 __device__ __forceinline__ void gemm_tile_fp8_rows(int rows32, const uint8_t* A, int lda, const float* asc,
                                                    const uint8_t* B, int n0, int up_rows, const float* wsc, int K,
                                                    void* out, int ldo, float* osc, int ldsc, char* lds,
-                                                   const int32_t* rowmap = nullptr, int k = 1, int a_rows = 0) {
+                                                   const int32_t* rowmap = nullptr, int k = 1, int a_rows = 0,
+                                                   Hook hook = Hook{}) {
     static_assert(S::MB == 2, "dispatch written for 64-row tiles");
     if (rows32 > 32)
         gemm_tile_fp8_depth<S, GLU, 2>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap, k,
-                                       a_rows);
+                                       a_rows, hook);
     else
         gemm_tile_fp8_depth<S, GLU, 1>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap, k,
-                                       a_rows);
+                                       a_rows, hook);
 }
 
 }  // namespace moeapk
