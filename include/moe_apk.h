@@ -219,7 +219,9 @@ typedef struct moe_sched_config {
     int32_t decode_quota_max_wg; /* Q_max; 0 = n_workgroups / 2                          */
     int32_t x_moe_expected;   /* x*_moe; <= 0 selects the fixed quota (ratio 1)         */
     int32_t round_multiple;   /* c; 0 = 8 (one workgroup per XCD)                       */
-    int32_t reserved0;
+    int32_t group_row_tiles;  /* most row tiles of one expert whose tiles run column
+                                 block by column block together, so one fetch of a
+                                 weight slice serves all of them; 0 = 8, max 64     */
     const uint32_t* abort_word;   /* NULL, or host/peer-writable: non-zero stops the
                                      kernel at the next tile boundary (MOE_ERR_ABORTED) */
     moe_trace_rec* trace;     /* NULL, or [trace_capacity] records                      */

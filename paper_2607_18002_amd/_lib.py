@@ -46,7 +46,7 @@ class OpDesc(C.Structure):
 class SchedConfig(C.Structure):
     _fields_ = [
         ("n_workgroups", _i32), ("decode_quota_wg", _i32), ("decode_quota_max_wg", _i32),
-        ("x_moe_expected", _i32), ("round_multiple", _i32), ("reserved0", _i32),
+        ("x_moe_expected", _i32), ("round_multiple", _i32), ("group_row_tiles", _i32),
         ("abort_word", _p), ("trace", _p), ("trace_capacity", _i64), ("op_stats", _p),
         ("spin_limit", _i64),
     ]

@@ -69,12 +69,12 @@ struct OpArg {
     float* hs;
     uint32_t* done_word;
     const int32_t* rmap;       // gathered GEMM-1 operand: row -> assignment (x row = assignment / top_k), else NULL
-    int32_t cls, phase, layer, E, H, I, capacity, mt, n1, n2, max_mtiles, table_off, g1_off, T, top_k, pad;
+    int32_t cls, phase, layer, E, H, I, capacity, mt, n1, n2, max_mtiles, table_off, g1_off, grp_off, T, top_k;
 };
 
 struct KArgs {
     OpArg op[MOE_MAX_OPS];
-    int32_t n_ops, q, q_max, x_star, c, pad;
+    int32_t n_ops, q, q_max, x_star, c, gmax;
     int64_t spin_limit;
     const uint32_t* abort_word;
     moe_trace_rec* trace;
@@ -108,11 +108,12 @@ struct Hdr {
 };
 
 // One tile queue per (op, XCD): the op's row tiles are cut into kXcds
-// contiguous, balanced ranges [m_lo, m_lo + n_mt); queue x holds the GEMM-1
-// tiles of its range, then its GEMM-2 tiles.  Workgroups claim from their own
-// XCD's queue, so the activation rows and h of a row tile stay in one L2;
-// a workgroup whose queue is empty steals from the others.  claim is an
-// atomic counter; size / m_lo / n_mt are written once at instantiation.
+// contiguous ranges [m_lo, m_lo + n_mt), balanced by row tiles and cut only
+// between groups (below); queue x holds the GEMM-1 tiles of its range, then
+// its GEMM-2 tiles.  Workgroups claim from their own XCD's queue, so the
+// activation rows and h of a row tile and the weight slices of a group stay
+// in one L2; a workgroup whose queue is empty steals from the others.  claim
+// is an atomic counter; size / m_lo / n_mt are written once at instantiation.
 constexpr int kXcds = 8;
 struct XQueue {
     int32_t claim, size, m_lo, n_mt;
@@ -120,10 +121,15 @@ struct XQueue {
 };
 static_assert(sizeof(XQueue) == 128, "one L2 line per queue");
 
-// Within a queue, tiles run in groups of kGroupM row tiles: for each column
-// block, the group's row tiles back to back, so a weight slice fetched into
-// L2 serves kGroupM tiles while it is hot.
-constexpr int kGroupM = 4;
+// Groups: an expert's row tiles are split into ceil(n / gmax) groups of
+// near-equal size (gmax = group_row_tiles), and a queue runs each group column
+// block by column block, the group's row tiles back to back, so one fetch of
+// a weight slice into the XCD's L2 serves every row tile of the group while
+// it is hot.  A group never holds two experts, so an expert's weights are
+// streamed once per group.  grp[p] = first row tile | size << 16 of the group
+// holding row tile p.
+constexpr int kDefaultGroup = 8;
+constexpr int kMaxGroup = 64;
 
 constexpr size_t kHdrBytes = 256;
 constexpr size_t kDynOff = kHdrBytes;
@@ -137,18 +143,24 @@ __device__ __forceinline__ OpStatic* static_of(char* ws) { return (OpStatic*)(ws
 __device__ __forceinline__ char* arr_of(char* ws) { return ws + kArraysOff; }
 __device__ __forceinline__ XQueue* xq_of(char* ws, int o, int x) { return (XQueue*)(ws + kXqOff) + o * kXcds + x; }
 
-// Tile t of a queue holding n_mt row tiles starting at m_lo -> (stage, row tile, column block).
-__device__ __forceinline__ void queue_tile(int t, int n_mt, int m_lo, int n1, int n2, int& stage, int& mtile, int& nb) {
+// Tile t of a queue holding n_mt row tiles starting at m_lo: its stage and
+// the row tile p whose group holds it (a group of s row tiles starting at f
+// owns the tile numbers [(f - m_lo) * nn, (f - m_lo + s) * nn) of its stage).
+__device__ __forceinline__ void queue_pos(int t, int n_mt, int m_lo, int n1, int n2, int& stage, int& u, int& nn, int& p) {
     const int n1x = n_mt * n1;
-    int u = t, nn = n1;
+    u = t;
+    nn = n1;
     stage = 1;
     if (t >= n1x) { stage = 2; u = t - n1x; nn = n2; }
-    const int group = u / (kGroupM * nn);
-    const int within = u - group * (kGroupM * nn);
-    const int rest = n_mt - group * kGroupM;
-    const int gsz = rest < kGroupM ? rest : kGroupM;
-    nb = within / gsz;
-    mtile = m_lo + group * kGroupM + (within - nb * gsz);
+    p = m_lo + u / nn;
+}
+// ... then, with that group's entry g: column block and row tile (nb < 0: the entry is not a valid group of p).
+__device__ __forceinline__ void group_tile(uint32_t g, int u, int nn, int m_lo, int n_mt, int p, int& mtile, int& nb) {
+    const int f = (int)(g & 0xFFFFu), sz = (int)(g >> 16);
+    if (sz < 1 || f < m_lo || p < f || p >= f + sz || f + sz > m_lo + n_mt) { nb = -1; mtile = -1; return; }
+    const int w = u - (f - m_lo) * nn;
+    nb = w / sz;
+    mtile = f + (w - nb * sz);
 }
 
 // A row-tile table entry packs everything a claim needs into one 64-bit word:
@@ -252,6 +264,7 @@ __device__ __forceinline__ void run_tile(const OpArg& op, int stage, int row0, i
 constexpr int kTabCache = 64;
 struct TabCache {
     uint64_t ent[MOE_MAX_OPS][kTabCache];
+    uint32_t grp[MOE_MAX_OPS][kTabCache];
     int32_t lo[MOE_MAX_OPS];
     int32_t cnt[MOE_MAX_OPS];
 };
@@ -475,13 +488,17 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
             finish_prev();
             const OpArg& op = a.op[o];
             const uint64_t* table = (const uint64_t*)(arr_of(a.ws) + op.table_off);
+            const uint32_t* grp = (const uint32_t*)(arr_of(a.ws) + op.grp_off);
             int m_lo, n_mt;
             if (src == myx) {
                 if (tab->lo[o] < 0) {                                 // first claim from this op's own queue
                     const XQueue* qs = xq_of(a.ws, o, myx);
                     m_lo = ld_relaxed_agent(&qs->m_lo);
                     n_mt = ld_relaxed_agent(&qs->n_mt);
-                    if (n_mt <= kTabCache && lane < n_mt) tab->ent[o][lane] = ld_relaxed_agent(table + m_lo + lane);
+                    if (n_mt <= kTabCache && lane < n_mt) {
+                        tab->ent[o][lane] = ld_relaxed_agent(table + m_lo + lane);
+                        tab->grp[o][lane] = ld_relaxed_agent(grp + m_lo + lane);
+                    }
                     if (lane == 0) { tab->lo[o] = m_lo; tab->cnt[o] = n_mt; }
                 } else {
                     m_lo = tab->lo[o];
@@ -493,12 +510,16 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
                 n_mt = ld_relaxed_agent(&qs->n_mt);
             }
             if (lane == 0) {
-                int stage, mtile, nb;
-                queue_tile(t, n_mt, m_lo, op.n1, op.n2, stage, mtile, nb);
+                int stage, u, nn, p, mtile, nb;
+                queue_pos(t, n_mt, m_lo, op.n1, op.n2, stage, u, nn, p);
                 const int lo = tab->lo[o];
                 const int cnt = tab->cnt[o];
-                const uint64_t ent = (lo >= 0 && cnt <= kTabCache && mtile >= lo && mtile < lo + cnt)
-                                         ? tab->ent[o][mtile - lo] : ld_relaxed_agent(table + mtile);
+                const bool cached = lo >= 0 && cnt <= kTabCache;   // entries of the own queue's row tiles
+                const uint32_t g = (cached && p >= lo && p < lo + cnt) ? tab->grp[o][p - lo]
+                                   : (p >= 0 && p < op.max_mtiles ? ld_relaxed_agent(grp + p) : 0u);
+                group_tile(g, u, nn, m_lo, n_mt, p, mtile, nb);
+                const uint64_t ent = (cached && mtile >= lo && mtile < lo + cnt) ? tab->ent[o][mtile - lo]
+                                     : (mtile >= 0 && mtile < op.max_mtiles ? ld_relaxed_agent(table + mtile) : 0ull);
                 const int rows = (int)((ent >> 24) & 0xFF);
                 const int e = (int)(ent & 0x3FF);
                 const int row0 = (int)(ent >> 32);
@@ -522,7 +543,7 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
                     __hip_atomic_compare_exchange_strong(&dyn[o].t_first, &zero, cmd->t_claim, __ATOMIC_RELAXED,
                                                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                 }
-                if (stage == 2) {                                     // GEMM-1 of this row tile must be committed
+                if (stage == 2 && cmd->kind == CMD_TILE) {            // GEMM-1 of this row tile must be committed
                     const int32_t* g1 = (const int32_t*)(arr_of(a.ws) + op.g1_off) + mtile;
                     int64_t spins = 0;
                     while (ld_relaxed_agent(g1) < op.n1) {
@@ -552,12 +573,14 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
     OpDyn* d = dyn_of(a.ws) + o;
     if (static_of(a.ws)[o].rel_word) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");  // system scope: peer-written inputs
     uint64_t* table = (uint64_t*)(arr_of(a.ws) + op.table_off);
+    uint32_t* grp = (uint32_t*)(arr_of(a.ws) + op.grp_off);
+    const int gmax = a.gmax;
     for (int e = threadIdx.x; e < op.E; e += 256) {
         const int c = op.counts[e];
         scan[e] = c > 0 ? (c + op.mt - 1) / op.mt : 0;
     }
     __syncthreads();
-    __shared__ int32_t s_total, s_bad;
+    __shared__ int32_t s_total, s_bad, s_cut[kXcds + 1];
     if (threadIdx.x == 0) {
         int run = 0;
         for (int e = 0; e < op.E; ++e) { const int v = scan[e]; scan[e] = run; run += v; }
@@ -571,12 +594,36 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
         const int pos = scan[e];
         const int off = op.offsets[e];
         if (pos + nt > op.max_mtiles || off < 0 || (long)off + (long)nt * op.mt > op.capacity) { s_bad = 1; continue; }
-        for (int mb = 0; mb < nt; ++mb) {
-            const int rows = (c - mb * op.mt) < op.mt ? (c - mb * op.mt) : op.mt;
-            table[pos + mb] = pack_entry(e, mb, rows, off + mb * op.mt);
+        const int ng = (nt + gmax - 1) / gmax;
+        for (int j = 0; j < ng; ++j) {                     // near-equal groups of this expert's row tiles
+            const int glo = (int)((long)nt * j / ng), ghi = (int)((long)nt * (j + 1) / ng);
+            for (int mb = glo; mb < ghi; ++mb) {
+                const int rows = (c - mb * op.mt) < op.mt ? (c - mb * op.mt) : op.mt;
+                table[pos + mb] = pack_entry(e, mb, rows, off + mb * op.mt);
+                grp[pos + mb] = (uint32_t)(pos + glo) | ((uint32_t)(ghi - glo) << 16);
+            }
         }
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");       // each wave's entries, before ACTIVE is published
+    // Queue cuts: cut x (1..kXcds-1) is the group boundary nearest to x/kXcds
+    // of the row tiles (ties: the lower one), so no group spans two queues;
+    // cuts are non-decreasing in x.
+    if (threadIdx.x >= 1 && threadIdx.x < kXcds) {
+        const int xm = s_total;
+        const int target = (int)((long)xm * threadIdx.x / kXcds);
+        int best = 0, bestd = 0x7fffffff;
+        for (int e = 0; e < op.E; ++e) {
+            const int pos = scan[e], nt = (e + 1 < op.E ? scan[e + 1] : xm) - pos;
+            if (nt <= 0 || target < pos || target > pos + nt) continue;
+            const int ng = (nt + gmax - 1) / gmax;
+            for (int j = 0; j <= ng; ++j) {
+                const int b = pos + (int)((long)nt * j / ng);
+                const int dd = b > target ? b - target : target - b;
+                if (dd < bestd) { bestd = dd; best = b; }
+            }
+        }
+        s_cut[threadIdx.x] = best;
+    }
     __syncthreads();
     if (threadIdx.x == 0) {
         Hdr* hdr = hdr_of(a.ws);
@@ -593,9 +640,9 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
             __hip_atomic_store(&hdr->quota, qd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         __hip_atomic_store(&d->x_moe, xm, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        for (int x = 0; x < kXcds; ++x) {                      // balanced contiguous row-tile ranges
+        for (int x = 0; x < kXcds; ++x) {                      // contiguous row-tile ranges, cut between groups
             XQueue* qx = xq_of(a.ws, o, x);
-            const int lo = (int)((long)xm * x / kXcds), hi = (int)((long)xm * (x + 1) / kXcds);
+            const int lo = x == 0 ? 0 : s_cut[x], hi = x + 1 == kXcds ? xm : s_cut[x + 1];
             __hip_atomic_store(&qx->m_lo, lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_store(&qx->n_mt, hi - lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_store(&qx->size, (hi - lo) * (op.n1 + op.n2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -679,14 +726,15 @@ int class_of(int phase, int dtype) {
     return phase == MOE_PREFILL ? CLS_P_BF16 : CLS_D_BF16;
 }
 
-// Per op: a row-tile table (8 bytes per row tile) and GEMM-1 counters (4 bytes
-// per row tile), each padded to 256 bytes so no L2 line is shared between ops.
+// Per op: a row-tile table (8 bytes per row tile), GEMM-1 counters and group
+// entries (4 bytes per row tile each), each padded to 256 bytes so no L2 line
+// is shared between ops.
 size_t op_array_bytes(int capacity, int mt, size_t* table_bytes) {
     const size_t mm = (size_t)((capacity + mt - 1) / mt) + 1;
     const size_t tb = (mm * 8 + 255) & ~(size_t)255;
     const size_t gb = (mm * 4 + 255) & ~(size_t)255;
     if (table_bytes) *table_bytes = tb;
-    return tb + gb;
+    return tb + 2 * gb;
 }
 
 size_t ws_bytes_for(const moe_op_desc* ops, int n_ops) {
@@ -808,6 +856,7 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
         const size_t ob = op_array_bytes(d.capacity, d.row_align, &tb);
         p.table_off = (int32_t)off;
         p.g1_off = (int32_t)(off + tb);
+        p.grp_off = (int32_t)(off + tb + (ob - tb) / 2);
         off += ob;
         ia.rel_words[o] = d.release_word;
         ia.rel_after[o] = d.release_after_ns < 0 ? -1 : d.release_after_ns * (int64_t)wc_khz / 1000000;
@@ -822,6 +871,9 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
     a.q_max = cfg->decode_quota_max_wg > 0 ? cfg->decode_quota_max_wg : n_wg / 2;
     a.x_star = cfg->x_moe_expected;
     a.c = cfg->round_multiple > 0 ? cfg->round_multiple : 8;
+    if (cfg->group_row_tiles < 0 || cfg->group_row_tiles > kMaxGroup)
+        return fail(MOE_ERR_INVALID_ARG, "group_row_tiles=%d outside [0,%d]", cfg->group_row_tiles, kMaxGroup);
+    a.gmax = cfg->group_row_tiles > 0 ? cfg->group_row_tiles : kDefaultGroup;
     a.spin_limit = cfg->spin_limit > 0 ? cfg->spin_limit : (int64_t)2000000;
     a.abort_word = cfg->abort_word;
     a.trace = cfg->trace;

@@ -112,7 +112,7 @@ class MoEPipeline:
     def __init__(self, specs: List[OpSpec], n_workgroups: int = 0, decode_quota_wg: int = 64,
                  decode_quota_max_wg: int = 0, x_moe_expected: int = 0, round_multiple: int = 8,
                  trace_capacity: int = 0, spin_limit: int = 0, abort_word: Optional[torch.Tensor] = None,
-                 y_dtype: torch.dtype = torch.bfloat16, fused_gather: bool = False):
+                 y_dtype: torch.dtype = torch.bfloat16, fused_gather: bool = False, group_row_tiles: int = 0):
         """fused_gather: GEMM-1 reads its rows straight from x through row_to_assign
         (permute then only builds the maps), instead of from a permuted copy x_perm."""
         if not specs:
@@ -157,7 +157,7 @@ class MoEPipeline:
         self.abort_word = abort_word
         self.cfg = SchedConfig(n_workgroups=n_workgroups, decode_quota_wg=decode_quota_wg,
                                decode_quota_max_wg=decode_quota_max_wg, x_moe_expected=x_moe_expected,
-                               round_multiple=round_multiple,
+                               round_multiple=round_multiple, group_row_tiles=group_row_tiles,
                                abort_word=abort_word.data_ptr() if abort_word is not None else None,
                                trace=self.trace.data_ptr() if trace_capacity > 0 else None,
                                trace_capacity=trace_capacity, op_stats=self.stats.data_ptr(),
