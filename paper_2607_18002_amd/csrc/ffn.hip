@@ -37,18 +37,18 @@
 #include <cstring>
 
 #include "tile_bf16.hpp"
+#include "tile_bf16_tall.hpp"
 #include "tile_fp8.hpp"
 
 namespace {
 
 using namespace moeapk;
 
-using ShapeP = TileShape<128, 256, 64>;    // bf16 prefill: 128 x 256 tile, K step 64
+using ShapeP = TileShape<192, 256, 64>;    // bf16 prefill: 192 x 256 tall tile, K step 64
 using ShapeD = TileShape<128, 256, 64>;    // bf16 decode : 128 x 256 tile, K step 64
 using ShapeF8 = TileShapeF8<64, 256>;      // fp8 (both phases): 64 x 256 tile, K step 128 (one scale block)
 constexpr int kMax2(int a, int b) { return a > b ? a : b; }
-constexpr int kLdsBytes = kMax2(kMax2(ShapeP::LDS, ShapeD::LDS), ShapeF8::LDS);
-constexpr int kRowAlign = 128;             // M_t of both bf16 classes
+constexpr int kLdsBytes = kMax2(kMax2(TallLds<ShapeP>::bytes, ShapeD::LDS), ShapeF8::LDS);
 constexpr int kMaxRowTiles = 1 << 14;      // per op (14-bit field of a table entry)
 
 enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1, CLS_FP8 = 2 };
@@ -202,20 +202,34 @@ __global__ __launch_bounds__(256) void apk_init_kernel(const InitArgs a) {
 }
 
 // ----------------------------------------------------------------------------- tiles
-template <class S, class Hook>
+// bf16 tiles: TALL selects the 192-row prefill tile (tile_bf16_tall.hpp),
+// else the 128-row tile (tile_bf16.hpp); both take the same operands.
+template <class S, bool TALL, class Hook>
 __device__ __forceinline__ void run_tile_cls(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds,
                                              Hook hook) {
     const long H = op.H, I = op.I;
     if (stage == 1) {
         const bool g = op.rmap != nullptr;
-        gemm_tile_bf16_rows<S, true, true>(rows32, g ? op.x : op.x + row0 * H, (int)H,
-                                     op.wgu + (long)e * 2 * I * H + (long)nb * (S::BN / 2) * H, (int)H, (int)I,
-                                     (int)H, op.h + row0 * I + nb * (S::BN / 2), (int)I, lds,
-                                     g ? op.rmap + row0 : nullptr, op.top_k, op.T, hook);
+        const uint16_t* A = g ? op.x : op.x + row0 * H;
+        const uint16_t* B = op.wgu + (long)e * 2 * I * H + (long)nb * (S::BN / 2) * H;
+        uint16_t* out = op.h + row0 * I + nb * (S::BN / 2);
+        const int32_t* rmap = g ? op.rmap + row0 : nullptr;
+        if constexpr (TALL)
+            gemm_tile_tall_rows<S, true>(rows32, A, (int)H, B, (int)H, (int)I, (int)H, out, (int)I, lds, rmap,
+                                         op.top_k, op.T, hook);
+        else
+            gemm_tile_bf16_rows<S, true, true>(rows32, A, (int)H, B, (int)H, (int)I, (int)H, out, (int)I, lds, rmap,
+                                               op.top_k, op.T, hook);
     } else {
-        gemm_tile_bf16_rows<S, false, true>(rows32, op.h + row0 * I, (int)I, op.wd + (long)e * H * I + (long)nb * S::BN * I,
-                                      (int)I, 0, (int)I, op.y + row0 * H + nb * S::BN, (int)H, lds, nullptr, 1, 0,
-                                      hook);
+        const uint16_t* A = op.h + row0 * I;
+        const uint16_t* B = op.wd + (long)e * H * I + (long)nb * S::BN * I;
+        uint16_t* out = op.y + row0 * H + nb * S::BN;
+        if constexpr (TALL)
+            gemm_tile_tall_rows<S, false>(rows32, A, (int)I, B, (int)I, 0, (int)I, out, (int)H, lds, nullptr, 1, 0,
+                                          hook);
+        else
+            gemm_tile_bf16_rows<S, false, true>(rows32, A, (int)I, B, (int)I, 0, (int)I, out, (int)H, lds, nullptr, 1,
+                                                0, hook);
     }
 }
 
@@ -247,12 +261,12 @@ __device__ __forceinline__ void run_tile_fp8(const OpArg& op, int stage, int row
 template <class Hook>
 __device__ __forceinline__ void run_tile(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds,
                                          Hook hook) {
-    // Both bf16 classes currently share one tile shape.
-    static_assert(ShapeP::BM == ShapeD::BM && ShapeP::BN == ShapeD::BN && ShapeP::BK == ShapeD::BK, "one shape");
     if (op.cls == CLS_FP8)
         run_tile_fp8(op, stage, row0, rows32, nb, e, lds, hook);
+    else if (op.cls == CLS_P_BF16)
+        run_tile_cls<ShapeP, true>(op, stage, row0, rows32, nb, e, lds, hook);
     else
-        run_tile_cls<ShapeP>(op, stage, row0, rows32, nb, e, lds, hook);
+        run_tile_cls<ShapeD, false>(op, stage, row0, rows32, nb, e, lds, hook);
 }
 
 // ----------------------------------------------------------------------------- scheduler
@@ -719,7 +733,7 @@ struct ClassInfo {
 };
 ClassInfo class_info(int cls) {
     if (cls == CLS_FP8) return ClassInfo{ShapeF8::BM, ShapeF8::BN, ShapeF8::BK};
-    return cls == CLS_P_BF16 ? ClassInfo{kRowAlign, ShapeP::BN, ShapeP::BK} : ClassInfo{kRowAlign, ShapeD::BN, ShapeD::BK};
+    return cls == CLS_P_BF16 ? ClassInfo{ShapeP::BM, ShapeP::BN, ShapeP::BK} : ClassInfo{ShapeD::BM, ShapeD::BN, ShapeD::BK};
 }
 int class_of(int phase, int dtype) {
     if (dtype == MOE_FP8_E4M3) return CLS_FP8;

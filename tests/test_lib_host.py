@@ -79,7 +79,7 @@ def test_decode_quota_matches_oracle():
 
 def test_row_align_and_workspace_queries():
     from paper_2607_18002_amd import _lib, ops
-    assert ops.moe_ffn_row_align(_lib.MOE_PREFILL, _lib.MOE_BF16) == 128
+    assert ops.moe_ffn_row_align(_lib.MOE_PREFILL, _lib.MOE_BF16) == 192   # tall prefill tile
     assert ops.moe_ffn_row_align(_lib.MOE_DECODE, _lib.MOE_BF16) == 128
     assert ops.moe_ffn_row_align(_lib.MOE_PREFILL, _lib.MOE_FP8_E4M3) == 64
     assert ops.moe_ffn_row_align(_lib.MOE_DECODE, _lib.MOE_FP8_E4M3) == 64
