@@ -75,6 +75,8 @@ struct OpArg {
 struct KArgs {
     OpArg op[MOE_MAX_OPS];
     int32_t n_ops, q, q_max, x_star, c, gmax;
+    int32_t pre_wg;            // prefill tiles are claimed ahead only by workgroups >= pre_wg
+    int32_t pre_dec_all;       // no prefill op in the launch: every workgroup claims decode tiles ahead
     int64_t spin_limit;
     const uint32_t* abort_word;
     moe_trace_rec* trace;
@@ -285,7 +287,8 @@ struct TabCache {
 
 // Command block written by wave 0 and read by the whole workgroup.
 struct Cmd {
-    int32_t kind, op, stage, e, row0, rows32, nb, mtile, mblk, rows, t, pad;
+    int32_t kind, op, stage, e, row0, rows32, nb, mtile, mblk, rows, t;
+    int32_t pre_next;          // op whose next tile wave 0 claims ahead during this tile, or -1
     unsigned long long t_boundary, t_polled, t_claim, t_start;
 };
 
@@ -348,12 +351,109 @@ __device__ __forceinline__ Polls issue_polls(const KArgs& a) {
     return p;
 }
 
+// Wave 0: turn claim t of op o's queue on XCD src into the command block
+// (table lookup, validation of the descriptor, GEMM-1 dependency of a GEMM-2
+// tile).  The own queue's range and entries are cached in LDS at the first
+// claim from it.  Returns, to lane 0, whether the claimed tile was not the own
+// queue's last (a next claim from it may succeed).
+__device__ bool take_tile(const KArgs& a, int o, int src, int t, int myx, TabCache* tab, Cmd* cmd,
+                  unsigned long long t_boundary, unsigned long long now) {
+    const int lane = threadIdx.x;
+    Hdr* hdr = hdr_of(a.ws);
+    OpDyn* dyn = dyn_of(a.ws);
+    bool more = false;
+    const OpArg& op = a.op[o];
+    const uint64_t* table = (const uint64_t*)(arr_of(a.ws) + op.table_off);
+    const uint32_t* grp = (const uint32_t*)(arr_of(a.ws) + op.grp_off);
+    int m_lo, n_mt;
+    if (src == myx) {
+        if (tab->lo[o] < 0) {                                 // first claim from this op's own queue
+            const XQueue* qs = xq_of(a.ws, o, myx);
+            m_lo = ld_relaxed_agent(&qs->m_lo);
+            n_mt = ld_relaxed_agent(&qs->n_mt);
+            if (n_mt <= kTabCache && lane < n_mt) {
+                tab->ent[o][lane] = ld_relaxed_agent(table + m_lo + lane);
+                tab->grp[o][lane] = ld_relaxed_agent(grp + m_lo + lane);
+            }
+            if (lane == 0) { tab->lo[o] = m_lo; tab->cnt[o] = n_mt; }
+        } else {
+            m_lo = tab->lo[o];
+            n_mt = tab->cnt[o];
+        }
+    } else {
+        const XQueue* qs = xq_of(a.ws, o, src);
+        m_lo = ld_relaxed_agent(&qs->m_lo);
+        n_mt = ld_relaxed_agent(&qs->n_mt);
+    }
+    if (lane == 0) {
+        int stage, u, nn, p, mtile, nb;
+        queue_pos(t, n_mt, m_lo, op.n1, op.n2, stage, u, nn, p);
+        const int lo = tab->lo[o];
+        const int cnt = tab->cnt[o];
+        const bool cached = lo >= 0 && cnt <= kTabCache;   // entries of the own queue's row tiles
+        const uint32_t g = (cached && p >= lo && p < lo + cnt) ? tab->grp[o][p - lo]
+                           : (p >= 0 && p < op.max_mtiles ? ld_relaxed_agent(grp + p) : 0u);
+        group_tile(g, u, nn, m_lo, n_mt, p, mtile, nb);
+        const uint64_t ent = (cached && mtile >= lo && mtile < lo + cnt) ? tab->ent[o][mtile - lo]
+                             : (mtile >= 0 && mtile < op.max_mtiles ? ld_relaxed_agent(table + mtile) : 0ull);
+        const int rows = (int)((ent >> 24) & 0xFF);
+        const int e = (int)(ent & 0x3FF);
+        const int row0 = (int)(ent >> 32);
+        cmd->kind = CMD_TILE; cmd->op = o; cmd->stage = stage;
+        cmd->e = e; cmd->mblk = (int)((ent >> 10) & 0x3FFF);
+        cmd->row0 = row0; cmd->rows = rows; cmd->rows32 = (rows + 31) & ~31;
+        // The tile descriptor must address memory inside the op's buffers;
+        // if a scheduler invariant broke, stop instead of running the tile.
+        if (mtile < 0 || mtile >= op.max_mtiles || e >= op.E || rows < 1 || rows > op.mt || row0 < 0 ||
+            (long)row0 + op.mt > (long)op.capacity || nb < 0 || nb >= (stage == 1 ? op.n1 : op.n2)) {
+            set_status(a.status, MOE_ERR_INTERNAL);
+            st_release_agent(&hdr->stop, 1);
+            cmd->kind = CMD_EXIT;
+        }
+        cmd->nb = nb; cmd->mtile = mtile; cmd->t = t;
+        cmd->t_boundary = t_boundary;
+        cmd->t_polled = now;
+        cmd->t_claim = wall_ticks();
+        if (t == 0) {
+            unsigned long long zero = 0;
+            __hip_atomic_compare_exchange_strong(&dyn[o].t_first, &zero, cmd->t_claim, __ATOMIC_RELAXED,
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        if (stage == 2 && cmd->kind == CMD_TILE) {            // GEMM-1 of this row tile must be committed
+            const int32_t* g1 = (const int32_t*)(arr_of(a.ws) + op.g1_off) + mtile;
+            int64_t spins = 0;
+            while (ld_relaxed_agent(g1) < op.n1) {
+                if (++spins > a.spin_limit || ld_relaxed_agent(&hdr->stop)) {
+                    set_status(a.status, MOE_ERR_TIMEOUT);
+                    st_release_agent(&hdr->stop, 1);
+                    cmd->kind = CMD_EXIT;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+        }
+        cmd->t_start = wall_ticks();
+        more = src == myx && t + 1 < n_mt * (op.n1 + op.n2);
+    }
+    return more;
+}
+
+// Whether a workgroup may claim its next tile of an op of this phase ahead,
+// during the current tile: only in its preferred phase (decode below q', or
+// any workgroup when the launch holds no prefill op), and for prefill only if
+// it can never be asked to prefer decode (index >= every possible q'), so a
+// claim made ahead never delays a decode tile or holds one beyond the quota.
+__device__ __forceinline__ bool pre_allowed(const KArgs& a, int wg, int q, int phase) {
+    return phase == MOE_DECODE ? (wg < q || a.pre_dec_all) : wg >= a.pre_wg;
+}
+__device__ __forceinline__ int phase_of(const KArgs& a, int o) { return a.op[o].phase; }
+
 // Wave 0 at a tile boundary: commit the previous tile (if any), decide with
 // the polled words (pre, issued after the previous tile's K loop, when
 // have_pre; else read now), claim, and only then wait for the commit's
 // completion count, so the commit and the claim share one round trip.
 __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool have_prev, int64_t& idle,
-                         TabCache* tab, bool have_pre, Polls pre) {
+                         TabCache* tab, bool have_pre, Polls pre, int pre_t) {
     const int lane = threadIdx.x;
     Hdr* hdr = hdr_of(a.ws);
     OpDyn* dyn = dyn_of(a.ws);
@@ -363,6 +463,7 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
     // registers across the tile.
     Cmd prev;
     if (have_prev) prev = *cmd;
+    if (lane == 0) cmd->pre_next = -1;
     const unsigned long long t_boundary = wall_ticks();
     const Polls pl = have_pre ? pre : issue_polls(a);
 
@@ -429,6 +530,20 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
         return;
     }
     const uint64_t now = wall_ticks();
+
+    // 3b. a claim made ahead during the previous tile (the hook claimed in this
+    //     XCD's queue of op prev.pre_next): take it if it landed inside the queue
+    const int pre_op_u = have_prev ? prev.pre_next : -1;
+    if (pre_op_u >= 0) {
+        const int pt = __shfl(pre_t, 0, 64);
+        if (pt < __shfl(own_size, pre_op_u, 64)) {
+            finish_prev();
+            const bool more = take_tile(a, pre_op_u, myx, pt, myx, tab, cmd, t_boundary, now);
+            if (lane == 0) cmd->pre_next = more && pre_allowed(a, wg, q, phase_of(a, pre_op_u)) ? pre_op_u : -1;
+            idle = 0;
+            return;
+        }
+    }
 
     // 4. ready signals of waiting operation templates -> instantiate one of them
     bool ready = false;
@@ -500,78 +615,8 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
             }
             if (src < 0) continue;
             finish_prev();
-            const OpArg& op = a.op[o];
-            const uint64_t* table = (const uint64_t*)(arr_of(a.ws) + op.table_off);
-            const uint32_t* grp = (const uint32_t*)(arr_of(a.ws) + op.grp_off);
-            int m_lo, n_mt;
-            if (src == myx) {
-                if (tab->lo[o] < 0) {                                 // first claim from this op's own queue
-                    const XQueue* qs = xq_of(a.ws, o, myx);
-                    m_lo = ld_relaxed_agent(&qs->m_lo);
-                    n_mt = ld_relaxed_agent(&qs->n_mt);
-                    if (n_mt <= kTabCache && lane < n_mt) {
-                        tab->ent[o][lane] = ld_relaxed_agent(table + m_lo + lane);
-                        tab->grp[o][lane] = ld_relaxed_agent(grp + m_lo + lane);
-                    }
-                    if (lane == 0) { tab->lo[o] = m_lo; tab->cnt[o] = n_mt; }
-                } else {
-                    m_lo = tab->lo[o];
-                    n_mt = tab->cnt[o];
-                }
-            } else {
-                const XQueue* qs = xq_of(a.ws, o, src);
-                m_lo = ld_relaxed_agent(&qs->m_lo);
-                n_mt = ld_relaxed_agent(&qs->n_mt);
-            }
-            if (lane == 0) {
-                int stage, u, nn, p, mtile, nb;
-                queue_pos(t, n_mt, m_lo, op.n1, op.n2, stage, u, nn, p);
-                const int lo = tab->lo[o];
-                const int cnt = tab->cnt[o];
-                const bool cached = lo >= 0 && cnt <= kTabCache;   // entries of the own queue's row tiles
-                const uint32_t g = (cached && p >= lo && p < lo + cnt) ? tab->grp[o][p - lo]
-                                   : (p >= 0 && p < op.max_mtiles ? ld_relaxed_agent(grp + p) : 0u);
-                group_tile(g, u, nn, m_lo, n_mt, p, mtile, nb);
-                const uint64_t ent = (cached && mtile >= lo && mtile < lo + cnt) ? tab->ent[o][mtile - lo]
-                                     : (mtile >= 0 && mtile < op.max_mtiles ? ld_relaxed_agent(table + mtile) : 0ull);
-                const int rows = (int)((ent >> 24) & 0xFF);
-                const int e = (int)(ent & 0x3FF);
-                const int row0 = (int)(ent >> 32);
-                cmd->kind = CMD_TILE; cmd->op = o; cmd->stage = stage;
-                cmd->e = e; cmd->mblk = (int)((ent >> 10) & 0x3FFF);
-                cmd->row0 = row0; cmd->rows = rows; cmd->rows32 = (rows + 31) & ~31;
-                // The tile descriptor must address memory inside the op's buffers;
-                // if a scheduler invariant broke, stop instead of running the tile.
-                if (mtile < 0 || mtile >= op.max_mtiles || e >= op.E || rows < 1 || rows > op.mt || row0 < 0 ||
-                    (long)row0 + op.mt > (long)op.capacity || nb < 0 || nb >= (stage == 1 ? op.n1 : op.n2)) {
-                    set_status(a.status, MOE_ERR_INTERNAL);
-                    st_release_agent(&hdr->stop, 1);
-                    cmd->kind = CMD_EXIT;
-                }
-                cmd->nb = nb; cmd->mtile = mtile; cmd->t = t;
-                cmd->t_boundary = t_boundary;
-                cmd->t_polled = now;
-                cmd->t_claim = wall_ticks();
-                if (t == 0) {
-                    unsigned long long zero = 0;
-                    __hip_atomic_compare_exchange_strong(&dyn[o].t_first, &zero, cmd->t_claim, __ATOMIC_RELAXED,
-                                                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                }
-                if (stage == 2 && cmd->kind == CMD_TILE) {            // GEMM-1 of this row tile must be committed
-                    const int32_t* g1 = (const int32_t*)(arr_of(a.ws) + op.g1_off) + mtile;
-                    int64_t spins = 0;
-                    while (ld_relaxed_agent(g1) < op.n1) {
-                        if (++spins > a.spin_limit || ld_relaxed_agent(&hdr->stop)) {
-                            set_status(a.status, MOE_ERR_TIMEOUT);
-                            st_release_agent(&hdr->stop, 1);
-                            cmd->kind = CMD_EXIT;
-                            break;
-                        }
-                        __builtin_amdgcn_s_sleep(1);
-                    }
-                }
-                cmd->t_start = wall_ticks();
-            }
+            const bool more = take_tile(a, o, src, t, myx, tab, cmd, t_boundary, now);
+            if (lane == 0) cmd->pre_next = more && pre_allowed(a, wg, q, phase_of(a, o)) ? o : -1;
             idle = 0;
             return;
         }
@@ -692,8 +737,9 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
     int64_t idle = 0;
     bool have_prev = false;
     Polls polls = {};                                         // wave 0: issued after the last tile's K loop
+    int pre_t = 0;                                            // lane 0: a claim issued ahead, during the tile
     for (;;) {
-        if (tid < 64) boundary(a, t0, wg, &cmd, have_prev, idle, &tab, have_prev, polls);
+        if (tid < 64) boundary(a, t0, wg, &cmd, have_prev, idle, &tab, have_prev, polls, pre_t);
         __syncthreads();
         const int kind = cmd.kind;
         have_prev = false;
@@ -718,7 +764,17 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
         const int e = __builtin_amdgcn_readfirstlane(cmd.e);
         __syncthreads();                                      // every thread has read cmd
         run_tile(a.op[o], stage, row0, rows32, nb, e, lds, [&]() {
-            if (tid < 64) polls = issue_polls(a);
+            // (both results are assigned on every path, so neither stays live across the K loop)
+            Polls p = {};
+            int t_ahead = 0;
+            if (tid < 64) {
+                p = issue_polls(a);
+                // claim the next tile of the same op ahead; its round trip overlaps the epilogue
+                const int pn = cmd.pre_next;                  // written by this wave at the boundary
+                if (tid == 0 && pn >= 0) t_ahead = atomicAdd(&xq_of(a.ws, pn, xcc_id())->claim, 1);
+            }
+            polls = p;
+            pre_t = t_ahead;
         });
         // Wave 0's release at the commit writes back this XCD's L2; the barrier does
         // not wait for global stores, so each wave first lets its own reach the L2.
@@ -888,6 +944,15 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
     if (cfg->group_row_tiles < 0 || cfg->group_row_tiles > kMaxGroup)
         return fail(MOE_ERR_INVALID_ARG, "group_row_tiles=%d outside [0,%d]", cfg->group_row_tiles, kMaxGroup);
     a.gmax = cfg->group_row_tiles > 0 ? cfg->group_row_tiles : kDefaultGroup;
+    // prefill tiles may be claimed ahead only by workgroups that no decode
+    // quota can reach: q' <= Q_max, and with a fixed quota q' is known
+    bool any_decode = false, any_prefill = false;
+    for (int o = 0; o < n_ops; ++o) {
+        any_decode |= ops[o].phase == MOE_DECODE;
+        any_prefill |= ops[o].phase == MOE_PREFILL;
+    }
+    a.pre_dec_all = any_prefill ? 0 : 1;
+    a.pre_wg = !any_decode ? 0 : (a.x_star <= 0 ? moeapk::decode_quota(a.q, 0, 0, a.q_max, a.c) : a.q_max);
     a.spin_limit = cfg->spin_limit > 0 ? cfg->spin_limit : (int64_t)2000000;
     a.abort_word = cfg->abort_word;
     a.trace = cfg->trace;

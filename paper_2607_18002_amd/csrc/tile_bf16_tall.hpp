@@ -13,8 +13,8 @@
 // (256 rows would fill all 256 AGPRs with accumulators; the register
 // allocator then spills the operand registers, so 192 is the tallest tile.)
 //  * B (weights, packed operand order) streams global -> registers through a
-//    ring of D K steps (ring depth 2..6 measured alike: the stream is not
-//    latency-bound);
+//    ring of D = 2 K steps (full tiles ran alike with D = 2..6; deeper rings
+//    for short tiles made the mixed workload slower);
 //  * A (activation rows, shared by the 4 waves) is loaded into registers one
 //    K step ahead and staged through double-buffered LDS (rows padded by 16
 //    bytes: the fragment reads are free of bank conflicts);
