@@ -103,8 +103,8 @@ moe_status_t moe_topk_route(const float* logits, int32_t T, int32_t E_global, in
  *                 [-1, E_local) set MOE_ERR_BAD_EXPERT and are treated as -1
  *  x              [T, H] activations: bf16, or fp8 codes with
  *  x_scales       [T, H/128] f32 per-row group scales (fp8 only, else NULL)
- *  row_align      M_t of the FFN op that consumes the layout
- *                 (moe_ffn_row_align()); 1 <= row_align <= 1024
+ *  row_align      segment alignment the FFN op that consumes the layout
+ *                 needs (moe_ffn_row_align()); 1 <= row_align <= 1024
  *  capacity       rows of row_to_assign / x_perm; must be at least
  *                 T*min(top_k, E_local) + E_local*(row_align-1)
  *  counts         [E_local] i32 out     offsets [E_local+1] i32 out
@@ -201,7 +201,7 @@ typedef struct moe_op_stats {
     uint64_t t_ready;         /* instantiation (release observed)                       */
     uint64_t t_first;         /* first tile started                                     */
     uint64_t t_done;          /* last tile committed                                    */
-    int32_t x_moe;            /* Eq. (3) footprint at the op's row_align                */
+    int32_t x_moe;            /* Eq. (3) footprint: row tiles at the class's tile height */
     int32_t n_tiles;          /* GEMM-1 + GEMM-2 tiles                                  */
     int32_t quota;            /* decode ops: q' of Eq. (4) in workgroups; prefill: 0    */
     int32_t reserved;
@@ -230,12 +230,15 @@ typedef struct moe_sched_config {
     int64_t spin_limit;       /* bounded waits, in polls; 0 = default (about 2 s)       */
 } moe_sched_config;
 
-/* Tile height M_t the FFN uses for ops of this phase and dtype; moe_permute's
- * row_align for such an op must equal it.  Returns <= 0 if unsupported. */
+/* Segment alignment the FFN needs for ops of this phase and dtype (32 rows,
+ * one MFMA row block); moe_permute's row_align for such an op must equal it.
+ * The FFN cuts an expert's m rows into ceil(m / M_t) row tiles of near-equal
+ * height in whole 32-row blocks, M_t = moe_ffn_tile_shape's bm.  Returns
+ * <= 0 if unsupported. */
 int32_t moe_ffn_row_align(moe_phase_t phase, moe_dtype_t dtype);
 
-/* Output tile of the FFN kernel for ops of this phase and dtype: *bm rows
- * (== moe_ffn_row_align), *bn columns (GEMM-1: bn/2 gate + bn/2 up columns,
+/* Output tile of the FFN kernel for ops of this phase and dtype: at most *bm
+ * rows (Eq. 3's M_t), *bn columns (GEMM-1: bn/2 gate + bn/2 up columns,
  * i.e. bn/2 columns of h; GEMM-2: bn columns of y_perm), *bk the K step.
  * An op with footprint x_moe (Eq. 3) runs x_moe*(I/(bn/2)) GEMM-1 tiles and
  * x_moe*(H/bn) GEMM-2 tiles.  Returns MOE_OK or MOE_ERR_UNSUPPORTED. */

@@ -50,6 +50,11 @@ using ShapeF8 = TileShapeF8<64, 256>;      // fp8 (both phases): 64 x 256 tile, 
 constexpr int kMax2(int a, int b) { return a > b ? a : b; }
 constexpr int kLdsBytes = kMax2(kMax2(TallLds<ShapeP>::bytes, ShapeD::LDS), ShapeF8::LDS);
 constexpr int kMaxRowTiles = 1 << 14;      // per op (14-bit field of a table entry)
+// Expert segments are aligned to 32 rows (one MFMA row block).  An expert's m
+// rows are cut into ceil(m / M_t) row tiles of near-equal height in whole
+// 32-row blocks (M_t = the class's tallest tile), so the row tiles that share
+// a weight slice run about equally long and stay in step.
+constexpr int kSegAlign = 32;
 
 enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1, CLS_FP8 = 2 };
 enum : int32_t { ST_WAIT = 0, ST_INIT = 1, ST_ACTIVE = 2, ST_DONE = 3 };
@@ -405,7 +410,7 @@ __device__ bool take_tile(const KArgs& a, int o, int src, int t, int myx, TabCac
         // The tile descriptor must address memory inside the op's buffers;
         // if a scheduler invariant broke, stop instead of running the tile.
         if (mtile < 0 || mtile >= op.max_mtiles || e >= op.E || rows < 1 || rows > op.mt || row0 < 0 ||
-            (long)row0 + op.mt > (long)op.capacity || nb < 0 || nb >= (stage == 1 ? op.n1 : op.n2)) {
+            (long)row0 + ((rows + 31) & ~31) > (long)op.capacity || nb < 0 || nb >= (stage == 1 ? op.n1 : op.n2)) {
             set_status(a.status, MOE_ERR_INTERNAL);
             st_release_agent(&hdr->stop, 1);
             cmd->kind = CMD_EXIT;
@@ -649,16 +654,19 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
     __syncthreads();
     for (int e = threadIdx.x; e < op.E; e += 256) {
         const int c = op.counts[e];
-        const int nt = c > 0 ? (c + op.mt - 1) / op.mt : 0;
+        const int nt = c > 0 ? (c + op.mt - 1) / op.mt : 0;      // Eq. (3): ceil(m_e / M_t) row tiles
+        const int nb32 = (c + kSegAlign - 1) / kSegAlign;        // 32-row blocks of the segment
         const int pos = scan[e];
         const int off = op.offsets[e];
-        if (pos + nt > op.max_mtiles || off < 0 || (long)off + (long)nt * op.mt > op.capacity) { s_bad = 1; continue; }
+        if (pos + nt > op.max_mtiles || off < 0 || (long)off + (long)nb32 * kSegAlign > op.capacity) { s_bad = 1; continue; }
         const int ng = (nt + gmax - 1) / gmax;
         for (int j = 0; j < ng; ++j) {                     // near-equal groups of this expert's row tiles
             const int glo = (int)((long)nt * j / ng), ghi = (int)((long)nt * (j + 1) / ng);
             for (int mb = glo; mb < ghi; ++mb) {
-                const int rows = (c - mb * op.mt) < op.mt ? (c - mb * op.mt) : op.mt;
-                table[pos + mb] = pack_entry(e, mb, rows, off + mb * op.mt);
+                // near-equal heights in whole 32-row blocks: tile mb holds blocks [b0, b1)
+                const int b0 = (int)((long)nb32 * mb / nt), b1 = (int)((long)nb32 * (mb + 1) / nt);
+                const int rows = (c < b1 * kSegAlign ? c : b1 * kSegAlign) - b0 * kSegAlign;
+                table[pos + mb] = pack_entry(e, mb, rows, off + b0 * kSegAlign);
                 grp[pos + mb] = (uint32_t)(pos + glo) | ((uint32_t)(ghi - glo) << 16);
             }
         }
@@ -785,7 +793,7 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
 }
 
 struct ClassInfo {
-    int bm, bn, bk;
+    int bm, bn, bk;            // tallest row tile (Eq. 3's M_t), output columns, K step
 };
 ClassInfo class_info(int cls) {
     if (cls == CLS_FP8) return ClassInfo{ShapeF8::BM, ShapeF8::BN, ShapeF8::BK};
@@ -809,7 +817,7 @@ size_t op_array_bytes(int capacity, int mt, size_t* table_bytes) {
 
 size_t ws_bytes_for(const moe_op_desc* ops, int n_ops) {
     size_t bytes = kArraysOff;
-    for (int o = 0; o < n_ops; ++o) bytes += op_array_bytes(ops[o].capacity, ops[o].row_align > 0 ? ops[o].row_align : 1, nullptr);
+    for (int o = 0; o < n_ops; ++o) bytes += op_array_bytes(ops[o].capacity, kSegAlign, nullptr);
     return (bytes + 255) & ~(size_t)255;
 }
 
@@ -818,7 +826,8 @@ size_t ws_bytes_for(const moe_op_desc* ops, int n_ops) {
 extern "C" int32_t moe_ffn_row_align(moe_phase_t phase, moe_dtype_t dtype) {
     if (phase != MOE_PREFILL && phase != MOE_DECODE) return -1;
     if (dtype != MOE_BF16 && dtype != MOE_FP8_E4M3) return -2;
-    return class_info(class_of(phase, dtype)).bm;
+    (void)class_info(class_of(phase, dtype));
+    return kSegAlign;
 }
 
 extern "C" moe_status_t moe_ffn_tile_shape(moe_phase_t phase, moe_dtype_t dtype, int32_t* bm, int32_t* bn,
@@ -874,9 +883,10 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
             if (!(d.x ? d.x_scales : d.x_perm_scales) || !d.w_gate_up_scales || !d.w_down_scales || !d.h_scales)
                 return fail(MOE_ERR_INVALID_ARG, "op %d: fp8 op without its scale buffers", o);
         }
-        if (d.row_align != ci.bm)
-            return fail(MOE_ERR_INVALID_ARG, "op %d: row_align=%d but the FFN tile height is %d", o, d.row_align, ci.bm);
-        if (d.capacity < d.row_align) return fail(MOE_ERR_CAPACITY, "op %d: capacity=%d below one tile", o, d.capacity);
+        if (d.row_align != kSegAlign)
+            return fail(MOE_ERR_INVALID_ARG, "op %d: row_align=%d but the FFN needs segments aligned to %d rows", o,
+                        d.row_align, kSegAlign);
+        if (d.capacity < d.row_align) return fail(MOE_ERR_CAPACITY, "op %d: capacity=%d below one block", o, d.capacity);
         if ((int64_t)d.capacity * d.H > INT32_MAX || (int64_t)d.capacity * d.I > INT32_MAX)
             return fail(MOE_ERR_UNSUPPORTED, "op %d: capacity*H exceeds 2^31 elements", o);
         if (d.capacity / d.row_align >= kMaxRowTiles)
@@ -918,12 +928,12 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
         p.H = d.H;
         p.I = d.I;
         p.capacity = d.capacity;
-        p.mt = d.row_align;
+        p.mt = ci.bm;
         p.n1 = d.I / (ci.bn / 2);
         p.n2 = d.H / ci.bn;
-        p.max_mtiles = (d.capacity + d.row_align - 1) / d.row_align + 1;
+        p.max_mtiles = (d.capacity + kSegAlign - 1) / kSegAlign + 1;   // row tiles never outnumber 32-row blocks
         size_t tb = 0;
-        const size_t ob = op_array_bytes(d.capacity, d.row_align, &tb);
+        const size_t ob = op_array_bytes(d.capacity, kSegAlign, &tb);
         p.table_off = (int32_t)off;
         p.g1_off = (int32_t)(off + tb);
         p.grp_off = (int32_t)(off + tb + (ob - tb) / 2);

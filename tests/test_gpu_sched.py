@@ -46,8 +46,7 @@ def _tiles_per_op(pipe, i):
     H, I = b.spec.weights.H, b.spec.weights.I
     from paper_2607_18002_amd import ops
     bm, bn, _ = ops.moe_ffn_tile_shape(b.spec.phase, b.spec.weights.dtype)
-    assert bm == b.row_align
-    xm = oracle.x_moe(counts, b.row_align)
+    xm = oracle.x_moe(counts, bm)                         # Eq. (3) at the tallest tile height
     return xm, xm * (I // (bn // 2)) + xm * (H // bn)
 
 

@@ -79,17 +79,19 @@ def test_decode_quota_matches_oracle():
 
 def test_row_align_and_workspace_queries():
     from paper_2607_18002_amd import _lib, ops
-    assert ops.moe_ffn_row_align(_lib.MOE_PREFILL, _lib.MOE_BF16) == 192   # tall prefill tile
-    assert ops.moe_ffn_row_align(_lib.MOE_DECODE, _lib.MOE_BF16) == 128
-    assert ops.moe_ffn_row_align(_lib.MOE_PREFILL, _lib.MOE_FP8_E4M3) == 64
-    assert ops.moe_ffn_row_align(_lib.MOE_DECODE, _lib.MOE_FP8_E4M3) == 64
+    # segments are aligned to one 32-row MFMA block; tiles are at most bm rows
+    for ph in (_lib.MOE_PREFILL, _lib.MOE_DECODE):
+        for dt in (_lib.MOE_BF16, _lib.MOE_FP8_E4M3):
+            assert ops.moe_ffn_row_align(ph, dt) == 32
+    assert ops.moe_ffn_tile_shape(_lib.MOE_PREFILL, _lib.MOE_BF16) == (192, 256, 64)   # tall prefill tile
+    assert ops.moe_ffn_tile_shape(_lib.MOE_DECODE, _lib.MOE_BF16) == (128, 256, 64)
     assert ops.moe_ffn_tile_shape(_lib.MOE_PREFILL, _lib.MOE_FP8_E4M3) == (64, 256, 128)
     assert ops.moe_ffn_row_align(7, _lib.MOE_BF16) < 0
     for ph in (_lib.MOE_PREFILL, _lib.MOE_DECODE):
         bm, bn, bk = ops.moe_ffn_tile_shape(ph, _lib.MOE_BF16)
-        assert bm == ops.moe_ffn_row_align(ph, _lib.MOE_BF16) and bn % 64 == 0 and bk % 16 == 0
+        assert bm % ops.moe_ffn_row_align(ph, _lib.MOE_BF16) == 0 and bn % 64 == 0 and bk % 16 == 0
     assert ops.moe_permute_workspace_bytes(16384, 8, 32) >= 32 * 32 * 4
-    d = _lib.OpDesc(capacity=69600, row_align=128)
+    d = _lib.OpDesc(capacity=69600, row_align=32)
     cfg = _lib.SchedConfig()
     assert ops.moe_ffn_workspace_bytes([d], cfg) >= 2 * (69600 // 128) * 4
 
