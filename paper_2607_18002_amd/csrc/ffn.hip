@@ -184,16 +184,18 @@ struct InitArgs {
     int64_t gaps[MOE_MAX_OPS];
     int32_t deps[MOE_MAX_OPS];
     int32_t phases[MOE_MAX_OPS];
-    int32_t n_ops, ws_words;
+    int32_t n_ops, ws_vec;           // ws_vec: 16-byte words of scheduler state
     char* ws;
     int32_t* status;
 };
 
-// Zeroes the scheduler state and writes the readiness fields; one workgroup,
-// launched on the same stream right before the persistent kernel.
+// Zeroes the scheduler state (16-byte stores; the row-tile tables too, so an
+// entry read before it was written reads as invalid rather than as a previous
+// launch's tile) and writes the readiness fields; one workgroup, launched on
+// the same stream right before the persistent kernel.
 __global__ __launch_bounds__(256) void apk_init_kernel(const InitArgs a) {
-    int32_t* w = (int32_t*)a.ws;
-    for (int i = threadIdx.x; i < a.ws_words; i += 256) w[i] = 0;
+    const u32x4 z = {0u, 0u, 0u, 0u};
+    for (int i = threadIdx.x; i < a.ws_vec; i += 256) ((u32x4*)a.ws)[i] = z;
     __syncthreads();
     if (threadIdx.x == 0) {
         OpStatic* st = static_of(a.ws);
@@ -984,7 +986,7 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
     if (n_wg > per_cu * cu) return fail(MOE_ERR_INVALID_ARG, "n_workgroups=%d exceeds co-resident capacity %d", n_wg, per_cu * cu);
 
     ia.n_ops = n_ops;
-    ia.ws_words = (int32_t)((kArraysOff + off) / 4);
+    ia.ws_vec = (int32_t)((kArraysOff + off) / 16);
     ia.ws = (char*)workspace;
     ia.status = status_word;
     hipStream_t s = (hipStream_t)stream;
