@@ -46,7 +46,7 @@ using namespace moeapk;
 
 using ShapeP = TileShape<192, 256, 64>;    // bf16 prefill: 192 x 256 tall tile, K step 64
 using ShapeD = TileShape<128, 256, 64>;    // bf16 decode : 128 x 256 tile, K step 64
-using ShapeF8 = TileShapeF8<64, 256>;      // fp8 (both phases): 64 x 256 tile, K step 128 (one scale block)
+using ShapeF8 = TileShapeF8<128, 256>;     // fp8 (both phases): 128 x 256 tile, K step 128 (one scale block)
 constexpr int kMax2(int a, int b) { return a > b ? a : b; }
 constexpr int kLdsBytes = kMax2(kMax2(TallLds<ShapeP>::bytes, ShapeD::LDS), ShapeF8::LDS);
 constexpr int kMaxRowTiles = 1 << 14;      // per op (14-bit field of a table entry)

@@ -16,7 +16,11 @@
 // the total costs one multiply and 16 FMAs per lane.
 //
 // Workgroup: 4 waves; wave w owns features [w*WCOLS, (w+1)*WCOLS) (NBW blocks
-// of 32) for all BM tokens.  Weights stream global -> registers through a ring
+// of 32) for all BM (up to 128) tokens.  Partial sums are kept for two row
+// blocks at a time (one folds while the next one's MFMAs run), so the tile
+// holds NBW * MACT running totals plus 2 * NBW partials: 192 accumulator
+// registers at 128 tokens.  The taller the tile, the fewer weight bytes per
+// flop it streams, and a 64-token tile was bound by that stream.  Weights stream global -> registers through a ring
 // of DEPTH K steps (moe_pack_weights' fp8 layout: per 32-row block and 128-K
 // chunk, [kk][half][lane][16 B]); activations are staged through double-
 // buffered LDS (rows padded by 16 bytes); the tile's activation scales are
@@ -55,6 +59,19 @@ struct TileRegsF8 {
     static constexpr int CA = MACT * 32 / S::RPP;     // activation chunks per thread and step
     static constexpr int DEPTH = MACT == 1 ? 4 : 2;   // weight steps in flight (32 VGPRs each)
 };
+
+// Per-lane scale factors of one K step's block: the token's activation scale
+// times each feature block's weight scale, folded into the running totals.
+template <class S, int MACT>
+__device__ __forceinline__ void fold_block(f32x16 (&tot)[S::NBW][MACT], const f32x16 (&part)[S::NBW], int i, float xs,
+                                           const float (&cw)[S::NBW]) {
+#pragma unroll
+    for (int j = 0; j < S::NBW; ++j) {
+        const float c = xs * cw[j];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) tot[j][i][r] = __builtin_fmaf(part[j][r], c, tot[j][i][r]);
+    }
+}
 
 // Weight operands of one K step: per block j and MFMA kk, 32 bytes per lane
 // (two 16-byte halves, each a 1 KB contiguous wave load).
@@ -160,40 +177,44 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
         for (int d = 0; d < D; ++d) {
             const int s = s0 + d;                                      // uniform; d and s & 1 are compile-time
             const char* cur = (d & 1) ? lds1 : lds0;
-            f32x16 part[S::NBW][MACT];
+            float cw[S::NBW];
 #pragma unroll
-            for (int kk = 0; kk < S::KK; ++kk) {
-                i32x8 xa[MACT];
+            for (int j = 0; j < S::NBW; ++j) cw[j] = sw[j][s];
+            const float* sxs = sx + s * S::BM + (lane & 31);
+            // Row block by row block: the block's two MFMAs per feature block
+            // go into a fresh partial (two partial sets alternate), and the
+            // previous row block's partial is folded into its total while
+            // they run, so partials take 2 * NBW accumulators, not MACT * NBW.
+            auto frag = [&](int i, int kk) {
+                const char* p = cur + arow + i * 32 * S::LDS_ROW + kk * 64;
+                const u32x4 lo = *(const u32x4*)p, hi = *(const u32x4*)(p + 16);
+                return i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+            };
+            f32x16 part[2][S::NBW];
+            i32x8 xa[2][S::KK];
 #pragma unroll
-                for (int i = 0; i < MACT; ++i) {
-                    const char* p = cur + arow + i * 32 * S::LDS_ROW + kk * 64;
-                    const u32x4 lo = *(const u32x4*)p, hi = *(const u32x4*)(p + 16);
-                    xa[i] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+            for (int kk = 0; kk < S::KK; ++kk) xa[0][kk] = frag(0, kk);
+#pragma unroll
+            for (int i = 0; i < MACT; ++i) {
+                if (i + 1 < MACT) {
+#pragma unroll
+                    for (int kk = 0; kk < S::KK; ++kk) xa[(i + 1) & 1][kk] = frag(i + 1, kk);
                 }
 #pragma unroll
-                for (int j = 0; j < S::NBW; ++j)
+                for (int j = 0; j < S::NBW; ++j) {
+                    const f32x16 c0 = {};
 #pragma unroll
-                    for (int i = 0; i < MACT; ++i) {
-                        const f32x16 c0 = {};
-                        part[j][i] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                            rw[d][j][kk], xa[i], kk == 0 ? c0 : part[j][i], 0, 0, 0, 127, 0, 127);
-                    }
+                    for (int kk = 0; kk < S::KK; ++kk)
+                        part[i & 1][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                            rw[d][j][kk], xa[i & 1][kk], kk == 0 ? c0 : part[i & 1][j], 0, 0, 0, 127, 0, 127);
+                }
+                if (i > 0) fold_block<S, MACT>(tot, part[(i - 1) & 1], i - 1, sxs[32 * (i - 1)], cw);
             }
             store_a<CA>((d & 1) ? lds0 : lds1, ra, alds);
             const int sw_ = s + D < last ? s + D : last, sa = s + 2 < last ? s + 2 : last;
             load_w8<S>(rw[d], Bb, boff, sw_ * KBW);
             load_a<CA>(ra, Ab, aoff, sa * S::BK);
-            // fold the block in: one scale per (feature block, token) pair
-#pragma unroll
-            for (int i = 0; i < MACT; ++i) {
-                const float xs = sx[s * S::BM + 32 * i + (lane & 31)];
-#pragma unroll
-                for (int j = 0; j < S::NBW; ++j) {
-                    const float c = xs * sw[j][s];
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) tot[j][i][r] = __builtin_fmaf(part[j][i][r], c, tot[j][i][r]);
-                }
-            }
+            fold_block<S, MACT>(tot, part[(MACT - 1) & 1], MACT - 1, sxs[32 * (MACT - 1)], cw);
             __syncthreads();
         }
     }
@@ -223,8 +244,8 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
             }
         }
         __syncthreads();
-        const int t = tid >> 2, qq = tid & 3;                       // 4 threads per token row, 32 values each
-        if (t < MACT * 32) {
+        const int qq = tid & 3;                                     // 4 threads per token row, 32 values each
+        for (int t = tid >> 2; t < MACT * 32; t += 64) {
             const f32x4* src = (const f32x4*)(hb + t * S::H_ROW + qq * 128);
             f32x4 v[8];
             float amax = 0.f;
@@ -305,13 +326,17 @@ __device__ __forceinline__ void gemm_tile_fp8_rows(int rows32, const uint8_t* A,
                                                    void* out, int ldo, float* osc, int ldsc, char* lds,
                                                    const int32_t* rowmap = nullptr, int k = 1, int a_rows = 0,
                                                    Hook hook = Hook{}) {
-    static_assert(S::MB == 2, "dispatch written for 64-row tiles");
-    if (rows32 > 32)
-        gemm_tile_fp8_depth<S, GLU, 2>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap, k,
-                                       a_rows, hook);
-    else
-        gemm_tile_fp8_depth<S, GLU, 1>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap, k,
-                                       a_rows, hook);
+    static_assert(S::MB == 4, "dispatch written for 128-row tiles");
+    switch (rows32 >> 5) {
+        case 1: gemm_tile_fp8_depth<S, GLU, 1>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap,
+                                               k, a_rows, hook); break;
+        case 2: gemm_tile_fp8_depth<S, GLU, 2>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap,
+                                               k, a_rows, hook); break;
+        case 3: gemm_tile_fp8_depth<S, GLU, 3>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap,
+                                               k, a_rows, hook); break;
+        default: gemm_tile_fp8_depth<S, GLU, 4>(A, lda, asc, B, n0, up_rows, wsc, K, out, ldo, osc, ldsc, lds, rowmap,
+                                                k, a_rows, hook); break;
+    }
 }
 
 }  // namespace moeapk

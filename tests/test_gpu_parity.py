@@ -456,7 +456,7 @@ def test_full_size_fp8_mixed_config(dev):
                                                    (768, 768, 900, 33, 128, 12, 8)])
 @pytest.mark.parametrize("fused", [False, True], ids=["x_perm", "gathered"])
 def test_fp8_small_configs(dev, H, I, T_p, T_d, E_g, E_l, k, fused):
-    """fp8 path on ragged shapes: 32- and 64-row tiles, several row tiles per
+    """fp8 path on ragged shapes: 32- to 128-row tiles, several row tiles per
     expert, an expert without rows; checked stage by stage (_check_fp8_op).
     At these small widths the fp8 rounding of h alone can exceed 3e-2 against
     the unquantized oracle, so the end-to-end 3e-2 bound is checked at the

@@ -85,7 +85,7 @@ def test_row_align_and_workspace_queries():
             assert ops.moe_ffn_row_align(ph, dt) == 32
     assert ops.moe_ffn_tile_shape(_lib.MOE_PREFILL, _lib.MOE_BF16) == (192, 256, 64)   # tall prefill tile
     assert ops.moe_ffn_tile_shape(_lib.MOE_DECODE, _lib.MOE_BF16) == (128, 256, 64)
-    assert ops.moe_ffn_tile_shape(_lib.MOE_PREFILL, _lib.MOE_FP8_E4M3) == (64, 256, 128)
+    assert ops.moe_ffn_tile_shape(_lib.MOE_PREFILL, _lib.MOE_FP8_E4M3) == (128, 256, 128)
     assert ops.moe_ffn_row_align(7, _lib.MOE_BF16) < 0
     for ph in (_lib.MOE_PREFILL, _lib.MOE_DECODE):
         bm, bn, bk = ops.moe_ffn_tile_shape(ph, _lib.MOE_BF16)
