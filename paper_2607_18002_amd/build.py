@@ -22,7 +22,8 @@ LIB = os.path.join(PKG, "libmoe_apk.so")
 SOURCES = ["api.cpp", "route.hip", "permute.hip", "combine.hip", "ffn.hip", "pack.hip"]
 # Every source file the persistent FFN kernel is compiled from (hashed to tie
 # recorded hardware-counter figures to the kernel they were taken on).
-FFN_KERNEL_SOURCES = ["paper_2607_18002_amd/csrc/ffn.hip", "paper_2607_18002_amd/csrc/tile_bf16.hpp", "paper_2607_18002_amd/csrc/tile_bf16_tall.hpp",
+FFN_KERNEL_SOURCES = ["paper_2607_18002_amd/csrc/ffn.hip", "paper_2607_18002_amd/csrc/tile_bf16.hpp",
+                      "paper_2607_18002_amd/csrc/tile_bf16_tall.hpp", "paper_2607_18002_amd/csrc/tile_fp8.hpp",
                       "paper_2607_18002_amd/csrc/common.hpp", "include/moe_apk.h"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
