@@ -228,6 +228,12 @@ typedef struct moe_sched_config {
     int64_t trace_capacity;
     moe_op_stats* op_stats;   /* NULL, or [n_ops]                                       */
     int64_t spin_limit;       /* bounded waits, in polls; 0 = default (about 2 s)       */
+    int32_t static_partition; /* 0: tile-level sharing as above.  1: a static split for
+                                 comparison (the analogue of fixed SM partitions such
+                                 as Green Contexts): workgroups below the fixed q' take
+                                 only decode tiles, the others only prefill tiles, and
+                                 neither borrows idle workgroups of the other phase   */
+    int32_t reserved1;
 } moe_sched_config;
 
 /* Segment alignment the FFN needs for ops of this phase and dtype (32 rows,

@@ -82,6 +82,8 @@ struct KArgs {
     int32_t n_ops, q, q_max, x_star, c, gmax;
     int32_t pre_wg;            // prefill tiles are claimed ahead only by workgroups >= pre_wg
     int32_t pre_dec_all;       // no prefill op in the launch: every workgroup claims decode tiles ahead
+    int32_t split;             // static partition: decode only below pre_wg, prefill only at or above
+    int32_t pad_k;
     int64_t spin_limit;
     const uint32_t* abort_word;
     moe_trace_rec* trace;
@@ -584,9 +586,9 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
     const uint64_t dmask = __ballot(active && phase == MOE_DECODE);
     const uint64_t pmask = __ballot(active && phase == MOE_PREFILL);
     const uint64_t own_avail = __ballot(active && own_claim < own_size);
-    const bool prefer_decode = wg < q;
+    const bool prefer_decode = a.split ? wg < a.pre_wg : wg < q;
     const uint64_t order[2] = {prefer_decode ? dmask : pmask, prefer_decode ? pmask : dmask};
-    for (int p = 0; p < 2; ++p) {
+    for (int p = 0; p < (a.split ? 1 : 2); ++p) {                   // a static partition never borrows
         uint64_t m = order[p];
         while (m) {                                                  // wave-uniform loop
             const int o = __ffsll((long long)m) - 1;
@@ -964,6 +966,15 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
         any_prefill |= ops[o].phase == MOE_PREFILL;
     }
     a.pre_dec_all = any_prefill ? 0 : 1;
+    if (cfg->static_partition < 0 || cfg->static_partition > 1)
+        return fail(MOE_ERR_INVALID_ARG, "static_partition=%d must be 0 or 1", cfg->static_partition);
+    a.split = cfg->static_partition;
+    if (a.split) {                                   // the split is the fixed q' (Eq. 4 with x*_moe <= 0)
+        a.pre_wg = moeapk::decode_quota(a.q, 0, 0, a.q_max, a.c);
+        a.pre_dec_all = 0;
+        if (a.x_star > 0 || a.pre_wg < 1 || a.pre_wg >= n_wg)
+            return fail(MOE_ERR_INVALID_ARG, "static_partition needs a fixed quota 0 < q' < n_workgroups");
+    }
     a.pre_wg = !any_decode ? 0 : (a.x_star <= 0 ? moeapk::decode_quota(a.q, 0, 0, a.q_max, a.c) : a.q_max);
     a.spin_limit = cfg->spin_limit > 0 ? cfg->spin_limit : (int64_t)2000000;
     a.abort_word = cfg->abort_word;

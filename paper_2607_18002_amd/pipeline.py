@@ -112,7 +112,8 @@ class MoEPipeline:
     def __init__(self, specs: List[OpSpec], n_workgroups: int = 0, decode_quota_wg: int = 64,
                  decode_quota_max_wg: int = 0, x_moe_expected: int = 0, round_multiple: int = 8,
                  trace_capacity: int = 0, spin_limit: int = 0, abort_word: Optional[torch.Tensor] = None,
-                 y_dtype: torch.dtype = torch.bfloat16, fused_gather: bool = False, group_row_tiles: int = 0):
+                 y_dtype: torch.dtype = torch.bfloat16, fused_gather: bool = False, group_row_tiles: int = 0,
+                 static_partition: bool = False):
         """fused_gather: GEMM-1 reads its rows straight from x through row_to_assign
         (permute then only builds the maps), instead of from a permuted copy x_perm."""
         if not specs:
@@ -161,7 +162,7 @@ class MoEPipeline:
                                abort_word=abort_word.data_ptr() if abort_word is not None else None,
                                trace=self.trace.data_ptr() if trace_capacity > 0 else None,
                                trace_capacity=trace_capacity, op_stats=self.stats.data_ptr(),
-                               spin_limit=spin_limit)
+                               spin_limit=spin_limit, static_partition=int(static_partition))
         self.descs = [self._desc(i, b, fused_gather) for i, b in enumerate(self.bufs)]
         self.ffn_ws = torch.zeros((K.moe_ffn_workspace_bytes(self.descs, self.cfg),), dtype=torch.uint8, device=dev)
 

@@ -180,3 +180,21 @@ def test_release_word_set_before_launch(dev):
     pipe = _pipe(dev, specs)
     assert pipe.statuses() == (0, 0)
     assert int(pipe.bufs[1].done_word.item()) == 1 and int(pipe.bufs[0].done_word.item()) == 1
+
+
+def test_static_partition_never_borrows(dev):
+    """The comparison mode of a static split: decode tiles run only on
+    workgroups below q, prefill tiles only on the others, even while one side
+    idles; results stay bitwise those of tile-level sharing."""
+    cfg = _mixed_cfg()
+    specs, _, _ = layer_specs(cfg, 0, dev, decode=dict(release_after_ns=3_000))
+    shared = _pipe(dev, specs, decode_quota_wg=64)
+    want = [b.y.view(torch.int16).cpu().numpy().copy() for b in shared.bufs]
+    specs, _, _ = layer_specs(cfg, 0, dev, decode=dict(release_after_ns=3_000))
+    pipe = _pipe(dev, specs, decode_quota_wg=64, static_partition=True, trace_capacity=1 << 16)
+    assert pipe.statuses() == (0, 0)
+    tr = pipe.trace_records()
+    assert tr[tr["op"] == 1]["wg"].max() < 64
+    assert tr[tr["op"] == 0]["wg"].min() >= 64
+    for b, w in zip(pipe.bufs, want):
+        np.testing.assert_array_equal(b.y.view(torch.int16).cpu().numpy(), w)
