@@ -87,6 +87,19 @@ moe_status_t moe_topk_route(const float* logits, int32_t T, int32_t E_global, in
                             int32_t local_begin, int32_t E_local,
                             int32_t* topk_ids, float* topk_w, void* stream);
 
+/* The same gating for up to MOE_MAX_OPS operations (e.g. the layers and
+ * phases of one persistent launch) in ONE kernel launch: each entry is one
+ * moe_topk_route call's arguments, with the same meaning, limits and results
+ * (bitwise).  ops: host array of n_ops entries, read before the call returns;
+ * argument errors of any entry are returned before anything is launched. */
+typedef struct moe_route_args {
+    const float* logits;
+    int32_t T, E_global, top_k, local_begin, E_local;
+    int32_t* topk_ids;
+    float* topk_w;
+} moe_route_args;
+moe_status_t moe_topk_route_batch(const moe_route_args* ops, int32_t n_ops, void* stream);
+
 /* ------------------------------------------------------------------------- a2
  * Permutation into per-expert contiguous segments at final offsets
  * (Background, "Prefill-Decode Disaggregation": the contiguous layout;
@@ -129,6 +142,30 @@ moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t top_k, int3
                          int32_t* counts, int32_t* offsets, int32_t* row_to_assign,
                          int32_t* assign_to_row, void* x_perm, float* x_perm_scales,
                          void* workspace, int32_t* error_flag, void* stream);
+
+/* The same permutation for up to MOE_MAX_OPS operations with one launch per
+ * pass (count, scatter; the optional activation copies stay one launch per
+ * op): each entry is one moe_permute call's arguments, same meaning, limits
+ * and results (bitwise).  Entries must not share a workspace.  ops: host
+ * array of n_ops entries, read before the call returns; argument errors of
+ * any entry are returned before anything is launched. */
+typedef struct moe_permute_args {
+    const int32_t* topk_ids;
+    int32_t T, top_k, E_local;
+    moe_dtype_t x_dtype;
+    const void* x;
+    const float* x_scales;
+    int32_t H, row_align, capacity, pad0;
+    int32_t* counts;
+    int32_t* offsets;
+    int32_t* row_to_assign;
+    int32_t* assign_to_row;
+    void* x_perm;
+    float* x_perm_scales;
+    void* workspace;
+    int32_t* error_flag;
+} moe_permute_args;
+moe_status_t moe_permute_batch(const moe_permute_args* ops, int32_t n_ops, void* stream);
 
 /* ------------------------------------------------------------------------- a3-a6
  * Operation template (Adaptive Persistent Kernel, "Tile-Level Scheduling":
@@ -293,6 +330,21 @@ moe_status_t moe_combine(const void* y_perm, const int32_t* assign_to_row, const
                          int32_t T, int32_t top_k, int32_t H, void* y, moe_dtype_t y_dtype,
                          void* stream);
 
+/* The same combine for up to MOE_MAX_OPS operations in ONE launch: each entry
+ * is one moe_combine call's arguments, same meaning, limits and results
+ * (bitwise); all entries take the same y_dtype.  ops: host array of n_ops
+ * entries, read before the call returns; argument errors of any entry are
+ * returned before anything is launched. */
+typedef struct moe_combine_args {
+    const void* y_perm;
+    const int32_t* assign_to_row;
+    const float* topk_w;
+    int32_t T, top_k, H;
+    moe_dtype_t y_dtype;
+    void* y;
+} moe_combine_args;
+moe_status_t moe_combine_batch(const moe_combine_args* ops, int32_t n_ops, void* stream);
+
 /* ------------------------------------------------------------------------- host helpers
  * Pure host arithmetic shared with the kernels (no device access):
  * Eq. (3) footprint over host counts, and Eq. (4) quota in workgroups. */
@@ -301,7 +353,8 @@ int32_t moe_decode_quota(int32_t q, int32_t x_moe, int32_t x_moe_expected, int32
                          int32_t round_multiple);
 
 /* sizeof() of the ABI structs, so bindings can check their layout:
- * 0 moe_op_desc, 1 moe_sched_config, 2 moe_trace_rec, 3 moe_op_stats; 0 otherwise. */
+ * 0 moe_op_desc, 1 moe_sched_config, 2 moe_trace_rec, 3 moe_op_stats,
+ * 4 moe_route_args, 5 moe_permute_args, 6 moe_combine_args; 0 otherwise. */
 size_t moe_abi_sizeof(int32_t which);
 
 const char* moe_status_string(moe_status_t status);

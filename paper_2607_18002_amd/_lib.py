@@ -68,9 +68,35 @@ class OpStats(C.Structure):
     ]
 
 
+class RouteArgs(C.Structure):
+    _fields_ = [
+        ("logits", _p), ("T", _i32), ("E_global", _i32), ("top_k", _i32), ("local_begin", _i32),
+        ("E_local", _i32), ("topk_ids", _p), ("topk_w", _p),
+    ]
+
+
+class PermuteArgs(C.Structure):
+    _fields_ = [
+        ("topk_ids", _p), ("T", _i32), ("top_k", _i32), ("E_local", _i32), ("x_dtype", _i32),
+        ("x", _p), ("x_scales", _p), ("H", _i32), ("row_align", _i32), ("capacity", _i32), ("pad0", _i32),
+        ("counts", _p), ("offsets", _p), ("row_to_assign", _p), ("assign_to_row", _p), ("x_perm", _p),
+        ("x_perm_scales", _p), ("workspace", _p), ("error_flag", _p),
+    ]
+
+
+class CombineArgs(C.Structure):
+    _fields_ = [
+        ("y_perm", _p), ("assign_to_row", _p), ("topk_w", _p), ("T", _i32), ("top_k", _i32), ("H", _i32),
+        ("y_dtype", _i32), ("y", _p),
+    ]
+
+
 # name -> (restype, argtypes)
 PROTOTYPES = {
     "moe_topk_route": (_i32, [_p, _i32, _i32, _i32, _i32, _i32, _p, _p, _p]),
+    "moe_topk_route_batch": (_i32, [C.POINTER(RouteArgs), _i32, _p]),
+    "moe_permute_batch": (_i32, [C.POINTER(PermuteArgs), _i32, _p]),
+    "moe_combine_batch": (_i32, [C.POINTER(CombineArgs), _i32, _p]),
     "moe_permute_workspace_bytes": (C.c_size_t, [_i32, _i32, _i32]),
     "moe_permute": (_i32, [_p, _i32, _i32, _i32, _p, _i32, _p, _i32, _i32, _i32,
                            _p, _p, _p, _p, _p, _p, _p, _p, _p]),
@@ -103,7 +129,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
         fn = getattr(lib, name)
         fn.restype = res
         fn.argtypes = args
-    for which, cls in enumerate((OpDesc, SchedConfig, TraceRec, OpStats)):
+    for which, cls in enumerate((OpDesc, SchedConfig, TraceRec, OpStats, RouteArgs, PermuteArgs, CombineArgs)):
         if lib.moe_abi_sizeof(which) != C.sizeof(cls):
             raise RuntimeError(f"ABI mismatch: sizeof({cls.__name__}) is {C.sizeof(cls)} in Python, "
                                f"{lib.moe_abi_sizeof(which)} in the library")

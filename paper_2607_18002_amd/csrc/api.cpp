@@ -84,6 +84,9 @@ size_t moe_abi_sizeof(int32_t which) {
         case 1: return sizeof(moe_sched_config);
         case 2: return sizeof(moe_trace_rec);
         case 3: return sizeof(moe_op_stats);
+        case 4: return sizeof(moe_route_args);
+        case 5: return sizeof(moe_permute_args);
+        case 6: return sizeof(moe_combine_args);
         default: return 0;
     }
 }

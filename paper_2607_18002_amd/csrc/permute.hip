@@ -17,6 +17,8 @@
 //             launch marks every padding row of the segments -1.
 //   gather  : only with x_perm: one wave per row copies x[a / k] (16-byte
 //             vectors) into x_perm and zero-fills padding rows.
+#include <cstring>
+
 #include "common.hpp"
 
 namespace {
@@ -59,18 +61,18 @@ __device__ void block_offsets(int E, int align, int capacity, const int32_t* tot
     __syncthreads();
 }
 
-__global__ __launch_bounds__(256) void permute_count_kernel(const int32_t* __restrict__ ids, int A, int E, int NB,
-                                                           int align, int capacity, unsigned* __restrict__ ticket,
-                                                           int32_t* __restrict__ blk_cnt,   // counts, then bases
-                                                           int32_t* __restrict__ counts,
-                                                           int32_t* __restrict__ offsets,
-                                                           int32_t* __restrict__ err) {
+// Block blk (of NB) of one op's count pass.
+__device__ __forceinline__ void count_block(const int32_t* __restrict__ ids, int A, int E, int NB, int align,
+                                            int capacity, unsigned* __restrict__ ticket,
+                                            int32_t* __restrict__ blk_cnt,   // counts, then bases
+                                            int32_t* __restrict__ counts, int32_t* __restrict__ offsets,
+                                            int32_t* __restrict__ err, int blk) {
     extern __shared__ int32_t hist[];                          // [E] histogram, later [E] totals + [E] offsets
     __shared__ int32_t part[kThreads * 4];                     // per (expert, run): run sum, then run base
     __shared__ int s_last;
     for (int e = threadIdx.x; e < E; e += kThreads) hist[e] = 0;
     __syncthreads();
-    const int base = blockIdx.x * kChunk;
+    const int base = blk * kChunk;
     for (int it = 0; it < kIters; ++it) {
         const int a = base + it * kThreads + threadIdx.x;
         if (a < A) {
@@ -80,7 +82,7 @@ __global__ __launch_bounds__(256) void permute_count_kernel(const int32_t* __res
         }
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < E; e += kThreads) blk_cnt[(size_t)blockIdx.x * E + e] = hist[e];
+    for (int e = threadIdx.x; e < E; e += kThreads) blk_cnt[(size_t)blk * E + e] = hist[e];
     // Publish this block's counts, then take a ticket; the last block scans.
     // atomicInc wraps to 0 on the last ticket, so the counter is ready for the next call.
     __threadfence();
@@ -141,15 +143,16 @@ __global__ __launch_bounds__(256) void permute_count_kernel(const int32_t* __res
     }
 }
 
-__global__ __launch_bounds__(256) void permute_scatter_kernel(const int32_t* __restrict__ ids, int A, int E,
-                                                             int capacity, const int32_t* __restrict__ blk_base,
-                                                             const int32_t* __restrict__ counts,
-                                                             const int32_t* __restrict__ offsets,
-                                                             int32_t* __restrict__ row_to_assign,
-                                                             int32_t* __restrict__ assign_to_row,
-                                                             int32_t* __restrict__ err) {
-    // padding rows [offsets[e] + counts[e], offsets[e+1]) of experts e = block, block + grid, ...
-    for (int e = blockIdx.x; e < E; e += gridDim.x) {
+// Block blk (of NB) of one op's scatter pass.
+__device__ __forceinline__ void scatter_block(const int32_t* __restrict__ ids, int A, int E, int capacity,
+                                              const int32_t* __restrict__ blk_base,
+                                              const int32_t* __restrict__ counts,
+                                              const int32_t* __restrict__ offsets,
+                                              int32_t* __restrict__ row_to_assign,
+                                              int32_t* __restrict__ assign_to_row, int32_t* __restrict__ err,
+                                              int blk, int NB) {
+    // padding rows [offsets[e] + counts[e], offsets[e+1]) of experts e = blk, blk + NB, ...
+    for (int e = blk; e < E; e += NB) {
         const int r0 = offsets[e] + counts[e], r1 = min(offsets[e + 1], capacity);
         for (int r = r0 + (int)threadIdx.x; r < r1; r += kThreads) row_to_assign[r] = -1;
     }
@@ -159,8 +162,8 @@ __global__ __launch_bounds__(256) void permute_scatter_kernel(const int32_t* __r
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int i = tid; i < 5 * E; i += kThreads) sm[i] = 0;
     __syncthreads();
-    const int base = blockIdx.x * kChunk;
-    const int32_t* my_base = blk_base + (size_t)blockIdx.x * E;
+    const int base = blk * kChunk;
+    const int32_t* my_base = blk_base + (size_t)blk * E;
     for (int it = 0; it < kIters; ++it) {
         const int a = base + it * kThreads + tid;
         int id = (a < A) ? ids[a] : -1;
@@ -197,6 +200,58 @@ __global__ __launch_bounds__(256) void permute_scatter_kernel(const int32_t* __r
         for (int i = tid; i < 4 * E; i += kThreads) wcnt[i] = 0;
         __syncthreads();
     }
+}
+
+__global__ __launch_bounds__(256) void permute_count_kernel(const int32_t* __restrict__ ids, int A, int E, int NB,
+                                                           int align, int capacity, unsigned* __restrict__ ticket,
+                                                           int32_t* __restrict__ blk_cnt, int32_t* __restrict__ counts,
+                                                           int32_t* __restrict__ offsets, int32_t* __restrict__ err) {
+    count_block(ids, A, E, NB, align, capacity, ticket, blk_cnt, counts, offsets, err, blockIdx.x);
+}
+
+__global__ __launch_bounds__(256) void permute_scatter_kernel(const int32_t* __restrict__ ids, int A, int E,
+                                                             int capacity, const int32_t* __restrict__ blk_base,
+                                                             const int32_t* __restrict__ counts,
+                                                             const int32_t* __restrict__ offsets,
+                                                             int32_t* __restrict__ row_to_assign,
+                                                             int32_t* __restrict__ assign_to_row,
+                                                             int32_t* __restrict__ err) {
+    scatter_block(ids, A, E, capacity, blk_base, counts, offsets, row_to_assign, assign_to_row, err, blockIdx.x,
+                  gridDim.x);
+}
+
+// Several ops' count and scatter passes in one launch each: op o owns blocks
+// [blk0[o], blk0[o + 1]) and its own workspace (ticket and chunk table).
+struct PermOp {
+    const int32_t* ids;
+    int32_t *counts, *offsets, *row_to_assign, *assign_to_row, *err, *blk;
+    unsigned* ticket;
+    int32_t A, E, NB, align, capacity, pad;
+};
+struct PermBatch {
+    PermOp op[MOE_MAX_OPS];
+    int32_t blk0[MOE_MAX_OPS + 1];
+    int32_t n;
+};
+
+__device__ __forceinline__ int batch_op(const PermBatch& b) {
+    int o = 0;
+    while (o + 1 < b.n && (int)blockIdx.x >= b.blk0[o + 1]) ++o;      // uniform
+    return o;
+}
+
+__global__ __launch_bounds__(256) void permute_count_batch_kernel(const PermBatch b) {
+    const int o = batch_op(b);
+    const PermOp& p = b.op[o];
+    count_block(p.ids, p.A, p.E, p.NB, p.align, p.capacity, p.ticket, p.blk, p.counts, p.offsets, p.err,
+                (int)blockIdx.x - b.blk0[o]);
+}
+
+__global__ __launch_bounds__(256) void permute_scatter_batch_kernel(const PermBatch b) {
+    const int o = batch_op(b);
+    const PermOp& p = b.op[o];
+    scatter_block(p.ids, p.A, p.E, p.capacity, p.blk, p.counts, p.offsets, p.row_to_assign, p.assign_to_row, p.err,
+                  (int)blockIdx.x - b.blk0[o], p.NB);
 }
 
 // One wave per row, grid-stride over rows [0, offsets[E]).
@@ -254,11 +309,12 @@ extern "C" size_t moe_permute_workspace_bytes(int32_t T, int32_t top_k, int32_t 
     return kWsHeader + (size_t)(nb > 0 ? nb : 1) * (size_t)E_local * sizeof(int32_t);
 }
 
-extern "C" moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t top_k, int32_t E_local,
-                                    const void* x, moe_dtype_t x_dtype, const float* x_scales, int32_t H,
-                                    int32_t row_align, int32_t capacity, int32_t* counts, int32_t* offsets,
-                                    int32_t* row_to_assign, int32_t* assign_to_row, void* x_perm,
-                                    float* x_perm_scales, void* workspace, int32_t* error_flag, void* stream) {
+namespace {
+moe_status_t check_permute(const int32_t* topk_ids, int32_t T, int32_t top_k, int32_t E_local, const void* x,
+                           moe_dtype_t x_dtype, const float* x_scales, int32_t H, int32_t row_align,
+                           int32_t capacity, const int32_t* counts, const int32_t* offsets,
+                           const int32_t* row_to_assign, const int32_t* assign_to_row, const void* x_perm,
+                           const float* x_perm_scales, const void* workspace, const int32_t* error_flag) {
     using moeapk_host::fail;
     if (T < 0 || top_k < 1 || top_k > 32) return fail(MOE_ERR_INVALID_ARG, "moe_permute: T=%d top_k=%d", T, top_k);
     if (E_local < 1 || E_local > 1024) return fail(MOE_ERR_UNSUPPORTED, "moe_permute: E_local=%d outside [1,1024]", E_local);
@@ -277,8 +333,37 @@ extern "C" moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t 
         return fail(MOE_ERR_INVALID_ARG, "moe_permute: null pointer");
     if (fp8 && x_perm && (!x_scales || !x_perm_scales))
         return fail(MOE_ERR_INVALID_ARG, "moe_permute: fp8 activations need x_scales and x_perm_scales");
-    moe_status_t st = moeapk_host::check_device();
+    return MOE_OK;
+}
+
+// The activation copy of one op (only when x_perm is requested).
+moe_status_t launch_gather(const int32_t* counts, const int32_t* offsets, int32_t E_local, int32_t top_k,
+                           int32_t capacity, const void* x, bool fp8, const float* x_scales, int32_t H,
+                           int32_t* row_to_assign, void* x_perm, float* x_perm_scales, hipStream_t s) {
+    const int row_bytes = fp8 ? H : 2 * H;
+    int grid = (capacity + 3) / 4;
+    if (grid > 4096) grid = 4096;
+    if (grid < 1) grid = 1;
+    hipLaunchKernelGGL(permute_gather_kernel, dim3(grid), dim3(256), (2 * E_local + 1) * sizeof(int32_t), s, counts,
+                       offsets, E_local, top_k, capacity, (const uint4*)x, row_bytes / 16, x_scales,
+                       fp8 ? H / 128 : 0, row_to_assign, (uint4*)x_perm, fp8 ? x_perm_scales : nullptr);
+    return MOE_OK;
+}
+}  // namespace
+
+extern "C" moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t top_k, int32_t E_local,
+                                    const void* x, moe_dtype_t x_dtype, const float* x_scales, int32_t H,
+                                    int32_t row_align, int32_t capacity, int32_t* counts, int32_t* offsets,
+                                    int32_t* row_to_assign, int32_t* assign_to_row, void* x_perm,
+                                    float* x_perm_scales, void* workspace, int32_t* error_flag, void* stream) {
+    using moeapk_host::fail;
+    moe_status_t st = check_permute(topk_ids, T, top_k, E_local, x, x_dtype, x_scales, H, row_align, capacity,
+                                    counts, offsets, row_to_assign, assign_to_row, x_perm, x_perm_scales,
+                                    workspace, error_flag);
     if (st != MOE_OK) return st;
+    st = moeapk_host::check_device();
+    if (st != MOE_OK) return st;
+    const bool fp8 = x_dtype == MOE_FP8_E4M3;
 
     hipStream_t s = (hipStream_t)stream;
     const int A = T * top_k;
@@ -295,15 +380,64 @@ extern "C" moe_status_t moe_permute(const int32_t* topk_ids, int32_t T, int32_t 
         if (err != hipSuccess) return fail(MOE_ERR_HIP, "moe_permute: launch failed: %s", hipGetErrorString(err));
         return MOE_OK;
     }
-    const int row_bytes = fp8 ? H : 2 * H;
-    const int rows_max = capacity;
-    int grid = (rows_max + 3) / 4;
-    if (grid > 4096) grid = 4096;
-    if (grid < 1) grid = 1;
-    hipLaunchKernelGGL(permute_gather_kernel, dim3(grid), dim3(256), (2 * E_local + 1) * sizeof(int32_t), s, counts,
-                       offsets, E_local, top_k, capacity, (const uint4*)x, row_bytes / 16, x_scales,
-                       fp8 ? H / 128 : 0, row_to_assign, (uint4*)x_perm, fp8 ? x_perm_scales : nullptr);
+    launch_gather(counts, offsets, E_local, top_k, capacity, x, fp8, x_scales, H, row_to_assign, x_perm, x_perm_scales,
+                  s);
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(MOE_ERR_HIP, "moe_permute: launch failed: %s", hipGetErrorString(err));
+    return MOE_OK;
+}
+
+extern "C" moe_status_t moe_permute_batch(const moe_permute_args* ops, int32_t n_ops, void* stream) {
+    using moeapk_host::fail;
+    if (!ops || n_ops < 1 || n_ops > MOE_MAX_OPS)
+        return fail(MOE_ERR_INVALID_ARG, "moe_permute_batch: n_ops=%d outside [1,%d]", n_ops, MOE_MAX_OPS);
+    PermBatch b;
+    memset(&b, 0, sizeof(b));
+    int64_t blocks = 0;
+    int e_max = 1;
+    for (int o = 0; o < n_ops; ++o) {
+        const moe_permute_args& a = ops[o];
+        const moe_status_t st = check_permute(a.topk_ids, a.T, a.top_k, a.E_local, a.x, a.x_dtype, a.x_scales, a.H,
+                                              a.row_align, a.capacity, a.counts, a.offsets, a.row_to_assign,
+                                              a.assign_to_row, a.x_perm, a.x_perm_scales, a.workspace,
+                                              a.error_flag);
+        if (st != MOE_OK) return st;
+        const int nb = num_chunks(a.T, a.top_k);
+        PermOp& p = b.op[o];
+        p.ids = a.topk_ids;
+        p.counts = a.counts;
+        p.offsets = a.offsets;
+        p.row_to_assign = a.row_to_assign;
+        p.assign_to_row = a.assign_to_row;
+        p.err = a.error_flag;
+        p.ticket = (unsigned*)a.workspace;
+        p.blk = (int32_t*)((char*)a.workspace + kWsHeader);
+        p.A = a.T * a.top_k;
+        p.E = a.E_local;
+        p.NB = nb > 0 ? nb : 1;                                 // T == 0: one block writes zero counts
+        p.align = a.row_align;
+        p.capacity = a.capacity;
+        b.blk0[o] = (int32_t)blocks;
+        blocks += p.NB;
+        e_max = a.E_local > e_max ? a.E_local : e_max;
+    }
+    if (blocks > INT32_MAX) return fail(MOE_ERR_UNSUPPORTED, "moe_permute_batch: too many assignments");
+    b.blk0[n_ops] = (int32_t)blocks;
+    b.n = n_ops;
+    moe_status_t st = moeapk_host::check_device();
+    if (st != MOE_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    hipLaunchKernelGGL(permute_count_batch_kernel, dim3((unsigned)blocks), dim3(kThreads),
+                       2 * e_max * sizeof(int32_t), s, b);
+    hipLaunchKernelGGL(permute_scatter_batch_kernel, dim3((unsigned)blocks), dim3(kThreads),
+                       5 * e_max * sizeof(int32_t), s, b);
+    for (int o = 0; o < n_ops; ++o) {
+        const moe_permute_args& a = ops[o];
+        if (a.x_perm)
+            launch_gather(a.counts, a.offsets, a.E_local, a.top_k, a.capacity, a.x, a.x_dtype == MOE_FP8_E4M3,
+                          a.x_scales, a.H, a.row_to_assign, a.x_perm, a.x_perm_scales, s);
+    }
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return fail(MOE_ERR_HIP, "moe_permute_batch: launch failed: %s", hipGetErrorString(err));
     return MOE_OK;
 }

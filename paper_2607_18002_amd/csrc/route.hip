@@ -7,6 +7,8 @@
 // wave-wide max and retires the winner; lane j keeps slot j.  The wave-wide
 // reductions stay in the vector ALU: DPP quad permutes and row mirrors give
 // every lane its 16-lane row's result, four lane reads combine the rows.
+#include <cstring>
+
 #include "common.hpp"
 
 namespace {
@@ -64,12 +66,12 @@ __device__ __forceinline__ float wave_sum(float v) {
     return (r0 + r1) + (r2 + r3);
 }
 
+// One op's routing: block `blk` of the op handles tokens [4*blk, 4*blk + 4).
 template <int EPL>
-__global__ __launch_bounds__(256) void topk_route_kernel(const float* __restrict__ logits, int T, int E, int k,
-                                                        int local_begin, int E_local, int32_t* __restrict__ ids,
-                                                        float* __restrict__ wts) {
+__device__ __forceinline__ void route_block(const float* __restrict__ logits, int T, int E, int k, int local_begin,
+                                            int E_local, int32_t* __restrict__ ids, float* __restrict__ wts, int blk) {
     const int lane = threadIdx.x & 63;
-    const int t = blockIdx.x * kTokensPerBlock + (threadIdx.x >> 6);
+    const int t = blk * kTokensPerBlock + (threadIdx.x >> 6);
     if (t >= T) return;  // wave-uniform
     const float* row = logits + (size_t)t * E;
     // all loads first (clamped in-row indices, no branches), so they are in flight together
@@ -108,11 +110,31 @@ __global__ __launch_bounds__(256) void topk_route_kernel(const float* __restrict
     }
 }
 
-}  // namespace
+template <int EPL>
+__global__ __launch_bounds__(256) void topk_route_kernel(const float* __restrict__ logits, int T, int E, int k,
+                                                        int local_begin, int E_local, int32_t* __restrict__ ids,
+                                                        float* __restrict__ wts) {
+    route_block<EPL>(logits, T, E, k, local_begin, E_local, ids, wts, blockIdx.x);
+}
 
-extern "C" moe_status_t moe_topk_route(const float* logits, int32_t T, int32_t E_global, int32_t top_k,
-                                       int32_t local_begin, int32_t E_local, int32_t* topk_ids, float* topk_w,
-                                       void* stream) {
+// Several ops in one launch: op o owns blocks [blk0[o], blk0[o + 1]).
+struct RouteBatch {
+    moe_route_args op[MOE_MAX_OPS];
+    int32_t blk0[MOE_MAX_OPS + 1];
+    int32_t n;
+};
+
+template <int EPL>
+__global__ __launch_bounds__(256) void topk_route_batch_kernel(const RouteBatch b) {
+    int o = 0;
+    while (o + 1 < b.n && (int)blockIdx.x >= b.blk0[o + 1]) ++o;      // uniform
+    const moe_route_args& a = b.op[o];
+    route_block<EPL>(a.logits, a.T, a.E_global, a.top_k, a.local_begin, a.E_local, a.topk_ids, a.topk_w,
+                     (int)blockIdx.x - b.blk0[o]);
+}
+
+moe_status_t check_route(const float* logits, int32_t T, int32_t E_global, int32_t top_k, int32_t local_begin,
+                         int32_t E_local, const int32_t* topk_ids, const float* topk_w) {
     using moeapk_host::fail;
     if (T < 0) return fail(MOE_ERR_INVALID_ARG, "moe_topk_route: T=%d < 0", T);
     if (E_global < 1 || E_global > 1024)
@@ -121,9 +143,20 @@ extern "C" moe_status_t moe_topk_route(const float* logits, int32_t T, int32_t E
         return fail(MOE_ERR_INVALID_ARG, "moe_topk_route: top_k=%d outside [1, min(E_global,32)]", top_k);
     if (local_begin < 0 || E_local < 1)
         return fail(MOE_ERR_INVALID_ARG, "moe_topk_route: local_begin=%d E_local=%d", local_begin, E_local);
+    if (T > 0 && (!logits || !topk_ids || !topk_w)) return fail(MOE_ERR_INVALID_ARG, "moe_topk_route: null pointer");
+    return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" moe_status_t moe_topk_route(const float* logits, int32_t T, int32_t E_global, int32_t top_k,
+                                       int32_t local_begin, int32_t E_local, int32_t* topk_ids, float* topk_w,
+                                       void* stream) {
+    using moeapk_host::fail;
+    moe_status_t st = check_route(logits, T, E_global, top_k, local_begin, E_local, topk_ids, topk_w);
+    if (st != MOE_OK) return st;
     if (T == 0) return MOE_OK;
-    if (!logits || !topk_ids || !topk_w) return fail(MOE_ERR_INVALID_ARG, "moe_topk_route: null pointer");
-    moe_status_t st = moeapk_host::check_device();
+    st = moeapk_host::check_device();
     if (st != MOE_OK) return st;
     hipStream_t s = (hipStream_t)stream;
     const dim3 grid((T + kTokensPerBlock - 1) / kTokensPerBlock), block(256);
@@ -135,5 +168,42 @@ extern "C" moe_status_t moe_topk_route(const float* logits, int32_t T, int32_t E
     else hipLaunchKernelGGL(topk_route_kernel<16>, grid, block, 0, s, logits, T, E_global, top_k, local_begin, E_local, topk_ids, topk_w);
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(MOE_ERR_HIP, "moe_topk_route: launch failed: %s", hipGetErrorString(err));
+    return MOE_OK;
+}
+
+extern "C" moe_status_t moe_topk_route_batch(const moe_route_args* ops, int32_t n_ops, void* stream) {
+    using moeapk_host::fail;
+    if (!ops || n_ops < 1 || n_ops > MOE_MAX_OPS)
+        return fail(MOE_ERR_INVALID_ARG, "moe_topk_route_batch: n_ops=%d outside [1,%d]", n_ops, MOE_MAX_OPS);
+    RouteBatch b;
+    memset(&b, 0, sizeof(b));
+    int epl = 1;
+    int64_t blocks = 0;
+    for (int o = 0; o < n_ops; ++o) {
+        const moe_route_args& a = ops[o];
+        const moe_status_t st = check_route(a.logits, a.T, a.E_global, a.top_k, a.local_begin, a.E_local,
+                                            a.topk_ids, a.topk_w);
+        if (st != MOE_OK) return st;
+        b.op[o] = a;
+        b.blk0[o] = (int32_t)blocks;
+        blocks += (a.T + kTokensPerBlock - 1) / kTokensPerBlock;
+        const int e = (a.E_global + 63) / 64;
+        epl = e > epl ? e : epl;
+    }
+    if (blocks > INT32_MAX) return fail(MOE_ERR_UNSUPPORTED, "moe_topk_route_batch: too many tokens");
+    b.blk0[n_ops] = (int32_t)blocks;
+    b.n = n_ops;
+    if (blocks == 0) return MOE_OK;
+    moe_status_t st = moeapk_host::check_device();
+    if (st != MOE_OK) return st;
+    hipStream_t s = (hipStream_t)stream;
+    const dim3 grid((unsigned)blocks), block(256);
+    if (epl <= 1) hipLaunchKernelGGL(topk_route_batch_kernel<1>, grid, block, 0, s, b);
+    else if (epl <= 2) hipLaunchKernelGGL(topk_route_batch_kernel<2>, grid, block, 0, s, b);
+    else if (epl <= 4) hipLaunchKernelGGL(topk_route_batch_kernel<4>, grid, block, 0, s, b);
+    else if (epl <= 8) hipLaunchKernelGGL(topk_route_batch_kernel<8>, grid, block, 0, s, b);
+    else hipLaunchKernelGGL(topk_route_batch_kernel<16>, grid, block, 0, s, b);
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return fail(MOE_ERR_HIP, "moe_topk_route_batch: launch failed: %s", hipGetErrorString(err));
     return MOE_OK;
 }

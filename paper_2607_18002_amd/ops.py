@@ -9,7 +9,8 @@ from typing import Optional, Sequence
 import torch
 
 from . import _lib
-from ._lib import MOE_BF16, MOE_F32, MOE_FP8_E4M3, OpDesc, SchedConfig, check, load_library
+from ._lib import (MOE_BF16, MOE_F32, MOE_FP8_E4M3, CombineArgs, OpDesc, PermuteArgs, RouteArgs, SchedConfig, check,
+                   load_library)
 
 
 def _stream(stream: Optional[torch.cuda.Stream]) -> int:
@@ -49,6 +50,26 @@ def moe_topk_route(logits: torch.Tensor, top_k: int, local_begin: int, E_local: 
     return topk_ids, topk_w
 
 
+def _array(cls, entries):
+    arr = (cls * len(entries))()
+    for i, e in enumerate(entries):
+        arr[i] = e
+    return arr
+
+
+def moe_topk_route_batch(entries: Sequence[RouteArgs], stream=None) -> None:
+    """moe_topk_route for several ops in one launch (entries: RouteArgs)."""
+    check(load_library().moe_topk_route_batch(_array(RouteArgs, entries), len(entries), _stream(stream)),
+          "moe_topk_route_batch")
+
+
+def route_args(logits: torch.Tensor, top_k: int, local_begin: int, E_local: int, topk_ids: torch.Tensor,
+               topk_w: torch.Tensor) -> RouteArgs:
+    T, E = logits.shape
+    return RouteArgs(logits=_ptr(logits), T=T, E_global=E, top_k=top_k, local_begin=local_begin, E_local=E_local,
+                     topk_ids=_ptr(topk_ids), topk_w=_ptr(topk_w))
+
+
 def moe_permute_workspace_bytes(T: int, top_k: int, E_local: int) -> int:
     return int(load_library().moe_permute_workspace_bytes(T, top_k, E_local))
 
@@ -65,6 +86,25 @@ def moe_permute(topk_ids: torch.Tensor, E_local: int, x: torch.Tensor, x_scales:
                           row_align, capacity, _ptr(counts), _ptr(offsets), _ptr(row_to_assign),
                           _ptr(assign_to_row), _ptr(x_perm), _ptr(x_perm_scales), _ptr(workspace),
                           _ptr(error_flag), _stream(stream)), "moe_permute")
+
+
+def permute_args(topk_ids: torch.Tensor, E_local: int, x: torch.Tensor, x_scales: Optional[torch.Tensor],
+                 row_align: int, capacity: int, counts: torch.Tensor, offsets: torch.Tensor,
+                 row_to_assign: torch.Tensor, assign_to_row: torch.Tensor, x_perm: Optional[torch.Tensor],
+                 x_perm_scales: Optional[torch.Tensor], workspace: torch.Tensor,
+                 error_flag: torch.Tensor) -> PermuteArgs:
+    T, k = topk_ids.shape
+    return PermuteArgs(topk_ids=_ptr(topk_ids), T=T, top_k=k, E_local=E_local, x_dtype=act_dtype_code(x),
+                       x=_ptr(x), x_scales=_ptr(x_scales), H=x.shape[1], row_align=row_align, capacity=capacity,
+                       counts=_ptr(counts), offsets=_ptr(offsets), row_to_assign=_ptr(row_to_assign),
+                       assign_to_row=_ptr(assign_to_row), x_perm=_ptr(x_perm), x_perm_scales=_ptr(x_perm_scales),
+                       workspace=_ptr(workspace), error_flag=_ptr(error_flag))
+
+
+def moe_permute_batch(entries: Sequence[PermuteArgs], stream=None) -> None:
+    """moe_permute for several ops, one launch per pass (entries: PermuteArgs)."""
+    check(load_library().moe_permute_batch(_array(PermuteArgs, entries), len(entries), _stream(stream)),
+          "moe_permute_batch")
 
 
 def moe_ffn_row_align(phase: int, dtype: int) -> int:
@@ -112,6 +152,21 @@ def moe_combine(y_perm: torch.Tensor, assign_to_row: torch.Tensor, topk_w: torch
     return y
 
 
+def combine_args(y_perm: torch.Tensor, assign_to_row: torch.Tensor, topk_w: torch.Tensor, T: int, top_k: int,
+                 y: torch.Tensor) -> CombineArgs:
+    code = MOE_BF16 if y.dtype == torch.bfloat16 else MOE_F32 if y.dtype == torch.float32 else None
+    if code is None:
+        raise ValueError("y must be bf16 or f32")
+    return CombineArgs(y_perm=_ptr(y_perm), assign_to_row=_ptr(assign_to_row), topk_w=_ptr(topk_w), T=T,
+                       top_k=top_k, H=y_perm.shape[1], y_dtype=code, y=_ptr(y))
+
+
+def moe_combine_batch(entries: Sequence[CombineArgs], stream=None) -> None:
+    """moe_combine for several ops in one launch (entries: CombineArgs)."""
+    check(load_library().moe_combine_batch(_array(CombineArgs, entries), len(entries), _stream(stream)),
+          "moe_combine_batch")
+
+
 def moe_pack_weights(src: torch.Tensor, dst: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """[E, N, K] bf16 or fp8-code (uint8) row-major -> the FFN kernel's packed
     weight layout (same shape and size)."""
@@ -138,6 +193,7 @@ def status_string(status: int) -> str:
     return load_library().moe_status_string(status).decode()
 
 
-__all__ = ["moe_topk_route", "moe_permute_workspace_bytes", "moe_permute", "moe_ffn_row_align", "moe_ffn_tile_shape",
-           "moe_ffn_workspace_bytes", "moe_grouped_ffn_persistent", "moe_combine", "moe_pack_weights", "moe_x_moe",
-           "moe_decode_quota", "status_string", "OpDesc", "SchedConfig", "_lib"]
+__all__ = ["moe_topk_route", "moe_topk_route_batch", "moe_permute_workspace_bytes", "moe_permute", "moe_permute_batch",
+           "moe_ffn_row_align", "moe_ffn_tile_shape", "moe_ffn_workspace_bytes", "moe_grouped_ffn_persistent",
+           "moe_combine", "moe_combine_batch", "moe_pack_weights", "moe_x_moe", "moe_decode_quota", "status_string",
+           "route_args", "permute_args", "combine_args", "OpDesc", "SchedConfig", "_lib"]

@@ -1,8 +1,9 @@
 """Buffer plumbing around the four C-ABI calls for a set of MoE operations
 (layers x phases) that share one persistent FFN launch.  Allocates the
 capacity-sized buffers once (device memory comes from torch), then issues
-route -> permute for every op, one moe_grouped_ffn_persistent over all ops,
-and combine for every op, all on one stream.  No arithmetic happens here."""
+route -> permute for every op (one batched launch per pass), one
+moe_grouped_ffn_persistent over all ops, and one batched combine, all on one
+stream.  No arithmetic happens here."""
 from __future__ import annotations
 
 import ctypes as C
@@ -164,6 +165,14 @@ class MoEPipeline:
                                trace_capacity=trace_capacity, op_stats=self.stats.data_ptr(),
                                spin_limit=spin_limit, static_partition=int(static_partition))
         self.descs = [self._desc(i, b, fused_gather) for i, b in enumerate(self.bufs)]
+        self._route_args = [K.route_args(b.spec.logits, b.spec.top_k, b.spec.local_begin, b.spec.E_local, b.topk_ids,
+                                         b.topk_w) for b in self.bufs]
+        self._permute_args = [K.permute_args(b.topk_ids, b.spec.E_local, b.spec.x, b.spec.x_scales, b.row_align,
+                                             b.capacity, b.counts, b.offsets, b.row_to_assign, b.assign_to_row,
+                                             b.x_perm, b.x_perm_scales, b.perm_ws, self.error_flag)
+                              for b in self.bufs]
+        self._combine_args = [K.combine_args(b.y_perm, b.assign_to_row, b.topk_w, b.T, b.spec.top_k, b.y)
+                              for b in self.bufs]
         self.ffn_ws = torch.zeros((K.moe_ffn_workspace_bytes(self.descs, self.cfg),), dtype=torch.uint8, device=dev)
 
     @staticmethod
@@ -184,12 +193,20 @@ class MoEPipeline:
                       done_word=p(b.done_word))
 
     # ---------------------------------------------------------------- the four calls
-    def route(self, stream=None):
+    # Every op's route, permute and combine go out as one launch per pass
+    # (moe_*_batch); batched=False issues the per-op calls instead.
+    def route(self, stream=None, batched: bool = True):
+        if batched:
+            K.moe_topk_route_batch(self._route_args, stream)
+            return
         for b in self.bufs:
             s = b.spec
             K.moe_topk_route(s.logits, s.top_k, s.local_begin, s.E_local, b.topk_ids, b.topk_w, stream)
 
-    def permute(self, stream=None):
+    def permute(self, stream=None, batched: bool = True):
+        if batched:
+            K.moe_permute_batch(self._permute_args, stream)
+            return
         for b in self.bufs:
             s = b.spec
             K.moe_permute(b.topk_ids, s.E_local, s.x, s.x_scales, b.row_align, b.capacity, b.counts, b.offsets,
@@ -199,7 +216,10 @@ class MoEPipeline:
     def ffn(self, stream=None):
         K.moe_grouped_ffn_persistent(self.descs, self.cfg, self.ffn_ws, self.status, stream)
 
-    def combine(self, stream=None):
+    def combine(self, stream=None, batched: bool = True):
+        if batched:
+            K.moe_combine_batch(self._combine_args, stream)
+            return
         for b in self.bufs:
             K.moe_combine(b.y_perm, b.assign_to_row, b.topk_w, b.T, b.spec.top_k, b.y, stream=stream)
 

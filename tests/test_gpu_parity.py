@@ -567,3 +567,32 @@ def test_gathered_operand_argument_errors(dev):
         assert rc == _lib.MOE_ERR_INVALID_ARG, (kw, rc)
     torch.cuda.synchronize()
     assert int(pipe.status.item()) == 0
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_batched_calls_match_per_op_calls(dev, dtype):
+    """moe_topk_route_batch / moe_permute_batch / moe_combine_batch over the
+    ops of one launch (2 layers x 2 phases) give bitwise the results of the
+    per-op calls."""
+    from paper_2607_18002_amd.pipeline import MoEPipeline
+    base = 2 if dtype == "bf16" else 5
+    cfg = custom_config(base, cfg_id=710 + base, H=512, I=512, prefill_tokens=700, decode_tokens=90, E_global=64,
+                        E_local=12, top_k=6, zipf_s=(1.2, 0.7), n_layers=2)
+    specs = []
+    for layer in range(2):
+        s, _, _ = layer_specs(cfg, layer, dev)
+        specs += s
+    outs = []
+    for batched in (False, True):
+        pipe = MoEPipeline(specs, fused_gather=True)
+        pipe.route(batched=batched)
+        pipe.permute(batched=batched)
+        pipe.ffn()
+        pipe.combine(batched=batched)
+        torch.cuda.synchronize()
+        assert pipe.statuses() == (0, 0)
+        outs.append([(b.topk_ids.cpu(), b.topk_w.cpu(), b.counts.cpu(), b.offsets.cpu(), b.row_to_assign.cpu(),
+                      b.assign_to_row.cpu(), b.y.view(torch.int16).cpu()) for b in pipe.bufs])
+    for a, b in zip(*outs):
+        for ta, tb in zip(a, b):
+            assert torch.equal(ta, tb)
