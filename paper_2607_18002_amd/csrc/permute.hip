@@ -82,15 +82,19 @@ __device__ __forceinline__ void count_block(const int32_t* __restrict__ ids, int
         }
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < E; e += kThreads) blk_cnt[(size_t)blk * E + e] = hist[e];
     // Publish this block's counts, then take a ticket; the last block scans.
+    // The counts go out as device-coherent stores and every wave waits for its
+    // own before the barrier, so the ticket needs no fence: a device-scope fence
+    // here would write back the whole L2 of the XCD once per block.  The last
+    // block reads the counts with coherent loads for the same reason.
     // atomicInc wraps to 0 on the last ticket, so the counter is ready for the next call.
-    __threadfence();
+    for (int e = threadIdx.x; e < E; e += kThreads)
+        __hip_atomic_store(blk_cnt + (size_t)blk * E + e, hist[e], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    moeapk::wait_own_stores();
     __syncthreads();
     if (threadIdx.x == 0) s_last = atomicInc(ticket, (unsigned)(NB - 1)) == (unsigned)(NB - 1);
     __syncthreads();
     if (!s_last) return;
-    __threadfence();
 
     // Scan.  P threads per expert (the largest power of two with P*E <= 256, at
     // least 1); unit u = (e, j) sums chunks [j*R, (j+1)*R) of expert e.
@@ -106,11 +110,11 @@ __device__ __forceinline__ void count_block(const int32_t* __restrict__ ids, int
         for (; b + 8 <= b1; b += 8) {                          // eight independent loads in flight
             int c[8];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) c[i] = blk_cnt[(size_t)(b + i) * E + e];
+            for (int i = 0; i < 8; ++i) c[i] = moeapk::ld_relaxed_agent(blk_cnt + (size_t)(b + i) * E + e);
 #pragma unroll
             for (int i = 0; i < 8; ++i) sum += c[i];
         }
-        for (; b < b1; ++b) sum += blk_cnt[(size_t)b * E + e];
+        for (; b < b1; ++b) sum += moeapk::ld_relaxed_agent(blk_cnt + (size_t)b * E + e);
         part[u] = sum;
     }
     __syncthreads();
@@ -131,12 +135,12 @@ __device__ __forceinline__ void count_block(const int32_t* __restrict__ ids, int
         for (; b + 8 <= b1; b += 8) {
             int c[8];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) c[i] = blk_cnt[(size_t)(b + i) * E + e];
+            for (int i = 0; i < 8; ++i) c[i] = moeapk::ld_relaxed_agent(blk_cnt + (size_t)(b + i) * E + e);
 #pragma unroll
             for (int i = 0; i < 8; ++i) { blk_cnt[(size_t)(b + i) * E + e] = run; run += c[i]; }
         }
         for (; b < b1; ++b) {
-            const int c = blk_cnt[(size_t)b * E + e];
+            const int c = moeapk::ld_relaxed_agent(blk_cnt + (size_t)b * E + e);
             blk_cnt[(size_t)b * E + e] = run;
             run += c;
         }

@@ -1,12 +1,14 @@
 // a1: top-k softmax gating (Background, "MoE LLM Inference").
 //
-// One 64-wide wave per token.  Lane l holds experts l, l+64, ... as 64-bit
-// order keys: high half = the fp32 logit mapped to an unsigned integer that
-// orders like the float (-0.0 folded onto +0.0), low half = ~expert so that
-// equal logits prefer the lower expert index.  Each of the k rounds takes a
-// wave-wide max and retires the winner; lane j keeps slot j.  The wave-wide
-// reductions stay in the vector ALU: DPP quad permutes and row mirrors give
-// every lane its 16-lane row's result, four lane reads combine the rows.
+// One 64-wide wave per token.  Lane l holds experts l, l+64, ... as 32-bit
+// order keys: the fp32 logit mapped to an unsigned integer that orders like the
+// float (-0.0 folded onto +0.0; key 0 is kept for absent or retired experts).
+// Each of the k rounds takes the wave-wide maximum key with DPP max steps
+// inside each 16-lane row and four lane reads across the rows, then one ballot
+// per lane slot finds the experts holding that key: the lowest such expert
+// index wins (ties go to the lower index), is retired, and lane j keeps the
+// winner of round j.  Rounds are bound by vector-ALU issue (four cycles per
+// wave64 instruction), so keys stay 32 bits wide and the tie break is scalar.
 #include <cstring>
 
 #include "common.hpp"
@@ -15,16 +17,15 @@ namespace {
 
 constexpr int kTokensPerBlock = 4;  // one wave each
 
-__device__ __forceinline__ uint64_t order_key(float v, uint32_t e) {
+__device__ __forceinline__ uint32_t order_key(float v) {
     uint32_t u = __float_as_uint(v);
     if (u == 0x80000000u) u = 0u;                        // -0.0 ties with +0.0
-    uint32_t k = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-    return ((uint64_t)k << 32) | (uint64_t)(0xFFFFFFFFu - e);
+    const uint32_t k = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return k > 1u ? k : 1u;                              // only a NaN pattern maps below 1
 }
 
-__device__ __forceinline__ float key_value(uint64_t key) {
-    uint32_t k = (uint32_t)(key >> 32);
-    uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+__device__ __forceinline__ float key_value(uint32_t k) {
+    const uint32_t u = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
     return __uint_as_float(u);
 }
 
@@ -32,25 +33,23 @@ __device__ __forceinline__ float key_value(uint64_t key) {
 constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
 
 template <int CTRL>
-__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
-    const int lo = __builtin_amdgcn_mov_dpp((int)(uint32_t)v, CTRL, 0xF, 0xF, false);
-    const int hi = __builtin_amdgcn_mov_dpp((int)(uint32_t)(v >> 32), CTRL, 0xF, 0xF, false);
-    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
-}
-__device__ __forceinline__ uint64_t max64(uint64_t a, uint64_t b) { return a > b ? a : b; }
-__device__ __forceinline__ uint64_t readlane64(uint64_t v, int l) {
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, l);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), l);
-    return ((uint64_t)hi << 32) | lo;
+__device__ __forceinline__ uint32_t dpp_max(uint32_t v) {
+    const uint32_t o = (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, false);
+    return v > o ? v : o;
 }
 
 // Maximum of v over the wave, the same value in every lane.
-__device__ __forceinline__ uint64_t wave_max64(uint64_t v) {
-    v = max64(v, dpp64<kDppXor1>(v));
-    v = max64(v, dpp64<kDppXor2>(v));
-    v = max64(v, dpp64<kDppHalfMirror>(v));
-    v = max64(v, dpp64<kDppMirror>(v));                  // every lane: its row's maximum
-    return max64(max64(readlane64(v, 0), readlane64(v, 16)), max64(readlane64(v, 32), readlane64(v, 48)));
+__device__ __forceinline__ uint32_t wave_max(uint32_t v) {
+    v = dpp_max<kDppXor1>(v);
+    v = dpp_max<kDppXor2>(v);
+    v = dpp_max<kDppHalfMirror>(v);
+    v = dpp_max<kDppMirror>(v);                          // every lane: its row's maximum
+    const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
+    const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
+    const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
+    const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+    const uint32_t a = r0 > r1 ? r0 : r1, b = r2 > r3 ? r2 : r3;
+    return a > b ? a : b;
 }
 
 // Sum of v over the wave, the same value in every lane.
@@ -78,28 +77,33 @@ __device__ __forceinline__ void route_block(const float* __restrict__ logits, in
     float v[EPL];
 #pragma unroll
     for (int i = 0; i < EPL; ++i) v[i] = row[min(lane + 64 * i, E - 1)];
-    uint64_t key[EPL];
+    uint32_t key[EPL];
 #pragma unroll
-    for (int i = 0; i < EPL; ++i) {
-        const int e = lane + 64 * i;
-        key[i] = (e < E) ? order_key(v[i], (uint32_t)e) : 0ull;
-    }
+    for (int i = 0; i < EPL; ++i) key[i] = (lane + 64 * i < E) ? order_key(v[i]) : 0u;
     int my_e = -1;
-    float my_v = 0.f;
+    uint32_t my_key = 0;
     for (int r = 0; r < k; ++r) {
-        uint64_t best = 0;
+        uint32_t best = key[0];
 #pragma unroll
-        for (int i = 0; i < EPL; ++i) best = key[i] > best ? key[i] : best;
-        best = wave_max64(best);
-        const int e = (int)(0xFFFFFFFFu - (uint32_t)best);
+        for (int i = 1; i < EPL; ++i) best = key[i] > best ? key[i] : best;
+        best = wave_max(best);
+        // lowest expert index holding the maximum: the first slot with a hit, its lowest lane
+        int e = 0;
+#pragma unroll
+        for (int i = EPL - 1; i >= 0; --i) {
+            const uint64_t hit = __ballot(key[i] == best);
+            if (hit) e = 64 * i + __ffsll((long long)hit) - 1;
+        }
+        const int wl = e & 63, wi = e >> 6;
 #pragma unroll
         for (int i = 0; i < EPL; ++i)
-            if (lane + 64 * i == e) key[i] = 0ull;       // retire the winner
+            if (i == wi && lane == wl) key[i] = 0u;      // retire the winner
         if (lane == r) {
             my_e = e;
-            my_v = key_value(best);
+            my_key = best;
         }
     }
+    const float my_v = key_value(my_key);
     const float m = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_v), 0));   // the largest selected logit
     const float ex = (lane < k) ? expf(my_v - m) : 0.f;
     const float s = wave_sum(ex);
