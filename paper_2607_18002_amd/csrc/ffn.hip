@@ -18,7 +18,10 @@
 // operation's tiles are numbered GEMM-1 tiles first (row-tile major), then
 // GEMM-2 tiles; a GEMM-2 tile waits (bounded) on a per-row-tile counter that
 // GEMM-1 tiles bump once their h rows are visible.  Every claimed tile belongs
-// to a running workgroup, so the dependency waits cannot deadlock.
+// to a running workgroup, so the dependency waits cannot deadlock.  Commits
+// are counted with atomics whose result nobody waits for; an operation whose
+// polled count of committed tiles reached its total is finished by the
+// workgroup that wins its ACTIVE -> FINISHING transition.
 //
 // Coherence across the eight XCD-private L2 caches.  An agent-scope acquire
 // invalidates the whole L2 of the XCD, which would destroy weight reuse if it
@@ -33,7 +36,7 @@
 // boundaries make earlier launches' copies coherent).  Row-tile tables, which
 // are written with ordinary stores, are published with a release by every
 // wave that wrote them.  The one acquire per operation is taken by the
-// workgroup that completes it, before it publishes the done word.
+// workgroup that finishes it, before it publishes the done word.
 #include <cstring>
 
 #include "tile_bf16.hpp"
@@ -57,7 +60,7 @@ constexpr int kMaxRowTiles = 1 << 14;      // per op (14-bit field of a table en
 constexpr int kSegAlign = 32;
 
 enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1, CLS_FP8 = 2 };
-enum : int32_t { ST_WAIT = 0, ST_INIT = 1, ST_ACTIVE = 2, ST_DONE = 3 };
+enum : int32_t { ST_WAIT = 0, ST_INIT = 1, ST_ACTIVE = 2, ST_DONE = 3, ST_FINISHING = 4 };
 enum : int32_t { CMD_EXIT = 0, CMD_TILE = 1, CMD_INST = 2, CMD_IDLE = 3 };
 
 struct OpArg {
@@ -94,8 +97,10 @@ struct KArgs {
 };
 
 // Run-time state of an op: every access is an atomic (one L2 line per op).
+// left: -(tiles not yet committed) once the op is instantiated, counting up to
+// 0 with one increment per commit; INT_MIN before, so a stale read is never 0.
 struct OpDyn {
-    int32_t state, pad_a, done, x_moe;
+    int32_t state, pad_a, left, x_moe;
     int32_t total, pad_b, quota, pad0;
     unsigned long long t_ready, t_first, t_done;
     char pad[128 - 56];
@@ -207,6 +212,7 @@ __global__ __launch_bounds__(256) void apk_init_kernel(const InitArgs a) {
             st[o].rel_word = a.rel_words[o];
             st[o].rel_after = a.rel_after[o];
             st[o].gap = a.gaps[o];
+            dyn_of(a.ws)[o].left = INT32_MIN;
         }
         *a.status = MOE_OK;
     }
@@ -329,34 +335,39 @@ __device__ void finish_op(const KArgs& a, int o, int total) {
 // (wave 0, one op per lane; lane 0 also the header words).  A workgroup
 // coming out of a tile issues them right after its K loop, so that their
 // round trip overlaps the epilogue; they are then older than the boundary by
-// the epilogue's duration.
+// the epilogue's duration.  The raw values are kept (lanes past n_ops read op
+// 0) and masked only at the boundary: any arithmetic on them where they are
+// issued would make the wave wait for their round trip there.
 struct Polls {
-    int state, own_claim, own_size, total, phase, stop, q;
+    int state, own_claim, own_size, left, phase, stop, q;
     uint32_t abort_v;
 };
 
 __device__ __forceinline__ Polls issue_polls(const KArgs& a) {
     const int lane = threadIdx.x;
-    const bool has = lane < a.n_ops;
-    const int o_l = has ? lane : 0;
+    const int o_l = lane < a.n_ops ? lane : 0;
     const OpDyn* dyn = dyn_of(a.ws);
     const XQueue* own = xq_of(a.ws, o_l, xcc_id());
     const Hdr* hdr = hdr_of(a.ws);
-    // every load unconditional (lanes past n_ops read op 0), results selected after
-    const int st = ld_relaxed_agent(&dyn[o_l].state);
-    const int cl = ld_relaxed_agent(&own->claim);
-    const int sz = ld_relaxed_agent(&own->size);
-    const int tot = ld_relaxed_agent(&dyn[o_l].total);
-    const int ph = static_of(a.ws)[o_l].phase;
     Polls p;
+    p.state = ld_relaxed_agent(&dyn[o_l].state);
+    p.own_claim = ld_relaxed_agent(&own->claim);
+    p.own_size = ld_relaxed_agent(&own->size);
+    p.left = ld_relaxed_agent(&dyn[o_l].left);
+    p.phase = static_of(a.ws)[o_l].phase;
     p.stop = ld_relaxed_agent(&hdr->stop);
     p.q = ld_relaxed_agent(&hdr->quota);
     p.abort_v = a.abort_word ? __hip_atomic_load(a.abort_word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) : 0u;
-    p.state = has ? st : ST_DONE;
-    p.own_claim = has ? cl : 0;
-    p.own_size = has ? sz : 0;
-    p.total = has ? tot : 0;
-    p.phase = has ? ph : 0;
+    return p;
+}
+
+// At the boundary: lanes past n_ops hold no op.
+__device__ __forceinline__ Polls mask_polls(const KArgs& a, Polls p) {
+    if ((int)threadIdx.x >= a.n_ops) {
+        p.state = ST_DONE;
+        p.own_claim = p.own_size = 0;
+        p.left = INT32_MIN;
+    }
     return p;
 }
 
@@ -474,11 +485,13 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
     if (have_prev) prev = *cmd;
     if (lane == 0) cmd->pre_next = -1;
     const unsigned long long t_boundary = wall_ticks();
-    const Polls pl = have_pre ? pre : issue_polls(a);
+    const Polls pl = mask_polls(a, have_pre ? pre : issue_polls(a));
 
-    // 1. commit: count the tile (its device-coherent stores have completed);
-    //    the completion count is read in finish_prev, after the claim
-    int done_after = -1;
+    // 1. commit: count the tile (its device-coherent stores have completed).
+    //    Both counters are bumped with atomics whose result is not used, so the
+    //    boundary never waits for their round trip; whether the op is complete
+    //    is read from the polled counts (step 2b), by whichever workgroup
+    //    first sees them full.
     unsigned long long t_end = 0;
     if (have_prev && lane == 0) {
         t_end = wall_ticks();
@@ -486,13 +499,11 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
             int32_t* g1 = (int32_t*)(arr_of(a.ws) + a.op[prev.op].g1_off);
             __hip_atomic_fetch_add(g1 + prev.mtile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        done_after = add_relaxed_agent(&dyn[prev.op].done, 1) + 1;
+        __hip_atomic_fetch_add(&dyn[prev.op].left, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    const int prev_total = __shfl(pl.total, have_prev ? prev.op : 0, 64);
-    // 3. finish the previous tile's op if that tile was its last; trace it
+    // 3. trace the previous tile
     auto finish_prev = [&]() {
         if (have_prev && lane == 0) {
-            if (done_after == prev_total) finish_op(a, prev.op, prev_total);
             if (a.trace) {
                 const int idx = add_relaxed_agent(&hdr->trace_count, 1);
                 if (idx < a.trace_cap) {
@@ -508,7 +519,8 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
     };
 
     // 2. stop conditions (polled)
-    const int state = pl.state, own_claim = pl.own_claim, own_size = pl.own_size;
+    int state = pl.state;
+    const int own_claim = pl.own_claim, own_size = pl.own_size;
     const int o_l = lane < a.n_ops ? lane : 0;
     const int phase = pl.phase;
     const int myx = xcc_id();
@@ -532,8 +544,24 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
         return;
     }
     const int q = __shfl(pl.q, 0, 64);
+    // 2b. an op whose every tile had committed when polled is finished by the
+    //     workgroup that wins its ACTIVE -> FINISHING transition (left only
+    //     grows and is 0 only once the last tile committed, so a stale poll can
+    //     only delay this, never fire it early)
+    const uint64_t fmask = __ballot(state == ST_ACTIVE && pl.left == 0);
+    if (fmask) {
+        int won = 0;
+        if ((fmask >> lane) & 1) won = atomicCAS(&dyn[lane].state, ST_ACTIVE, ST_FINISHING) == ST_ACTIVE;
+        uint64_t wmask = __ballot(won);
+        while (wmask) {                                              // wave-uniform loop
+            const int o = __ffsll((long long)wmask) - 1;
+            wmask &= wmask - 1;
+            if (lane == 0) finish_op(a, o, ld_relaxed_agent(&dyn[o].total));
+        }
+        if ((fmask >> lane) & 1) state = ST_DONE;                   // finished here or by its winner
+    }
     if (__ballot(state != ST_DONE) == 0) {
-        // every op was DONE when polled; an op the previous tile completes is finished below
+        // every op was DONE when polled (or was finished just above)
         finish_prev();
         if (lane == 0) cmd->kind = CMD_EXIT;
         return;
@@ -711,6 +739,9 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
             __hip_atomic_store(&hdr->quota, qd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         __hip_atomic_store(&d->x_moe, xm, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        // the commit counter is set before any queue can hand out a tile
+        __hip_atomic_store(&d->total, xm * (op.n1 + op.n2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&d->left, -(xm * (op.n1 + op.n2)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         for (int x = 0; x < kXcds; ++x) {                      // contiguous row-tile ranges, cut between groups
             XQueue* qx = xq_of(a.ws, o, x);
             const int lo = x == 0 ? 0 : s_cut[x], hi = x + 1 == kXcds ? xm : s_cut[x + 1];
@@ -718,7 +749,6 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
             __hip_atomic_store(&qx->n_mt, hi - lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_store(&qx->size, (hi - lo) * (op.n1 + op.n2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
-        __hip_atomic_store(&d->total, xm * (op.n1 + op.n2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(&d->quota, qd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(&d->t_ready, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (xm == 0) {                                   // nothing routed here: done at once

@@ -112,11 +112,13 @@ def test_decode_quota_under_contention(dev):
     """While prefill still has unclaimed tiles, decode tiles run only on
     workgroups below q'.  Only decode tiles whose claim decision was taken
     after prefill became claimable count: before that, decode was the lone
-    active phase and every workgroup may take it (both ops can become ready
-    at the same moment when the launch starts late against the release time)."""
+    active phase and every workgroup may take it.  Decode is released 40 us
+    after the launch, well past the workgroups' first boundaries, so prefill is
+    claimable first (a release inside the launch-start window can let decode be
+    instantiated first and be claimed whole as the lone phase)."""
     cfg = custom_config(2, cfg_id=404, H=1024, I=1024, prefill_tokens=8192, decode_tokens=256, E_global=64,
                         E_local=16, top_k=8)
-    specs, _, _ = layer_specs(cfg, 0, dev, decode=dict(release_after_ns=5_000))
+    specs, _, _ = layer_specs(cfg, 0, dev, decode=dict(release_after_ns=40_000))
     pipe = _pipe(dev, specs, trace_capacity=1 << 17, decode_quota_wg=64)
     assert pipe.statuses() == (0, 0)
     tr = pipe.trace_records()
