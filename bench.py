@@ -2,13 +2,14 @@
 """Benchmark of the routed-expert MoE hot path on one MI355X.
 
 A step is one pass of the whole path over one batch: moe_topk_route and
-moe_permute for every operation, ONE moe_grouped_ffn_persistent launch over
-all operations, and moe_combine for every operation.  The default workload is
+moe_permute over every operation (one batched launch each), ONE
+moe_grouped_ffn_persistent launch over all operations, and moe_combine over
+every operation (one batched launch).  The default workload is
 the mixed prefill+decode configuration: 4 layers x (8192 prefill + 1024 decode
 tokens), 32 of 256 experts local, top-8, hidden 3072, expert intermediate
 1536, bf16, in one persistent launch; decode layer 0 is released 10 us after
 the launch starts, each later layer of a phase when that phase's previous
-layer is done (+20 us for decode), decode quota 64 of 256 workgroups.
+layer is done (+20 us for decode), decode quota 80 of 256 workgroups.
 
 Prints ONE JSON line.  value = routed-expert TFLOP/s of the whole step
 (6*H*I flop per local routed row).  roofline = the persistent FFN kernel
@@ -45,7 +46,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=4, help="workload configuration (1-5); default 4")
-    ap.add_argument("--quota", type=int, default=64, help="decode quota q in workgroups")
+    ap.add_argument("--quota", type=int, default=80, help="decode quota q in workgroups")
     ap.add_argument("--group-row-tiles", type=int, default=0,
                     help="most row tiles of one expert that share each weight slice fetch (0 = library default)")
     ap.add_argument("--gather", choices=("fused", "copy"), default="fused",
