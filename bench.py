@@ -47,6 +47,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=4, help="workload configuration (1-5); default 4")
     ap.add_argument("--quota", type=int, default=80, help="decode quota q in workgroups")
+    ap.add_argument("--fused-combine", action="store_true",
+                    help="combine tiles inside the persistent kernel instead of a separate combine launch")
     ap.add_argument("--group-row-tiles", type=int, default=0,
                     help="most row tiles of one expert that share each weight slice fetch (0 = library default)")
     ap.add_argument("--gather", choices=("fused", "copy"), default="fused",
@@ -218,7 +220,7 @@ def main():
     specs, layers = build_specs(cfg, dev)
     t_gen = time.perf_counter() - t_gen
     fused = args.gather == "fused"
-    pipe = MoEPipeline(specs, decode_quota_wg=args.quota, fused_gather=fused,
+    pipe = MoEPipeline(specs, decode_quota_wg=args.quota, fused_gather=fused, fused_combine=args.fused_combine,
                        group_row_tiles=args.group_row_tiles)
     stream = torch.cuda.current_stream()
 
@@ -247,7 +249,7 @@ def main():
 
     flops, abytes, rows = algorithmic_work(pipe, cfg)
     # one more launch with the per-tile trace for the decode latency figures
-    traced = MoEPipeline(specs, decode_quota_wg=args.quota, trace_capacity=1 << 18, fused_gather=fused,
+    traced = MoEPipeline(specs, decode_quota_wg=args.quota, trace_capacity=1 << 18, fused_gather=fused, fused_combine=args.fused_combine,
                          group_row_tiles=args.group_row_tiles)
     traced.run()
     torch.cuda.synchronize()
@@ -263,7 +265,7 @@ def main():
     excl = None
     dec_specs = phase_subset(specs, 1)
     if lat is not None and dec_specs and len(dec_specs) < len(specs):
-        alone = MoEPipeline(dec_specs, decode_quota_wg=args.quota, trace_capacity=1 << 16, fused_gather=fused,
+        alone = MoEPipeline(dec_specs, decode_quota_wg=args.quota, trace_capacity=1 << 16, fused_gather=fused, fused_combine=args.fused_combine,
                             group_row_tiles=args.group_row_tiles)
         alone.run()
         alone.run()
@@ -330,7 +332,7 @@ def main():
                    "experts_local": cfg.E_local, "experts_global": cfg.E_global, "top_k": cfg.top_k,
                    "hidden": cfg.H, "intermediate": cfg.I, "decode_quota_wg": args.quota,
                    "group_row_tiles": args.group_row_tiles,
-                   "gather": args.gather, "local_rows": rows},
+                   "gather": args.gather, "combine": "fused" if args.fused_combine else "separate", "local_rows": rows},
         "hbm_gbps_alg": round(abytes / (ffn_ms * 1e-3) / 1e9, 1),
         "ffn_tflops": round(flops / (ffn_ms * 1e-3) / 1e12, 2),
         "decode_tile_latency": lat,

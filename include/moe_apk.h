@@ -217,7 +217,23 @@ typedef struct moe_op_desc {
     const void*  x;               /* [T, H] activations (bf16 or fp8 codes), or NULL    */
     const float* x_scales;        /* [T, H/128]                   fp8 only            */
     const int32_t* row_to_assign; /* [capacity] from moe_permute                       */
-    int32_t T, top_k;             /* rows of x; slots per token                         */
+    int32_t T, top_k;             /* tokens (rows of x); slots per token                */
+    /* Fused combine (Adaptive Persistent Kernel; Evaluation, "Implementation":
+     * the MoE data post-processing fused into the persistent kernel).  With y
+     * set, once every GEMM tile of the op has committed the kernel runs the
+     * op's combine tiles (32 tokens each): y[t] = sum over the token's local
+     * slots j, ascending, of topk_w[t,j] * y_perm[assign_to_row[t*top_k+j]],
+     * accumulated in fp32 exactly as moe_combine does (so the two agree bit for
+     * bit); tokens with no local slot get zeros.  The op completes (done word,
+     * dependants, t_done) only after its combine tiles.  y is written with
+     * device-coherent stores.  An assign_to_row entry >= capacity sets
+     * MOE_ERR_INTERNAL and is skipped.  With y NULL the caller runs
+     * moe_combine after the launch.                                            */
+    const int32_t* assign_to_row; /* [T*top_k] from moe_permute (-1: slot not local)  */
+    const float* topk_w;          /* [T, top_k] from moe_topk_route                   */
+    void* y;                      /* [T, H] out, or NULL                              */
+    moe_dtype_t y_dtype;          /* MOE_BF16 or MOE_F32                              */
+    int32_t reserved_c;           /* 0                                                 */
 } moe_op_desc;
 
 /* Per-tile trace record (times in device wall-clock ticks, 100 MHz on gfx950).

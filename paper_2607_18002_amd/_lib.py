@@ -40,6 +40,7 @@ class OpDesc(C.Structure):
         ("depends_on_op", _i32), ("weight_layout", _i32), ("gap_ns", _i64),
         ("done_word", _p),
         ("x", _p), ("x_scales", _p), ("row_to_assign", _p), ("T", _i32), ("top_k", _i32),
+        ("assign_to_row", _p), ("topk_w", _p), ("y", _p), ("y_dtype", _i32), ("reserved_c", _i32),
     ]
 
 

@@ -21,7 +21,10 @@
 // to a running workgroup, so the dependency waits cannot deadlock.  Commits
 // are counted with atomics whose result nobody waits for; an operation whose
 // polled count of committed tiles reached its total is finished by the
-// workgroup that wins its ACTIVE -> FINISHING transition.
+// workgroup that wins its ACTIVE -> FINISHING transition.  An op with a fused
+// combine turns COMBINING once its GEMM tiles have all committed; its combine
+// tiles (weighted sums of y_perm rows back into token order) are then claimed
+// from one shared counter, and it finishes after the last of them.
 //
 // Coherence across the eight XCD-private L2 caches.  An agent-scope acquire
 // invalidates the whole L2 of the XCD, which would destroy weight reuse if it
@@ -60,7 +63,8 @@ constexpr int kMaxRowTiles = 1 << 14;      // per op (14-bit field of a table en
 constexpr int kSegAlign = 32;
 
 enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1, CLS_FP8 = 2 };
-enum : int32_t { ST_WAIT = 0, ST_INIT = 1, ST_ACTIVE = 2, ST_DONE = 3, ST_FINISHING = 4 };
+enum : int32_t { ST_WAIT = 0, ST_INIT = 1, ST_ACTIVE = 2, ST_DONE = 3, ST_FINISHING = 4, ST_COMBINING = 5 };
+constexpr int kCombTokens = 32;           // tokens per fused-combine tile
 enum : int32_t { CMD_EXIT = 0, CMD_TILE = 1, CMD_INST = 2, CMD_IDLE = 3 };
 
 struct OpArg {
@@ -77,7 +81,11 @@ struct OpArg {
     float* hs;
     uint32_t* done_word;
     const int32_t* rmap;       // gathered GEMM-1 operand: row -> assignment (x row = assignment / top_k), else NULL
+    const int32_t* a2r;        // fused combine: assignment -> row, topk weights, output (y NULL: none)
+    const float* tw;
+    void* yc;
     int32_t cls, phase, layer, E, H, I, capacity, mt, n1, n2, max_mtiles, table_off, g1_off, grp_off, T, top_k;
+    int32_t ct, ck, y_f32, n3;  // combine: tokens, slots per token, fp32 output, combine tiles
 };
 
 struct KArgs {
@@ -99,8 +107,11 @@ struct KArgs {
 // Run-time state of an op: every access is an atomic (one L2 line per op).
 // left: -(tiles not yet committed) once the op is instantiated, counting up to
 // 0 with one increment per commit; INT_MIN before, so a stale read is never 0.
+// With a fused combine the count holds the GEMM tiles and the n3 combine tiles:
+// it passes -n3 when the last GEMM tile commits (ACTIVE -> COMBINING) and 0
+// when the last combine tile does.  cclaim: the combine tiles' claim counter.
 struct OpDyn {
-    int32_t state, pad_a, left, x_moe;
+    int32_t state, cclaim, left, x_moe;
     int32_t total, pad_b, quota, pad0;
     unsigned long long t_ready, t_first, t_done;
     char pad[128 - 56];
@@ -286,6 +297,91 @@ __device__ __forceinline__ void run_tile(const OpArg& op, int stage, int row0, i
         run_tile_cls<ShapeD, false>(op, stage, row0, rows32, nb, e, lds, hook);
 }
 
+// ----------------------------------------------------------------------------- fused combine
+// Combine tile t of an op: tokens [t * kCombTokens, ...), 8 per pass, 32 threads
+// per token, each thread H/256 16-byte vectors of the token's row (loads of all
+// its vectors for one slot are issued together).  Per token and column the
+// arithmetic is moe_combine's: fp32 fmaf over the local slots in ascending
+// order, then one rounding to the output type.  Outputs are written with
+// device-coherent stores, like the tiles' outputs.
+constexpr int kCombVec = 6;
+
+__device__ __forceinline__ void st_dev16(void* p, uint4 v) {
+    uint64_t* q = (uint64_t*)p;
+    __hip_atomic_store(q, (uint64_t)v.x | ((uint64_t)v.y << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(q + 1, (uint64_t)v.z | ((uint64_t)v.w << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ void run_combine(const OpArg& op, int t, char* lds, int32_t* status) {
+    const int tid = threadIdx.x;
+    const int k = op.ck;
+    const int tok0 = t * kCombTokens;
+    const int ntok = min(kCombTokens, op.ct - tok0);
+    int32_t* srow = (int32_t*)lds;                                     // [kCombTokens][k] rows
+    float* sw = (float*)(lds + kCombTokens * 32 * sizeof(int32_t));     // [kCombTokens][k] weights
+    for (int i = tid; i < ntok * k; i += 256) {
+        int r = op.a2r[(size_t)tok0 * k + i];
+        if (r >= op.capacity) {
+            set_status(status, MOE_ERR_INTERNAL);
+            r = -1;
+        }
+        srow[i] = r;
+        sw[i] = op.tw[(size_t)tok0 * k + i];
+    }
+    __syncthreads();
+    const int vecs = op.H >> 3, nv = op.H >> 8, sub = tid & 31;
+    const uint4* yp = (const uint4*)op.y;
+    for (int p = 0; p < ntok; p += 8) {
+        const int tt = p + (tid >> 5);
+        if (tt >= ntok) continue;
+        for (int u0 = 0; u0 < nv; u0 += kCombVec) {
+            float acc[kCombVec][8];
+#pragma unroll
+            for (int u = 0; u < kCombVec; ++u)
+#pragma unroll
+                for (int i = 0; i < 8; ++i) acc[u][i] = 0.f;
+            for (int j = 0; j < k; ++j) {
+                const int r = srow[tt * k + j];
+                if (r < 0) continue;
+                const float wj = sw[tt * k + j];
+                uint4 q[kCombVec];
+#pragma unroll
+                for (int u = 0; u < kCombVec; ++u)
+                    if (u0 + u < nv) q[u] = yp[(size_t)r * vecs + (u0 + u) * 32 + sub];
+#pragma unroll
+                for (int u = 0; u < kCombVec; ++u) {
+                    if (u0 + u >= nv) continue;
+                    const uint32_t w4[4] = {q[u].x, q[u].y, q[u].z, q[u].w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        acc[u][2 * i] = fmaf(wj, bf_bits2f(w4[i] & 0xFFFFu), acc[u][2 * i]);
+                        acc[u][2 * i + 1] = fmaf(wj, bf_bits2f(w4[i] >> 16), acc[u][2 * i + 1]);
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kCombVec; ++u) {
+                if (u0 + u >= nv) continue;
+                const size_t v = (size_t)(tok0 + tt) * vecs + (u0 + u) * 32 + sub;
+                if (op.y_f32) {
+                    float* out = (float*)op.yc + v * 8;
+                    st_dev16(out, make_uint4(__float_as_uint(acc[u][0]), __float_as_uint(acc[u][1]),
+                                             __float_as_uint(acc[u][2]), __float_as_uint(acc[u][3])));
+                    st_dev16(out + 4, make_uint4(__float_as_uint(acc[u][4]), __float_as_uint(acc[u][5]),
+                                                 __float_as_uint(acc[u][6]), __float_as_uint(acc[u][7])));
+                } else {
+                    uint4 o;
+                    o.x = f2bf_bits(acc[u][0]) | (f2bf_bits(acc[u][1]) << 16);
+                    o.y = f2bf_bits(acc[u][2]) | (f2bf_bits(acc[u][3]) << 16);
+                    o.z = f2bf_bits(acc[u][4]) | (f2bf_bits(acc[u][5]) << 16);
+                    o.w = f2bf_bits(acc[u][6]) | (f2bf_bits(acc[u][7]) << 16);
+                    st_dev16((uint4*)op.yc + v, o);
+                }
+            }
+        }
+    }
+}
+
 // ----------------------------------------------------------------------------- scheduler
 // Per-workgroup LDS copy of each op's own-XCD queue (wave 0 only), taken at the
 // workgroup's first claim from that queue -- after the claim atomic returned, so
@@ -458,6 +554,19 @@ __device__ bool take_tile(const KArgs& a, int o, int src, int t, int myx, TabCac
     return more;
 }
 
+// Wave 0: combine tile t of op o (stage 3) into the command block.
+__device__ void take_combine(int o, int t, Cmd* cmd, unsigned long long t_boundary, unsigned long long now) {
+    if (threadIdx.x == 0) {
+        cmd->kind = CMD_TILE; cmd->op = o; cmd->stage = 3; cmd->t = t;
+        cmd->e = -1; cmd->mblk = 0; cmd->row0 = 0; cmd->rows = 0; cmd->rows32 = 0; cmd->nb = 0; cmd->mtile = -1;
+        cmd->pre_next = -1;
+        cmd->t_boundary = t_boundary;
+        cmd->t_polled = now;
+        cmd->t_claim = wall_ticks();
+        cmd->t_start = cmd->t_claim;
+    }
+}
+
 // Whether a workgroup may claim its next tile of an op of this phase ahead,
 // during the current tile: only in its preferred phase (decode below q', or
 // any workgroup when the launch holds no prefill op), and for prefill only if
@@ -472,8 +581,9 @@ __device__ __forceinline__ int phase_of(const KArgs& a, int o) { return a.op[o].
 // the polled words (pre, issued after the previous tile's K loop, when
 // have_pre; else read now), claim, and only then wait for the commit's
 // completion count, so the commit and the claim share one round trip.
+template <bool COMB>
 __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool have_prev, int64_t& idle,
-                         TabCache* tab, bool have_pre, Polls pre, int pre_t) {
+                         TabCache* tab, bool have_pre, Polls pre, int pre_t, const int32_t* n3s) {
     const int lane = threadIdx.x;
     Hdr* hdr = hdr_of(a.ws);
     OpDyn* dyn = dyn_of(a.ws);
@@ -548,10 +658,16 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
     //     workgroup that wins its ACTIVE -> FINISHING transition (left only
     //     grows and is 0 only once the last tile committed, so a stale poll can
     //     only delay this, never fire it early)
-    const uint64_t fmask = __ballot(state == ST_ACTIVE && pl.left == 0);
-    if (fmask) {
+    //     With a fused combine, the op's GEMM tiles are all committed when left
+    //     reaches -n3: then it turns COMBINING, and its combine tiles can be
+    //     claimed (every y_perm row they read was stored before its commit).
+    const int n3_l = COMB && lane < a.n_ops ? n3s[lane] : 0;
+    const uint64_t fmask = __ballot(pl.left == 0 && ((state == ST_ACTIVE && n3_l == 0) || (COMB && state == ST_COMBINING)));
+    const uint64_t cmask = COMB ? __ballot(state == ST_ACTIVE && n3_l > 0 && pl.left == -n3_l) : 0ull;
+    if (fmask | cmask) {
         int won = 0;
-        if ((fmask >> lane) & 1) won = atomicCAS(&dyn[lane].state, ST_ACTIVE, ST_FINISHING) == ST_ACTIVE;
+        if ((fmask >> lane) & 1) won = atomicCAS(&dyn[lane].state, state, ST_FINISHING) == state;
+        if (COMB && ((cmask >> lane) & 1)) atomicCAS(&dyn[lane].state, ST_ACTIVE, ST_COMBINING);
         uint64_t wmask = __ballot(won);
         while (wmask) {                                              // wave-uniform loop
             const int o = __ffsll((long long)wmask) - 1;
@@ -559,6 +675,7 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
             if (lane == 0) finish_op(a, o, ld_relaxed_agent(&dyn[o].total));
         }
         if ((fmask >> lane) & 1) state = ST_DONE;                   // finished here or by its winner
+        if (COMB && ((cmask >> lane) & 1)) state = ST_COMBINING;    // turned here or by another workgroup
     }
     if (__ballot(state != ST_DONE) == 0) {
         // every op was DONE when polled (or was finished just above)
@@ -610,7 +727,8 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
 
     // 5. claim: decode first on workgroups below q', prefill first elsewhere;
     //    within a phase: the own XCD's queue first, then steal from the others
-    const bool active = state == ST_ACTIVE;
+    const bool active = state == ST_ACTIVE || (COMB && state == ST_COMBINING);
+    const uint64_t combining = COMB ? __ballot(state == ST_COMBINING) : 0ull;
     const uint64_t dmask = __ballot(active && phase == MOE_DECODE);
     const uint64_t pmask = __ballot(active && phase == MOE_PREFILL);
     const uint64_t own_avail = __ballot(active && own_claim < own_size);
@@ -622,6 +740,15 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
             const int o = __ffsll((long long)m) - 1;
             m &= m - 1;
             int src = -1, t = 0;
+            if (COMB && ((combining >> o) & 1)) {                   // one shared queue of combine tiles
+                if (lane == 0) t = atomicAdd(&dyn[o].cclaim, 1);
+                t = __shfl(t, 0, 64);
+                if (t >= n3s[o]) continue;
+                finish_prev();
+                take_combine(o, t, cmd, t_boundary, now);
+                idle = 0;
+                return;
+            }
             if ((own_avail >> o) & 1) {                             // own queue
                 if (lane == 0) t = atomicAdd(&xq_of(a.ws, o, myx)->claim, 1);
                 t = __shfl(t, 0, 64);
@@ -740,8 +867,8 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
         }
         __hip_atomic_store(&d->x_moe, xm, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         // the commit counter is set before any queue can hand out a tile
-        __hip_atomic_store(&d->total, xm * (op.n1 + op.n2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(&d->left, -(xm * (op.n1 + op.n2)), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&d->total, xm * (op.n1 + op.n2) + op.n3, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(&d->left, -(xm * (op.n1 + op.n2) + op.n3), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         for (int x = 0; x < kXcds; ++x) {                      // contiguous row-tile ranges, cut between groups
             XQueue* qx = xq_of(a.ws, o, x);
             const int lo = x == 0 ? 0 : s_cut[x], hi = x + 1 == kXcds ? xm : s_cut[x + 1];
@@ -753,22 +880,31 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
         __hip_atomic_store(&d->t_ready, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (xm == 0) {                                   // nothing routed here: done at once
             __hip_atomic_store(&d->t_first, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            finish_op(a, o, 0);
+            if (op.n3 > 0) st_release_agent(&d->state, (int32_t)ST_COMBINING);   // its combine writes zeros
+            else finish_op(a, o, 0);
         } else {
             st_release_agent(&d->state, (int32_t)ST_ACTIVE);   // table entries written before this
         }
     }
 }
 
+// COMB: some op of the launch has a fused combine (a separate instance, so the
+// plain kernel's register allocation does not carry the combine path).
+template <bool COMB>
 __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
     extern __shared__ __align__(16) char lds[];
     __shared__ Cmd cmd;
     __shared__ int32_t scan[1024];
     __shared__ unsigned long long s_t0;
     __shared__ TabCache tab;
+    __shared__ int32_t s_n3[MOE_MAX_OPS];                     // combine tiles per op
     const int tid = threadIdx.x;
     const int wg = blockIdx.x;
-    if (tid < MOE_MAX_OPS) { tab.lo[tid] = -1; tab.cnt[tid] = 0; }
+    if (tid < MOE_MAX_OPS) {
+        tab.lo[tid] = -1;
+        tab.cnt[tid] = 0;
+        s_n3[tid] = tid < a.n_ops ? a.op[tid].n3 : 0;
+    }
     if (tid == 0) {
         const unsigned long long now = wall_ticks();
         const unsigned long long prev = atomicCAS(&hdr_of(a.ws)->t0, 0ull, now);
@@ -778,13 +914,15 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
     const uint64_t t0 = s_t0;
     int64_t idle = 0;
     bool have_prev = false;
+    bool have_pre = false;                                    // polls issued during the last tile (GEMM tiles only)
     Polls polls = {};                                         // wave 0: issued after the last tile's K loop
     int pre_t = 0;                                            // lane 0: a claim issued ahead, during the tile
     for (;;) {
-        if (tid < 64) boundary(a, t0, wg, &cmd, have_prev, idle, &tab, have_prev, polls, pre_t);
+        if (tid < 64) boundary<COMB>(a, t0, wg, &cmd, have_prev, idle, &tab, have_pre, polls, pre_t, s_n3);
         __syncthreads();
         const int kind = cmd.kind;
         have_prev = false;
+        have_pre = false;                                     // set again only by a GEMM tile's hook
         if (kind == CMD_EXIT) break;
         if (kind == CMD_IDLE) {
             __builtin_amdgcn_s_sleep(8);
@@ -804,22 +942,28 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
         const int rows32 = __builtin_amdgcn_readfirstlane(cmd.rows32);
         const int nb = __builtin_amdgcn_readfirstlane(cmd.nb);
         const int e = __builtin_amdgcn_readfirstlane(cmd.e);
+        const int ct = __builtin_amdgcn_readfirstlane(cmd.t);
         __syncthreads();                                      // every thread has read cmd
-        run_tile(a.op[o], stage, row0, rows32, nb, e, lds, [&]() {
-            // (both results are assigned on every path, so neither stays live across the K loop)
-            Polls p = {};
-            int t_ahead = 0;
-            if (tid < 64) {
-                p = issue_polls(a);
-                // claim the next tile of the same op ahead; its round trip overlaps the epilogue
-                const int pn = cmd.pre_next;                  // written by this wave at the boundary
-                if (tid == 0 && pn >= 0) t_ahead = atomicAdd(&xq_of(a.ws, pn, xcc_id())->claim, 1);
-            }
-            polls = p;
-            pre_t = t_ahead;
-        });
-        // Wave 0's release at the commit writes back this XCD's L2; the barrier does
-        // not wait for global stores, so each wave first lets its own reach the L2.
+        if (COMB && stage == 3) {
+            run_combine(a.op[o], ct, lds, a.status);
+        } else {
+            have_pre = true;
+            run_tile(a.op[o], stage, row0, rows32, nb, e, lds, [&]() {
+                // (both results are assigned on every path, so neither stays live across the K loop)
+                Polls p = {};
+                int t_ahead = 0;
+                if (tid < 64) {
+                    p = issue_polls(a);
+                    // claim the next tile of the same op ahead; its round trip overlaps the epilogue
+                    const int pn = cmd.pre_next;                  // written by this wave at the boundary
+                    if (tid == 0 && pn >= 0) t_ahead = atomicAdd(&xq_of(a.ws, pn, xcc_id())->claim, 1);
+                }
+                polls = p;
+                pre_t = t_ahead;
+            });
+        }
+        // The commit counts on every wave's stores having reached the L2; the barrier
+        // does not wait for global stores, so each wave first waits for its own.
         wait_own_stores();
         __syncthreads();
         have_prev = true;
@@ -936,6 +1080,14 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
             if ((int64_t)d.T * d.H * (cls == CLS_FP8 ? 1 : 2) >= ((int64_t)1 << 31))
                 return fail(MOE_ERR_UNSUPPORTED, "op %d: T*H of the gathered operand exceeds 2^31 bytes", o);
         }
+        if (d.y) {                                    // fused combine
+            if (!d.assign_to_row || !d.topk_w || d.T < 0 || d.top_k < 1 || d.top_k > 32)
+                return fail(MOE_ERR_INVALID_ARG, "op %d: fused combine needs assign_to_row, topk_w, T >= 0, top_k in [1,32]", o);
+            if (d.y_dtype != MOE_BF16 && d.y_dtype != MOE_F32)
+                return fail(MOE_ERR_UNSUPPORTED, "op %d: fused combine y_dtype %d not supported", o, d.y_dtype);
+            if ((int64_t)d.T * d.top_k > INT32_MAX / 2 || (int64_t)d.T * d.H > INT32_MAX)
+                return fail(MOE_ERR_UNSUPPORTED, "op %d: fused combine T too large", o);
+        }
         if (d.depends_on_op >= o || d.depends_on_op < -1)
             return fail(MOE_ERR_INVALID_ARG, "op %d: depends_on_op=%d must be -1 or an earlier op", o, d.depends_on_op);
         if (d.gap_ns < 0) return fail(MOE_ERR_INVALID_ARG, "op %d: gap_ns < 0", o);
@@ -955,6 +1107,13 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
         p.wds = d.w_down_scales;
         p.hs = d.h_scales;
         p.done_word = d.done_word;
+        p.a2r = d.y ? d.assign_to_row : nullptr;
+        p.tw = d.y ? d.topk_w : nullptr;
+        p.yc = d.y;
+        p.ct = d.y ? d.T : 0;
+        p.ck = d.y ? d.top_k : 1;
+        p.y_f32 = d.y && d.y_dtype == MOE_F32;
+        p.n3 = d.y ? (d.T + kCombTokens - 1) / kCombTokens : 0;
         p.cls = cls;
         p.phase = d.phase;
         p.layer = d.layer;
@@ -1014,14 +1173,17 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
     a.status = status_word;
     a.ws = (char*)workspace;
 
-    static bool attr_set = false;
-    if (!attr_set) {
-        if (hipFuncSetAttribute((const void*)apk_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes) != hipSuccess)
+    bool comb = false;
+    for (int o = 0; o < n_ops; ++o) comb |= a.op[o].n3 > 0;
+    const void* kfn = comb ? (const void*)apk_kernel<true> : (const void*)apk_kernel<false>;
+    static bool attr_set[2] = {false, false};
+    if (!attr_set[comb]) {
+        if (hipFuncSetAttribute(kfn, hipFuncAttributeMaxDynamicSharedMemorySize, kLdsBytes) != hipSuccess)
             return fail(MOE_ERR_HIP, "hipFuncSetAttribute(LDS=%d) failed", kLdsBytes);
-        attr_set = true;
+        attr_set[comb] = true;
     }
     int per_cu = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, (const void*)apk_kernel, 256, kLdsBytes) != hipSuccess)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kfn, 256, kLdsBytes) != hipSuccess)
         return fail(MOE_ERR_HIP, "occupancy query failed");
     if (per_cu < 1) return fail(MOE_ERR_UNSUPPORTED, "persistent kernel does not fit on a CU");
     if (n_wg > per_cu * cu) return fail(MOE_ERR_INVALID_ARG, "n_workgroups=%d exceeds co-resident capacity %d", n_wg, per_cu * cu);
@@ -1032,7 +1194,8 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
     ia.status = status_word;
     hipStream_t s = (hipStream_t)stream;
     hipLaunchKernelGGL(apk_init_kernel, dim3(1), dim3(256), 0, s, ia);
-    hipLaunchKernelGGL(apk_kernel, dim3(n_wg), dim3(256), kLdsBytes, s, a);
+    if (comb) hipLaunchKernelGGL(apk_kernel<true>, dim3(n_wg), dim3(256), kLdsBytes, s, a);
+    else hipLaunchKernelGGL(apk_kernel<false>, dim3(n_wg), dim3(256), kLdsBytes, s, a);
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(MOE_ERR_HIP, "moe_grouped_ffn_persistent: launch failed: %s", hipGetErrorString(err));
     return MOE_OK;

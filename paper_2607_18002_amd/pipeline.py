@@ -14,7 +14,7 @@ import numpy as np
 import torch
 
 from . import ops as K
-from ._lib import (MOE_BF16, MOE_DECODE, MOE_FP8_E4M3, MOE_LAYOUT_PACKED, MOE_PREFILL, OpDesc, OpStats, SchedConfig,
+from ._lib import (MOE_BF16, MOE_DECODE, MOE_F32, MOE_FP8_E4M3, MOE_LAYOUT_PACKED, MOE_PREFILL, OpDesc, OpStats, SchedConfig,
                    TraceRec)
 
 TRACE_DTYPE = np.dtype([("op", "<i2"), ("stage", "<i2"), ("wg", "<i2"), ("xcc", "<i2"), ("expert", "<i4"),
@@ -114,13 +114,16 @@ class MoEPipeline:
                  decode_quota_max_wg: int = 0, x_moe_expected: int = 0, round_multiple: int = 8,
                  trace_capacity: int = 0, spin_limit: int = 0, abort_word: Optional[torch.Tensor] = None,
                  y_dtype: torch.dtype = torch.bfloat16, fused_gather: bool = False, group_row_tiles: int = 0,
-                 static_partition: bool = False):
+                 static_partition: bool = False, fused_combine: bool = False):
         """fused_gather: GEMM-1 reads its rows straight from x through row_to_assign
-        (permute then only builds the maps), instead of from a permuted copy x_perm."""
+        (permute then only builds the maps), instead of from a permuted copy x_perm.
+        fused_combine: the persistent kernel writes y itself (combine tiles after
+        each op's GEMM tiles), and combine() launches nothing."""
         if not specs:
             raise ValueError("no operations")
         self.device = specs[0].logits.device
         self.fused_gather = fused_gather
+        self.fused_combine = fused_combine
         dev = self.device
         self.bufs: List[OpBuffers] = []
         for s in specs:
@@ -164,7 +167,7 @@ class MoEPipeline:
                                trace=self.trace.data_ptr() if trace_capacity > 0 else None,
                                trace_capacity=trace_capacity, op_stats=self.stats.data_ptr(),
                                spin_limit=spin_limit, static_partition=int(static_partition))
-        self.descs = [self._desc(i, b, fused_gather) for i, b in enumerate(self.bufs)]
+        self.descs = [self._desc(i, b, fused_gather, fused_combine) for i, b in enumerate(self.bufs)]
         self._route_args = [K.route_args(b.spec.logits, b.spec.top_k, b.spec.local_begin, b.spec.E_local, b.topk_ids,
                                          b.topk_w) for b in self.bufs]
         self._permute_args = [K.permute_args(b.topk_ids, b.spec.E_local, b.spec.x, b.spec.x_scales, b.row_align,
@@ -176,13 +179,16 @@ class MoEPipeline:
         self.ffn_ws = torch.zeros((K.moe_ffn_workspace_bytes(self.descs, self.cfg),), dtype=torch.uint8, device=dev)
 
     @staticmethod
-    def _desc(i: int, b: OpBuffers, fused_gather: bool = False) -> OpDesc:
+    def _desc(i: int, b: OpBuffers, fused_gather: bool = False, fused_combine: bool = False) -> OpDesc:
         s, w = b.spec, b.spec.weights
         p = lambda t: None if t is None else t.data_ptr()  # noqa: E731
         gathered = {}
         if fused_gather:
             gathered = dict(x=p(s.x), x_scales=p(s.x_scales), row_to_assign=p(b.row_to_assign), T=b.T,
                             top_k=s.top_k)
+        if fused_combine:
+            gathered.update(T=b.T, top_k=s.top_k, assign_to_row=p(b.assign_to_row), topk_w=p(b.topk_w), y=p(b.y),
+                            y_dtype=MOE_F32 if b.y.dtype == torch.float32 else MOE_BF16)
         return OpDesc(**gathered, phase=s.phase, layer=s.layer, E_local=s.E_local, H=w.H, I=w.I, capacity=b.capacity,
                       row_align=b.row_align, dtype=w.dtype, counts=p(b.counts), offsets=p(b.offsets),
                       x_perm=p(b.x_perm), x_perm_scales=p(b.x_perm_scales), w_gate_up=p(w.w_gate_up),
@@ -217,6 +223,8 @@ class MoEPipeline:
         K.moe_grouped_ffn_persistent(self.descs, self.cfg, self.ffn_ws, self.status, stream)
 
     def combine(self, stream=None, batched: bool = True):
+        if self.fused_combine:                     # the persistent kernel wrote y
+            return
         if batched:
             K.moe_combine_batch(self._combine_args, stream)
             return

@@ -596,3 +596,38 @@ def test_batched_calls_match_per_op_calls(dev, dtype):
     for a, b in zip(*outs):
         for ta, tb in zip(a, b):
             assert torch.equal(ta, tb)
+
+
+@pytest.mark.parametrize("dtype,y_f32", [("bf16", False), ("fp8", False), ("bf16", True)])
+def test_fused_combine_matches_separate_combine(dev, dtype, y_f32):
+    """Combine tiles inside the persistent kernel give moe_combine's y bit for
+    bit (the same fp32 accumulation order) for every op of a 2-layer mixed
+    launch, including an op none of whose tokens routes to a local expert: it
+    runs no GEMM tile, and its combine tiles write zeros."""
+    import dataclasses
+    from paper_2607_18002_amd.pipeline import MoEPipeline
+    base = 2 if dtype == "bf16" else 5
+    cfg = custom_config(base, cfg_id=720 + base, H=512, I=512, prefill_tokens=700, decode_tokens=90, E_global=64,
+                        E_local=12, top_k=6, zipf_s=(1.2, 0.7), n_layers=2)
+    specs = []
+    for layer in range(2):
+        s, _, _ = layer_specs(cfg, layer, dev)
+        specs += s
+    last = specs[-1]
+    lg = last.logits.clone()
+    lg[:, last.local_begin:last.local_begin + last.E_local] = -1.0e4
+    specs[-1] = dataclasses.replace(last, logits=lg)
+    ydt = torch.float32 if y_f32 else torch.bfloat16
+    outs = []
+    for fused in (False, True):
+        pipe = MoEPipeline(specs, fused_gather=True, fused_combine=fused, y_dtype=ydt)
+        for b in pipe.bufs:
+            b.y.fill_(3.0)                                   # every element must be written
+        pipe.run()
+        torch.cuda.synchronize()
+        assert pipe.statuses() == (0, 0)
+        assert int(pipe.bufs[-1].counts.sum().item()) == 0
+        outs.append([b.y.view(torch.int32 if y_f32 else torch.int16).cpu() for b in pipe.bufs])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+    assert not outs[1][-1].any()
