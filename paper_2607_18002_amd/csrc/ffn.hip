@@ -558,7 +558,7 @@ __device__ bool take_tile(const KArgs& a, int o, int src, int t, int myx, TabCac
 __device__ void take_combine(int o, int t, Cmd* cmd, unsigned long long t_boundary, unsigned long long now) {
     if (threadIdx.x == 0) {
         cmd->kind = CMD_TILE; cmd->op = o; cmd->stage = 3; cmd->t = t;
-        cmd->e = -1; cmd->mblk = 0; cmd->row0 = 0; cmd->rows = 0; cmd->rows32 = 0; cmd->nb = 0; cmd->mtile = -1;
+        cmd->e = -1; cmd->mblk = t; cmd->row0 = 0; cmd->rows = 0; cmd->rows32 = 0; cmd->nb = 0; cmd->mtile = -1;   // trace: mblk = tile
         cmd->pre_next = -1;
         cmd->t_boundary = t_boundary;
         cmd->t_polled = now;

@@ -200,3 +200,33 @@ def test_static_partition_never_borrows(dev):
     assert tr[tr["op"] == 0]["wg"].min() >= 64
     for b, w in zip(pipe.bufs, want):
         np.testing.assert_array_equal(b.y.view(torch.int16).cpu().numpy(), w)
+
+
+def test_fused_combine_tiles_follow_gemm_and_precede_dependants(dev):
+    """With a fused combine, each op's combine tiles (trace stage 3, row-block
+    field = tile index) run exactly once each, none is claimed before the op's
+    last GEMM tile committed, the op's t_done follows its last combine tile,
+    and the next layer of the same phase starts only after that."""
+    from paper_2607_18002_amd.pipeline import MoEPipeline
+    cfg = custom_config(2, cfg_id=731, H=512, I=512, prefill_tokens=900, decode_tokens=70, E_global=64, E_local=12,
+                        top_k=6, zipf_s=(1.1,), n_layers=2)
+    specs, _, _ = layer_specs(cfg, 0, dev)                      # op 0 prefill, op 1 decode
+    s1, _, _ = layer_specs(cfg, 1, dev, prefill=dict(depends_on_op=0), decode=dict(depends_on_op=1))
+    specs += s1
+    assert [sp.depends_on_op for sp in specs] == [-1, -1, 0, 1]
+    pipe = MoEPipeline(specs, fused_gather=True, fused_combine=True, trace_capacity=1 << 16)
+    pipe.run()
+    torch.cuda.synchronize()
+    assert pipe.statuses() == (0, 0)
+    tr, st = pipe.trace_records(), pipe.op_stats()
+    for o, b in enumerate(pipe.bufs):
+        m = tr[tr["op"] == o]
+        comb, gemm = m[m["stage"] == 3], m[m["stage"] != 3]
+        n3 = (b.T + 31) // 32
+        assert sorted(comb["mblk"].tolist()) == list(range(n3))
+        if len(gemm):
+            assert comb["t_claim"].min() >= gemm["t_end"].max()
+        assert int(st["t_done"][o]) >= int(comb["t_end"].max())
+        dep = specs[o].depends_on_op
+        if dep >= 0:
+            assert m["t_claim"].min() >= int(st["t_done"][dep])
