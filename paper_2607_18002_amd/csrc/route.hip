@@ -32,9 +32,10 @@ __device__ __forceinline__ float key_value(uint32_t k) {
 // DPP controls: quad permutes [1,0,3,2] and [2,3,0,1], half-row and row mirrors.
 constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E, kDppHalfMirror = 0x141, kDppMirror = 0x140;
 
+// (0, the identity of an unsigned max, fills disabled lanes: the move folds into the max)
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp_max(uint32_t v) {
-    const uint32_t o = (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, false);
+    const uint32_t o = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, true);
     return v > o ? v : o;
 }
 
@@ -50,6 +51,36 @@ __device__ __forceinline__ uint32_t wave_max(uint32_t v) {
     const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
     const uint32_t a = r0 > r1 ? r0 : r1, b = r2 > r3 ? r2 : r3;
     return a > b ? a : b;
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_min(uint32_t v) {
+    const uint32_t o = (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, false);
+    return v < o ? v : o;
+}
+
+// Minimum of v over the wave, the same value in every lane.
+__device__ __forceinline__ uint32_t wave_min(uint32_t v) {
+    v = dpp_min<kDppXor1>(v);
+    v = dpp_min<kDppXor2>(v);
+    v = dpp_min<kDppHalfMirror>(v);
+    v = dpp_min<kDppMirror>(v);
+    const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
+    const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
+    const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
+    const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+    const uint32_t a = r0 < r1 ? r0 : r1, b = r2 < r3 ? r2 : r3;
+    return a < b ? a : b;
+}
+
+// (key, expert) pairs in selection order: larger key first, then lower expert.
+__device__ __forceinline__ void order_pair(uint32_t& ka, uint32_t& ia, uint32_t& kb, uint32_t& ib) {
+    const bool swap = kb > ka || (kb == ka && ib < ia);
+    const uint32_t k0 = swap ? kb : ka, i0 = swap ? ib : ia;
+    kb = swap ? ka : kb;
+    ib = swap ? ia : ib;
+    ka = k0;
+    ia = i0;
 }
 
 // Sum of v over the wave, the same value in every lane.
@@ -82,6 +113,39 @@ __device__ __forceinline__ void route_block(const float* __restrict__ logits, in
     for (int i = 0; i < EPL; ++i) key[i] = (lane + 64 * i < E) ? order_key(v[i]) : 0u;
     int my_e = -1;
     uint32_t my_key = 0;
+    if constexpr (EPL <= 4) {
+        // Each lane sorts its pairs once; a round then reduces only the lanes'
+        // heads, and the lane holding the winner drops its head.  The winner is
+        // the largest key, ties to the lower expert: a unique maximum head is
+        // found with one ballot; equal heads in several lanes take a wave-wide
+        // minimum over their experts.
+        uint32_t idx[EPL];
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) idx[i] = (uint32_t)(lane + 64 * i);
+        if constexpr (EPL >= 2) order_pair(key[0], idx[0], key[1], idx[1]);
+        if constexpr (EPL == 4) {
+            order_pair(key[2], idx[2], key[3], idx[3]);
+            order_pair(key[0], idx[0], key[2], idx[2]);
+            order_pair(key[1], idx[1], key[3], idx[3]);
+            order_pair(key[1], idx[1], key[2], idx[2]);
+        }
+        for (int r = 0; r < k; ++r) {
+            const uint32_t best = wave_max(key[0]);
+            const uint64_t hit = __ballot(key[0] == best);
+            int e;
+            if (__popcll(hit) == 1) e = __builtin_amdgcn_readlane((int)idx[0], __ffsll((long long)hit) - 1);
+            else e = (int)wave_min(key[0] == best ? idx[0] : 0xFFFFFFFFu);
+            if (lane == (e & 63)) {                          // drop the winner from its lane
+#pragma unroll
+                for (int i = 0; i + 1 < EPL; ++i) { key[i] = key[i + 1]; idx[i] = idx[i + 1]; }
+                key[EPL - 1] = 0u;
+            }
+            if (lane == r) {
+                my_e = e;
+                my_key = best;
+            }
+        }
+    } else {
     for (int r = 0; r < k; ++r) {
         uint32_t best = key[0];
 #pragma unroll
@@ -102,6 +166,7 @@ __device__ __forceinline__ void route_block(const float* __restrict__ logits, in
             my_e = e;
             my_key = best;
         }
+    }
     }
     const float my_v = key_value(my_key);
     const float m = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_v), 0));   // the largest selected logit
