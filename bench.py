@@ -2,7 +2,8 @@
 """Benchmark of the routed-expert MoE hot path on one MI355X.
 
 A step is one pass of the whole path over one batch: moe_topk_route and
-moe_permute over every operation (one batched launch each), ONE
+moe_permute over every operation (one batched launch each; decode operations
+use the masked layout by default, their rows placed by the routing launch), ONE
 moe_grouped_ffn_persistent launch over all operations, and moe_combine over
 every operation (one batched launch).  The default workload is
 the mixed prefill+decode configuration: 4 layers x (8192 prefill + 1024 decode
@@ -47,6 +48,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=4, help="workload configuration (1-5); default 4")
     ap.add_argument("--quota", type=int, default=80, help="decode quota q in workgroups")
+    ap.add_argument("--decode-layout", choices=["masked", "contiguous"], default="masked",
+                    help="masked: decode ops' rows placed by routing in per-expert regions (no permute pass); "
+                         "contiguous: permuted like prefill")
     ap.add_argument("--fused-combine", action="store_true",
                     help="combine tiles inside the persistent kernel instead of a separate combine launch")
     ap.add_argument("--group-row-tiles", type=int, default=0,
@@ -220,7 +224,9 @@ def main():
     specs, layers = build_specs(cfg, dev)
     t_gen = time.perf_counter() - t_gen
     fused = args.gather == "fused"
-    pipe = MoEPipeline(specs, decode_quota_wg=args.quota, fused_gather=fused, fused_combine=args.fused_combine,
+    masked = args.decode_layout == "masked" and fused     # the masked layout needs the fused gather
+    pipe = MoEPipeline(specs, decode_quota_wg=args.quota, fused_gather=fused,
+                       fused_combine=args.fused_combine, masked_decode=masked,
                        group_row_tiles=args.group_row_tiles)
     stream = torch.cuda.current_stream()
 
@@ -249,7 +255,8 @@ def main():
 
     flops, abytes, rows = algorithmic_work(pipe, cfg)
     # one more launch with the per-tile trace for the decode latency figures
-    traced = MoEPipeline(specs, decode_quota_wg=args.quota, trace_capacity=1 << 18, fused_gather=fused, fused_combine=args.fused_combine,
+    traced = MoEPipeline(specs, decode_quota_wg=args.quota, trace_capacity=1 << 18, fused_gather=fused,
+                       fused_combine=args.fused_combine, masked_decode=masked,
                          group_row_tiles=args.group_row_tiles)
     traced.run()
     torch.cuda.synchronize()
@@ -265,7 +272,8 @@ def main():
     excl = None
     dec_specs = phase_subset(specs, 1)
     if lat is not None and dec_specs and len(dec_specs) < len(specs):
-        alone = MoEPipeline(dec_specs, decode_quota_wg=args.quota, trace_capacity=1 << 16, fused_gather=fused, fused_combine=args.fused_combine,
+        alone = MoEPipeline(dec_specs, decode_quota_wg=args.quota, trace_capacity=1 << 16, fused_gather=fused,
+                       fused_combine=args.fused_combine, masked_decode=masked,
                             group_row_tiles=args.group_row_tiles)
         alone.run()
         alone.run()
@@ -332,7 +340,8 @@ def main():
                    "experts_local": cfg.E_local, "experts_global": cfg.E_global, "top_k": cfg.top_k,
                    "hidden": cfg.H, "intermediate": cfg.I, "decode_quota_wg": args.quota,
                    "group_row_tiles": args.group_row_tiles,
-                   "gather": args.gather, "combine": "fused" if args.fused_combine else "separate", "local_rows": rows},
+                   "gather": args.gather, "combine": "fused" if args.fused_combine else "separate",
+                   "decode_layout": "masked" if masked else "contiguous", "local_rows": rows},
         "hbm_gbps_alg": round(abytes / (ffn_ms * 1e-3) / 1e9, 1),
         "ffn_tflops": round(flops / (ffn_ms * 1e-3) / 1e12, 2),
         "decode_tile_latency": lat,

@@ -97,6 +97,27 @@ typedef struct moe_route_args {
     int32_t T, E_global, top_k, local_begin, E_local;
     int32_t* topk_ids;
     float* topk_w;
+    /* Masked layout (the decode layout of "Prefill-Decode Disaggregation":
+     * a fixed region of `slots` rows per local expert and a per-expert count,
+     * filled as routing decides, with no packing pass).  With counts non-NULL
+     * the entry also places every local slot a = t*top_k + j of expert e at
+     * row e*slots + (counts[e] before an atomic increment) and writes
+     * assign_to_row[a] (-1 for a slot that is not local) and row_to_assign[row].
+     * counts must be zero on entry; the row order inside a region follows the
+     * atomics (any order is a valid layout: rows are computed independently).
+     * slots: a multiple of 32 and >= T (a token has at most one slot per
+     * expert).  clear (E_local ints, or NULL) is zeroed by the same launch, so
+     * a caller alternating two count arrays never needs a separate reset.
+     * The FFN then takes counts, offsets[e] = e*slots (offsets[E_local] =
+     * E_local*slots) and capacity E_local*slots; moe_permute is not called.
+     * Rows of a region past its count keep stale row_to_assign entries; the
+     * FFN's gather bounds every entry by T*top_k and their outputs are never
+     * read.  With counts NULL the remaining fields are ignored. */
+    int32_t slots, pad0;
+    int32_t* counts;
+    int32_t* clear;
+    int32_t* assign_to_row;
+    int32_t* row_to_assign;
 } moe_route_args;
 moe_status_t moe_topk_route_batch(const moe_route_args* ops, int32_t n_ops, void* stream);
 

@@ -73,6 +73,7 @@ class RouteArgs(C.Structure):
     _fields_ = [
         ("logits", _p), ("T", _i32), ("E_global", _i32), ("top_k", _i32), ("local_begin", _i32),
         ("E_local", _i32), ("topk_ids", _p), ("topk_w", _p),
+        ("slots", _i32), ("pad0", _i32), ("counts", _p), ("clear", _p), ("assign_to_row", _p), ("row_to_assign", _p),
     ]
 
 

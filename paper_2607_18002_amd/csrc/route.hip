@@ -97,9 +97,18 @@ __device__ __forceinline__ float wave_sum(float v) {
 }
 
 // One op's routing: block `blk` of the op handles tokens [4*blk, 4*blk + 4).
+// Masked layout outputs of an op (counts NULL: none).
+struct MaskedOut {
+    int32_t* counts;
+    int32_t* a2r;
+    int32_t* r2a;
+    int slots;
+};
+
 template <int EPL>
 __device__ __forceinline__ void route_block(const float* __restrict__ logits, int T, int E, int k, int local_begin,
-                                            int E_local, int32_t* __restrict__ ids, float* __restrict__ wts, int blk) {
+                                            int E_local, int32_t* __restrict__ ids, float* __restrict__ wts, int blk,
+                                            MaskedOut mo = MaskedOut{nullptr, nullptr, nullptr, 0}) {
     const int lane = threadIdx.x & 63;
     const int t = blk * kTokensPerBlock + (threadIdx.x >> 6);
     if (t >= T) return;  // wave-uniform
@@ -174,8 +183,21 @@ __device__ __forceinline__ void route_block(const float* __restrict__ logits, in
     const float s = wave_sum(ex);
     if (lane < k) {
         const int loc = my_e - local_begin;
-        ids[(size_t)t * k + lane] = (loc >= 0 && loc < E_local) ? loc : -1;
+        const bool local = loc >= 0 && loc < E_local;
+        ids[(size_t)t * k + lane] = local ? loc : -1;
         wts[(size_t)t * k + lane] = ex / s;
+        if (mo.counts) {                                 // masked layout: the next free row of the expert's region
+            const int a = t * k + lane;
+            int row = -1;
+            if (local) {
+                const int slot = atomicAdd(mo.counts + loc, 1);
+                if (slot < mo.slots) {                   // always, as slots >= T
+                    row = loc * mo.slots + slot;
+                    mo.r2a[row] = a;
+                }
+            }
+            mo.a2r[a] = row;
+        }
     }
 }
 
@@ -198,8 +220,10 @@ __global__ __launch_bounds__(256) void topk_route_batch_kernel(const RouteBatch 
     int o = 0;
     while (o + 1 < b.n && (int)blockIdx.x >= b.blk0[o + 1]) ++o;      // uniform
     const moe_route_args& a = b.op[o];
+    if (a.clear && (int)blockIdx.x == b.blk0[o])
+        for (int i = threadIdx.x; i < a.E_local; i += 256) a.clear[i] = 0;
     route_block<EPL>(a.logits, a.T, a.E_global, a.top_k, a.local_begin, a.E_local, a.topk_ids, a.topk_w,
-                     (int)blockIdx.x - b.blk0[o]);
+                     (int)blockIdx.x - b.blk0[o], MaskedOut{a.counts, a.assign_to_row, a.row_to_assign, a.slots});
 }
 
 moe_status_t check_route(const float* logits, int32_t T, int32_t E_global, int32_t top_k, int32_t local_begin,
@@ -253,6 +277,15 @@ extern "C" moe_status_t moe_topk_route_batch(const moe_route_args* ops, int32_t 
         const moe_status_t st = check_route(a.logits, a.T, a.E_global, a.top_k, a.local_begin, a.E_local,
                                             a.topk_ids, a.topk_w);
         if (st != MOE_OK) return st;
+        if (a.counts) {
+            if (a.slots < a.T || a.slots % 32 != 0 || (int64_t)a.slots * a.E_local > INT32_MAX)
+                return fail(MOE_ERR_INVALID_ARG, "moe_topk_route_batch: entry %d: slots=%d must be a multiple of 32, "
+                            ">= T=%d, slots*E_local < 2^31", o, a.slots, a.T);
+            if (!a.assign_to_row || !a.row_to_assign || a.clear == a.counts)
+                return fail(MOE_ERR_INVALID_ARG, "moe_topk_route_batch: entry %d: masked layout needs assign_to_row, "
+                            "row_to_assign and a clear array other than counts", o);
+        }
+        if (a.T == 0 && a.clear) return fail(MOE_ERR_INVALID_ARG, "moe_topk_route_batch: entry %d: clear with T=0", o);
         b.op[o] = a;
         b.blk0[o] = (int32_t)blocks;
         blocks += (a.T + kTokensPerBlock - 1) / kTokensPerBlock;

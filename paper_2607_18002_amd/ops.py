@@ -64,10 +64,15 @@ def moe_topk_route_batch(entries: Sequence[RouteArgs], stream=None) -> None:
 
 
 def route_args(logits: torch.Tensor, top_k: int, local_begin: int, E_local: int, topk_ids: torch.Tensor,
-               topk_w: torch.Tensor) -> RouteArgs:
+               topk_w: torch.Tensor, slots: int = 0, counts: Optional[torch.Tensor] = None,
+               clear: Optional[torch.Tensor] = None, assign_to_row: Optional[torch.Tensor] = None,
+               row_to_assign: Optional[torch.Tensor] = None) -> RouteArgs:
+    """One entry of moe_topk_route_batch; with counts given it also places the
+    local slots in the masked layout (slots rows per local expert)."""
     T, E = logits.shape
     return RouteArgs(logits=_ptr(logits), T=T, E_global=E, top_k=top_k, local_begin=local_begin, E_local=E_local,
-                     topk_ids=_ptr(topk_ids), topk_w=_ptr(topk_w))
+                     topk_ids=_ptr(topk_ids), topk_w=_ptr(topk_w), slots=slots, counts=_ptr(counts),
+                     clear=_ptr(clear), assign_to_row=_ptr(assign_to_row), row_to_assign=_ptr(row_to_assign))
 
 
 def moe_permute_workspace_bytes(T: int, top_k: int, E_local: int) -> int:

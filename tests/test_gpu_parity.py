@@ -631,3 +631,47 @@ def test_fused_combine_matches_separate_combine(dev, dtype, y_f32):
     for a, b in zip(*outs):
         assert torch.equal(a, b)
     assert not outs[1][-1].any()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_masked_decode_layout(dev, dtype):
+    """Decode ops in the masked layout (routing places each local slot in its
+    expert's fixed region; no permute pass) give the contiguous layout's
+    routing, counts and y bit for bit, over three steps (the count arrays
+    alternate and the routing of each step clears the other), and the layout
+    is valid: every local slot of expert e has a distinct row in
+    [e*slots, e*slots + counts[e]) whose row_to_assign points back to it."""
+    from paper_2607_18002_amd import MOE_DECODE
+    from paper_2607_18002_amd.pipeline import MoEPipeline
+    base = 2 if dtype == "bf16" else 5
+    cfg = custom_config(base, cfg_id=740 + base, H=512, I=512, prefill_tokens=600, decode_tokens=77, E_global=64,
+                        E_local=12, top_k=6, zipf_s=(1.2, 0.7), n_layers=2)
+    specs = []
+    for layer in range(2):
+        s, _, _ = layer_specs(cfg, layer, dev)
+        specs += s
+    ref = MoEPipeline(specs, fused_gather=True)
+    msk = MoEPipeline(specs, fused_gather=True, masked_decode=True)
+    for step in range(3):
+        for p in (ref, msk):
+            p.run()
+        torch.cuda.synchronize()
+        assert ref.statuses() == (0, 0) and msk.statuses() == (0, 0)
+        for br, bm in zip(ref.bufs, msk.bufs):
+            assert torch.equal(br.topk_ids, bm.topk_ids) and torch.equal(br.topk_w, bm.topk_w)
+            assert torch.equal(br.counts, bm.counts)
+            assert torch.equal(br.y.view(torch.int16), bm.y.view(torch.int16))
+            if bm.spec.phase != MOE_DECODE:
+                continue
+            assert bm.slots > 0
+            ids = bm.topk_ids.cpu().numpy().reshape(-1)
+            a2r = bm.assign_to_row.cpu().numpy()
+            r2a = bm.row_to_assign.cpu().numpy()
+            cnt = bm.counts.cpu().numpy()
+            assert np.array_equal(a2r < 0, ids < 0)
+            loc = np.nonzero(ids >= 0)[0]
+            rows = a2r[loc]
+            assert len(np.unique(rows)) == len(rows)
+            e = ids[loc]
+            assert np.all(rows >= e * bm.slots) and np.all(rows < e * bm.slots + cnt[e])
+            assert np.array_equal(r2a[rows], loc)
