@@ -177,24 +177,24 @@ __device__ __forceinline__ void route_block(const float* __restrict__ logits, in
         }
     }
     }
+    // masked layout: claim the slot's row now, so the atomic's round trip overlaps the softmax
+    const int loc = my_e - local_begin;
+    const bool local = lane < k && loc >= 0 && loc < E_local;
+    int slot = 0;
+    if (mo.counts && local) slot = atomicAdd(mo.counts + loc, 1);
     const float my_v = key_value(my_key);
     const float m = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_v), 0));   // the largest selected logit
     const float ex = (lane < k) ? expf(my_v - m) : 0.f;
     const float s = wave_sum(ex);
     if (lane < k) {
-        const int loc = my_e - local_begin;
-        const bool local = loc >= 0 && loc < E_local;
         ids[(size_t)t * k + lane] = local ? loc : -1;
         wts[(size_t)t * k + lane] = ex / s;
         if (mo.counts) {                                 // masked layout: the next free row of the expert's region
             const int a = t * k + lane;
             int row = -1;
-            if (local) {
-                const int slot = atomicAdd(mo.counts + loc, 1);
-                if (slot < mo.slots) {                   // always, as slots >= T
-                    row = loc * mo.slots + slot;
-                    mo.r2a[row] = a;
-                }
+            if (local && slot < mo.slots) {              // always, as slots >= T
+                row = loc * mo.slots + slot;
+                mo.r2a[row] = a;
             }
             mo.a2r[a] = row;
         }
