@@ -10,7 +10,7 @@ the mixed prefill+decode configuration: 4 layers x (8192 prefill + 1024 decode
 tokens), 32 of 256 experts local, top-8, hidden 3072, expert intermediate
 1536, bf16, in one persistent launch; decode layer 0 is released 10 us after
 the launch starts, each later layer of a phase when that phase's previous
-layer is done (+20 us for decode), decode quota 80 of 256 workgroups.
+layer is done (+20 us for decode), decode quota 88 of 256 workgroups.
 
 Prints ONE JSON line.  value = routed-expert TFLOP/s of the whole step
 (6*H*I flop per local routed row).  roofline = the persistent FFN kernel
@@ -47,7 +47,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=4, help="workload configuration (1-5); default 4")
-    ap.add_argument("--quota", type=int, default=80, help="decode quota q in workgroups")
+    ap.add_argument("--quota", type=int, default=88, help="decode quota q in workgroups")
     ap.add_argument("--decode-layout", choices=["masked", "contiguous"], default="masked",
                     help="masked: decode ops' rows placed by routing in per-expert regions (no permute pass); "
                          "contiguous: permuted like prefill")
