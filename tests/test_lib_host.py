@@ -116,3 +116,27 @@ def test_argument_errors_before_any_launch():
     assert lib.moe_combine(None, None, None, 4, 2, 12, None, _lib.MOE_BF16, None) == _lib.MOE_ERR_UNSUPPORTED
     assert lib.moe_combine(None, None, None, 4, 2, 16, None, 7, None) == _lib.MOE_ERR_UNSUPPORTED
     assert lib.moe_grouped_ffn_persistent(None, 1, None, None, None, None) == _lib.MOE_ERR_INVALID_ARG
+
+
+def test_masked_route_argument_errors():
+    """The masked-layout fields of moe_topk_route_batch are checked on the host
+    before anything is launched: slots a multiple of 32 and >= T, both maps
+    given, and a clear array other than counts."""
+    from paper_2607_18002_amd import _lib
+    lib = _lib.load_library()
+    fake = 0x10000                                          # never dereferenced: the call fails first
+
+    def call(**kw):
+        a = dict(logits=fake, T=64, E_global=64, top_k=4, local_begin=0, E_local=8, topk_ids=fake, topk_w=fake,
+                 slots=64, counts=fake, clear=fake + 256, assign_to_row=fake, row_to_assign=fake)
+        a.update(kw)
+        arr = (_lib.RouteArgs * 1)(_lib.RouteArgs(**a))
+        return lib.moe_topk_route_batch(arr, 1, None)
+
+    assert call(slots=40) == _lib.MOE_ERR_INVALID_ARG            # not a multiple of 32
+    assert b"slots=40" in lib.moe_last_error()
+    assert call(slots=32) == _lib.MOE_ERR_INVALID_ARG            # fewer slots than tokens
+    assert call(assign_to_row=None) == _lib.MOE_ERR_INVALID_ARG
+    assert call(clear=fake) == _lib.MOE_ERR_INVALID_ARG          # clear is counts
+    assert call(T=0, slots=0, counts=None) == _lib.MOE_ERR_INVALID_ARG   # clear with no token to clear it
+    assert call(counts=None, clear=None) != _lib.MOE_ERR_INVALID_ARG     # unmasked entry passes the checks
