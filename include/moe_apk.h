@@ -274,9 +274,9 @@ typedef struct moe_trace_rec {
 typedef struct moe_op_stats {
     uint64_t t_ready;         /* instantiation (release observed)                       */
     uint64_t t_first;         /* first tile started                                     */
-    uint64_t t_done;          /* last tile committed                                    */
+    uint64_t t_done;          /* op finished: its last tile (combine tile, if fused) committed */
     int32_t x_moe;            /* Eq. (3) footprint: row tiles at the class's tile height */
-    int32_t n_tiles;          /* GEMM-1 + GEMM-2 tiles                                  */
+    int32_t n_tiles;          /* GEMM-1 + GEMM-2 tiles (+ combine tiles, if fused)       */
     int32_t quota;            /* decode ops: q' of Eq. (4) in workgroups; prefill: 0    */
     int32_t reserved;
 } moe_op_stats;
