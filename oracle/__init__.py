@@ -15,6 +15,7 @@ from .moe import (  # noqa: F401
     dequant_weight,
     route,
     permute,
+    permute_masked,
     expert_ffn,
     expert_hidden,
     expert_down,

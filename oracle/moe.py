@@ -16,12 +16,14 @@ What the paper fixes, and the readings taken where it is silent:
   renormalise).  Experts [local_begin, local_begin+E_local) are this GPU's
   share; other selections get id -1 and keep their weight (no renormalising
   over the local subset: the other expert-parallel ranks hold the rest).
-* Permutation ("Prefill-Decode Disaggregation": the contiguous expert layout;
-  "One-Sided Dispatch and Combine": routing fixes each expert's destination
-  and final offset before activations are written, into buffers sized for
-  the maximum routed volume).  Reading: each expert owns a contiguous segment
-  that starts at a multiple of the tile height; rows inside a segment are the
-  expert's assignments a = t*k + j in ascending a; padding rows are zero.
+* Permutation ("Prefill-Decode Disaggregation": the contiguous expert layout
+  and the masked decode layout; "One-Sided Dispatch and Combine": routing
+  fixes each expert's destination and final offset before activations are
+  written, into buffers sized for the maximum routed volume).  Reading:
+  contiguous -- each expert owns a segment that starts at a multiple of the
+  tile height, padding rows zero; masked -- each expert owns a fixed region
+  of `slots` rows and a count.  In both, the rows of an expert are its
+  assignments a = t*k + j in ascending a.
 * Expert FFN (Evaluation, "Implementation": two grouped GEMMs and the
   activation fused into one kernel).  Reading: SwiGLU,
   h = silu(x Wg^T) * (x Wu^T), out = h Wd^T, silu(z) = z / (1 + e^-z), with
@@ -212,6 +214,49 @@ def permute(ids: np.ndarray, E_local: int, row_align: int, x: Optional[np.ndarra
     return res
 
 
+def permute_masked(ids: np.ndarray, E_local: int, slots: int, x: Optional[np.ndarray] = None,
+                   x_scales: Optional[np.ndarray] = None):
+    """Masked layout ("Prefill-Decode Disaggregation": the decode layout, one
+    fixed region per expert plus a count, no packing pass).  Reading: local
+    expert e owns rows [e*slots, (e+1)*slots); its rows are its assignments
+    a = t*k + j in ascending a, from the region's start; rows past the count
+    hold -1 (and zero activations).  A token selects distinct experts, so a
+    region needs at most T rows: slots >= T always suffices."""
+    ids = np.asarray(ids, dtype=np.int32)
+    T, k = ids.shape
+    flat = ids.reshape(-1)
+    if np.any(flat >= E_local) or np.any(flat < -1):
+        raise ValueError("expert id out of range")
+    counts = np.array([np.count_nonzero(flat == e) for e in range(E_local)], dtype=np.int64)
+    if np.any(counts > slots):
+        raise ValueError("a region holds fewer rows than its expert's assignments")
+    offsets = np.arange(E_local + 1, dtype=np.int64) * slots
+    cap = E_local * slots
+    row_to_assign = np.full(cap, -1, dtype=np.int64)
+    assign_to_row = np.full(T * k, -1, dtype=np.int64)
+    fill = offsets[:-1].copy()
+    for a in range(T * k):                          # ascending a: token, then slot
+        e = flat[a]
+        if e < 0:
+            continue
+        row_to_assign[fill[e]] = a
+        assign_to_row[a] = fill[e]
+        fill[e] += 1
+    res = PermuteResult(counts.astype(np.int32), offsets.astype(np.int32),
+                        row_to_assign.astype(np.int32), assign_to_row.astype(np.int32), None)
+    if x is not None:
+        x = np.asarray(x)
+        xp = np.zeros((cap,) + x.shape[1:], dtype=x.dtype)
+        valid = row_to_assign >= 0
+        xp[valid] = x[row_to_assign[valid] // k]
+        res.x_perm = xp
+        if x_scales is not None:
+            xs = np.zeros((cap,) + x_scales.shape[1:], dtype=x_scales.dtype)
+            xs[valid] = x_scales[row_to_assign[valid] // k]
+            res.x_perm_scales = xs
+    return res
+
+
 # ----------------------------------------------------------------------------- steps 3-5: expert FFN
 
 def expert_hidden(x_rows: np.ndarray, w_gate: np.ndarray, w_up: np.ndarray) -> np.ndarray:
@@ -310,10 +355,15 @@ def combine(y_perm: np.ndarray, assign_to_row: np.ndarray, w: np.ndarray, T: int
 # ----------------------------------------------------------------------------- whole local share
 
 def moe_local_share(logits, x, weights: dict, top_k: int, local_begin: int, E_local: int,
-                    row_align: int, x_scales=None, capacity=None, h_fp8: bool = False) -> dict:
-    """Every step in order; returns all intermediates (float results in float64)."""
+                    row_align: int, x_scales=None, capacity=None, h_fp8: bool = False, slots: int = 0) -> dict:
+    """Every step in order; returns all intermediates (float results in float64).
+    slots > 0: the masked layout with regions of `slots` rows (row_align and
+    capacity are then unused)."""
     ids, w = route(logits, top_k, local_begin, E_local)
-    p = permute(ids, E_local, row_align, x, capacity, x_scales)
+    if slots > 0:
+        p = permute_masked(ids, E_local, slots, x, x_scales)
+    else:
+        p = permute(ids, E_local, row_align, x, capacity, x_scales)
     xp = dequant_rows(p.x_perm, p.x_perm_scales)
     y_perm = grouped_ffn(xp, p.counts, p.offsets, weights, h_fp8=h_fp8)
     y = combine(y_perm, p.assign_to_row, w, ids.shape[0], top_k)

@@ -38,6 +38,8 @@ def _run_pins():
         lambda: r.test_brute_force(16, 8, "normal"), r.test_invariants,
         lambda: p.test_worked_example(GOLDEN), lambda: p.test_brute_force(37, 2, 8, 16, 0.8),
         p.test_round_trip_and_layout, p.test_fp8_scales_follow_rows,
+        lambda: p.test_masked_worked_example(GOLDEN), lambda: p.test_masked_brute_force(37, 2, 8, 0.8),
+        p.test_masked_round_trip_and_regions,
         lambda: f.test_basis_closed_form(GOLDEN), lambda: f.test_formats(GOLDEN), f.test_block_dequant,
         f.test_dense_gate_matrix_form, f.test_identical_experts_reduce_to_dense_ffn, f.test_combine_properties,
         f.test_permute_combine_round_trip_is_identity, f.test_fp8_path_dequantizes_same_codes,
@@ -64,6 +66,12 @@ MUTANTS = [
     ("permute: padding ignored", "-(-counts[e] // row_align) * row_align", "counts[e]"),
     ("permute: rows in descending order", 'kind="stable")]', 'kind="stable")][::-1]'),
     ("permute: wrong source token", "x[row_to_assign[valid] // k]", "x[row_to_assign[valid] % k]"),
+    ("masked: region start off by one", "offsets = np.arange(E_local + 1, dtype=np.int64) * slots",
+     "offsets = np.arange(E_local + 1, dtype=np.int64) * slots + 1"),
+    ("masked: rows in descending order", "for a in range(T * k):                          # ascending a",
+     "for a in reversed(range(T * k)):                # ascending a"),
+    ("masked: wrong source token", "xp[valid] = x[row_to_assign[valid] // k]\n        res.x_perm = xp\n        if x_scales is not None:\n            xs = np.zeros((cap,) + x_scales.shape[1:], dtype=x_scales.dtype)\n            xs[valid] = x_scales[row_to_assign[valid] // k]\n            res.x_perm_scales = xs\n    return res\n\n\n# -----",
+     "xp[valid] = x[row_to_assign[valid] % k]\n        res.x_perm = xp\n        if x_scales is not None:\n            xs = np.zeros((cap,) + x_scales.shape[1:], dtype=x_scales.dtype)\n            xs[valid] = x_scales[row_to_assign[valid] // k]\n            res.x_perm_scales = xs\n    return res\n\n\n# -----"),
     ("ffn: up used as gate", "g = x_rows @ w_gate.T", "g = x_rows @ w_up.T"),
     ("ffn: sigmoid instead of silu", "h = g / (1.0 + np.exp(-g)) * u", "h = 1.0 / (1.0 + np.exp(-g)) * u"),
     ("ffn: gate/up halves swapped", "return gu[:I], gu[I:], wd", "return gu[I:], gu[:I], wd"),

@@ -95,3 +95,82 @@ def test_rejects_bad_ids():
         oracle.permute(np.array([[0, -2]], np.int32), 4, 1)
     with pytest.raises(ValueError):
         oracle.permute(np.array([[0, 1]], np.int32), 4, 4, capacity=4)
+
+
+# ----------------------------------------------------------------------------- masked layout
+
+def brute_permute_masked(ids, E_local, slots):
+    T, k = ids.shape
+    flat = ids.reshape(-1).tolist()
+    counts = [0] * E_local
+    r2a = [-1] * (E_local * slots)
+    a2r = [-1] * (T * k)
+    for a in range(T * k):
+        e = flat[a]
+        if e < 0:
+            continue
+        row = e * slots + counts[e]
+        counts[e] += 1
+        r2a[row] = a
+        a2r[a] = row
+    return counts, [e * slots for e in range(E_local + 1)], r2a, a2r
+
+
+def test_masked_worked_example(golden_dir):
+    g = json.load(open(os.path.join(golden_dir, "permute_masked_worked.json")))
+    ids = np.array(g["ids"], dtype=np.int32)
+    x = np.array(g["x"], dtype=np.uint16)
+    p = oracle.permute_masked(ids, g["E_local"], g["slots"], x)
+    np.testing.assert_array_equal(p.counts, g["counts"])
+    np.testing.assert_array_equal(p.offsets, g["offsets"])
+    np.testing.assert_array_equal(p.row_to_assign, g["row_to_assign"])
+    np.testing.assert_array_equal(p.assign_to_row, g["assign_to_row"])
+    np.testing.assert_array_equal(p.x_perm, np.array(g["x_perm"], dtype=np.uint16))
+
+
+@pytest.mark.parametrize("T,k,E,p_local", [(1, 1, 1, 1.0), (37, 2, 8, 0.8), (64, 8, 32, 0.3), (50, 3, 4, 0.0)])
+def test_masked_brute_force(T, k, E, p_local):
+    rng = np.random.default_rng(T * 3 + k + E)
+    ids = np.stack([rng.permutation(E)[:k] if k <= E else rng.integers(0, E, k) for _ in range(T)]).astype(np.int32)
+    ids[rng.random((T, k)) >= p_local] = -1
+    slots = (T + 31) // 32 * 32
+    p = oracle.permute_masked(ids, E, slots)
+    c, o, r2a, a2r = brute_permute_masked(ids, E, slots)
+    np.testing.assert_array_equal(p.counts, c)
+    np.testing.assert_array_equal(p.offsets, o)
+    np.testing.assert_array_equal(p.row_to_assign, r2a)
+    np.testing.assert_array_equal(p.assign_to_row, a2r)
+
+
+def test_masked_round_trip_and_regions():
+    """Every local slot has its own row inside its expert's region, in
+    ascending assignment order, and the gathered row is a bitwise copy of the
+    token's activations; rows past a region's count are -1 / zero."""
+    rng = np.random.default_rng(13)
+    T, k, E, H = 200, 4, 12, 16
+    ids = np.stack([rng.permutation(E)[:k] for _ in range(T)]).astype(np.int32)
+    ids[rng.random((T, k)) < 0.3] = -1
+    x = rng.integers(0, 65535, size=(T, H)).astype(np.uint16)
+    slots = 224
+    p = oracle.permute_masked(ids, E, slots, x)
+    flat = ids.reshape(-1)
+    assert int(p.counts.sum()) == int(np.count_nonzero(flat >= 0))
+    for e in range(E):
+        region = p.row_to_assign[e * slots:(e + 1) * slots]
+        mine = region[:p.counts[e]]
+        assert np.all(np.diff(mine) > 0)                    # ascending a
+        assert np.all(flat[mine] == e)
+        assert np.all(region[p.counts[e]:] == -1)
+    for a in range(T * k):
+        r = p.assign_to_row[a]
+        if flat[a] < 0:
+            assert r == -1
+            continue
+        assert p.row_to_assign[r] == a
+        assert np.array_equal(p.x_perm[r], x[a // k])
+    assert np.all(p.x_perm[p.row_to_assign < 0] == 0)
+
+
+def test_masked_rejects_small_regions():
+    with pytest.raises(ValueError):
+        oracle.permute_masked(np.array([[0, 1], [0, 2]], np.int32), 3, 1)
