@@ -10,18 +10,22 @@ the mixed prefill+decode configuration: 4 layers x (8192 prefill + 1024 decode
 tokens), 32 of 256 experts local, top-8, hidden 3072, expert intermediate
 1536, bf16, in one persistent launch; decode layer 0 is released 10 us after
 the launch starts, each later layer of a phase when that phase's previous
-layer is done (+20 us for decode), decode quota 88 of 256 workgroups.
+layer is done (+20 us for decode), decode quota 64 of 256 workgroups (the
+configuration's 25% of the CUs).
 
 Prints ONE JSON line.  value = routed-expert TFLOP/s of the whole step
 (6*H*I flop per local routed row).  roofline = the persistent FFN kernel
-against its bound (algorithmic bytes: each op's active expert weights once
-plus x_perm in and y_perm out; flops 6*H*I per row), its mean duration over
-the timed steps from HIP events on its stream; traffic = HBM bytes per launch
-from the committed rocprofv3 counter record when it was taken on the current
-kernel sources, else null.  decode_tile_latency comes from one extra traced
-launch, and from a launch of the decode ops alone (same inputs and release
-chain) for the latency without prefill load.  cpu_baseline = the float64 CPU
-oracle over the whole workload, on this host's cores.
+against its bound (algorithmic bytes: the weights of every (layer, expert)
+that receives a row, once per launch -- a layer's prefill and decode ops share
+them -- plus the activation rows in and y_perm rows out; flops 6*H*I per row),
+its mean duration over the timed steps from HIP events on its stream; traffic
+= HBM bytes per launch from the committed rocprofv3 counter record when it was
+taken on the current kernel sources, else null.  decode_tile_latency comes
+from one extra traced launch, and from a launch of the decode ops alone (same
+inputs and release chain) for the latency without prefill load.
+cpu_baseline = the float64 CPU oracle over the whole workload, on this host's
+cores; its outputs are then compared with the GPU's outputs of the last timed
+step (parity: per-token normwise error and the whole-tensor figure).
 """
 from __future__ import annotations
 
@@ -36,6 +40,10 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+# The pipeline the benchmark times (tests build the same one from here).
+DEFAULTS = dict(quota=64, decode_layout="masked", prefill_layout="contiguous", fused_combine=False,
+                group_row_tiles=0, gather="fused")
+
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0}
 TICK_NS = 10.0
@@ -47,10 +55,12 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", type=int, default=4, help="workload configuration (1-5); default 4")
-    ap.add_argument("--quota", type=int, default=88, help="decode quota q in workgroups")
-    ap.add_argument("--decode-layout", choices=["masked", "contiguous"], default="masked",
+    ap.add_argument("--quota", type=int, default=DEFAULTS["quota"], help="decode quota q in workgroups")
+    ap.add_argument("--decode-layout", choices=["masked", "contiguous"], default=DEFAULTS["decode_layout"],
                     help="masked: decode ops' rows placed by routing in per-expert regions (no permute pass); "
                          "contiguous: permuted like prefill")
+    ap.add_argument("--prefill-layout", choices=["masked", "contiguous"], default=DEFAULTS["prefill_layout"],
+                    help="the same choice for prefill ops")
     ap.add_argument("--fused-combine", action="store_true",
                     help="combine tiles inside the persistent kernel instead of a separate combine launch")
     ap.add_argument("--group-row-tiles", type=int, default=0,
@@ -93,23 +103,46 @@ def build_specs(cfg, dev):
     return specs, layers
 
 
+def pipeline_kwargs(quota=DEFAULTS["quota"], decode_layout=DEFAULTS["decode_layout"],
+                    prefill_layout=DEFAULTS["prefill_layout"], fused_combine=DEFAULTS["fused_combine"],
+                    group_row_tiles=DEFAULTS["group_row_tiles"], gather=DEFAULTS["gather"]):
+    """MoEPipeline arguments of a benchmark configuration (the masked layouts
+    need the fused gather)."""
+    fused = gather == "fused"
+    return dict(decode_quota_wg=quota, fused_gather=fused, fused_combine=fused_combine,
+                masked_decode=decode_layout == "masked" and fused, masked_prefill=prefill_layout == "masked" and fused,
+                group_row_tiles=group_row_tiles)
+
+
 def algorithmic_work(pipe, cfg):
-    """flops and HBM bytes the method itself must move, per persistent launch."""
+    """flops and HBM bytes the method itself must move, per persistent launch.
+
+    Weights: every (layer, local expert) that receives at least one row, once
+    per launch (the prefill and decode ops of a layer share the layer's
+    experts).  Activations: each routed row read once, its y_perm row written
+    once.  Also returns the weight bytes counted once per op instead (what a
+    schedule that never shares a fetch between the phases must move)."""
     b_w = 1 if cfg.dtype == "fp8" else 2
     b_x = 1 if cfg.dtype == "fp8" else 2
+    w_expert = 3.0 * cfg.H * cfg.I * b_w
+    if cfg.dtype == "fp8":
+        w_expert += 3.0 * (cfg.H // 128) * (cfg.I // 128) * 4
     flops = 0.0
-    bytes_ = 0.0
+    act_bytes = 0.0
+    per_op_w = 0.0
     rows_total = 0
+    active_by_layer = {}
     for b in pipe.bufs:
         counts = b.counts.cpu().numpy()
         R = int(counts.sum())
-        active = int(np.count_nonzero(counts))
         rows_total += R
         flops += 6.0 * cfg.H * cfg.I * R
-        bytes_ += active * 3.0 * cfg.H * cfg.I * b_w + R * cfg.H * (b_x + 2)
-        if cfg.dtype == "fp8":
-            bytes_ += active * 3.0 * (cfg.H // 128) * (cfg.I // 128) * 4 + R * (cfg.H // 128) * 4
-    return flops, bytes_, rows_total
+        act_bytes += R * cfg.H * (b_x + 2) + (R * (cfg.H // 128) * 4 if cfg.dtype == "fp8" else 0)
+        per_op_w += int(np.count_nonzero(counts)) * w_expert
+        lay = active_by_layer.setdefault(b.spec.layer, np.zeros(len(counts), dtype=bool))
+        lay |= counts > 0
+    unique_w = sum(int(v.sum()) for v in active_by_layer.values()) * w_expert
+    return flops, unique_w + act_bytes, rows_total, per_op_w + act_bytes
 
 
 def decode_latency(pipe, specs):
@@ -139,11 +172,23 @@ def decode_latency(pipe, specs):
         lat.extend(us(mine["t_end"]).tolist())
         waits.append(float(us(mine["t_start"]).min()))
         op_lat.append(float(us(mine["t_end"]).max()))
+    tiles = {}
+    for ph, pname in ((0, "prefill"), (1, "decode")):
+        ops_ph = [i for i, s in enumerate(specs) if s.phase == ph]
+        for stage in (1, 2):
+            sel = np.isin(tr["op"], ops_ph) & (tr["stage"] == stage)
+            if not np.any(sel):
+                continue
+            d = (tr["t_end"][sel].astype(np.float64) - tr["t_start"][sel]) * TICK_NS / 1000.0
+            tiles[f"{pname}_gemm{stage}"] = {"n": int(sel.sum()),
+                                             **{f"p{q}_us": round(float(np.percentile(d, q)), 2) for q in (10, 50, 90, 99)},
+                                             "max_us": round(float(d.max()), 2)}
     if not lat:
-        return None
+        return {"tile_duration": tiles}
     pre = np.isin(tr["op"], [i for i, s in enumerate(specs) if s.phase == 0])
     ptd = (tr["t_end"][pre].astype(np.float64) - tr["t_start"][pre]) * TICK_NS / 1000.0
-    return {"tile_p50_us": round(float(np.percentile(lat, 50)), 2),
+    return {"tile_duration": tiles,
+            "tile_p50_us": round(float(np.percentile(lat, 50)), 2),
             "tile_p99_us": round(float(np.percentile(lat, 99)), 2),
             "preempt_wait_max_us": round(max(waits), 2), "preempt_wait_mean_us": round(float(np.mean(waits)), 2),
             "decode_op_latency_us": [round(v, 1) for v in op_lat],
@@ -151,9 +196,10 @@ def decode_latency(pipe, specs):
             "prefill_tile_p50_us": round(float(np.percentile(ptd, 50)), 2) if len(ptd) else None}
 
 
-def cpu_baseline(cfg, layers):
+def cpu_baseline(cfg, layers, outputs=None):
     """The oracle as it stands, on the same workload: every operation of every
-    layer (all tokens, every step of the path), on this host's cores."""
+    layer (all tokens, every step of the path), on this host's cores.  When
+    `outputs` (the oracle's y per op, in op order) is a list, it is filled."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -167,6 +213,8 @@ def cpu_baseline(cfg, layers):
             res = oracle.moe_local_share(ph.logits, ph.x, lay.weights, cfg.top_k, cfg.local_begin, cfg.E_local,
                                          128, x_scales=ph.x_scales)
             dt += time.perf_counter() - t
+            if outputs is not None:
+                outputs.append(res["y"])
             R = int(res["perm"].counts.sum())
             rows += R
             flops += 6.0 * cfg.H * cfg.I * R
@@ -174,6 +222,25 @@ def cpu_baseline(cfg, layers):
     return {"value": round(flops / dt / 1e12, 5), "unit": "TFLOP/s", "cores": int(cores), "kind": "oracle",
             "sample": f"the whole workload: {cfg.n_layers} layer(s) x ({desc} tokens), {rows} local rows, every "
                       f"step of the path, float64 numpy, {dt:.1f} s"}
+
+
+def output_parity(pipe, want, tol):
+    """GPU y of every op against the oracle's: the largest per-token normwise
+    relative error (tokens whose oracle output is exactly zero must be exactly
+    zero on the GPU) and the whole-tensor max|y - y_ref| / max|y_ref|."""
+    worst, whole, zeros_ok = 0.0, 0.0, True
+    for b, ref in zip(pipe.bufs, want):
+        y = b.y.float().cpu().numpy().astype(np.float64)
+        nw = np.linalg.norm(ref, axis=1)
+        z = nw == 0
+        zeros_ok &= bool(np.all(y[z] == 0.0))
+        if np.any(~z):
+            worst = max(worst, float(np.max(np.linalg.norm(y[~z] - ref[~z], axis=1) / nw[~z])))
+        m = float(np.abs(ref).max())
+        if m > 0:
+            whole = max(whole, float(np.abs(y - ref).max()) / m)
+    return {"per_token_normwise_max": float(f"{worst:.3e}"), "whole_tensor_max_rel": float(f"{whole:.3e}"),
+            "zero_tokens_exact": zeros_ok, "tolerance": tol, "ok": bool(worst <= tol and zeros_ok)}
 
 
 def traffic_record(workload):
@@ -223,11 +290,9 @@ def main():
     t_gen = time.perf_counter()
     specs, layers = build_specs(cfg, dev)
     t_gen = time.perf_counter() - t_gen
-    fused = args.gather == "fused"
-    masked = args.decode_layout == "masked" and fused     # the masked layout needs the fused gather
-    pipe = MoEPipeline(specs, decode_quota_wg=args.quota, fused_gather=fused,
-                       fused_combine=args.fused_combine, masked_decode=masked,
-                       group_row_tiles=args.group_row_tiles)
+    pkw = pipeline_kwargs(args.quota, args.decode_layout, args.prefill_layout, args.fused_combine,
+                          args.group_row_tiles, args.gather)
+    pipe = MoEPipeline(specs, **pkw)
     stream = torch.cuda.current_stream()
 
     for _ in range(args.warmup):
@@ -253,11 +318,9 @@ def main():
     ffn_ms = float(np.mean(ffn_all))
     ms_step = wall * 1000.0 / args.steps
 
-    flops, abytes, rows = algorithmic_work(pipe, cfg)
+    flops, abytes, rows, abytes_per_op = algorithmic_work(pipe, cfg)
     # one more launch with the per-tile trace for the decode latency figures
-    traced = MoEPipeline(specs, decode_quota_wg=args.quota, trace_capacity=1 << 18, fused_gather=fused,
-                       fused_combine=args.fused_combine, masked_decode=masked,
-                         group_row_tiles=args.group_row_tiles)
+    traced = MoEPipeline(specs, trace_capacity=1 << 18, **pkw)
     traced.run()
     torch.cuda.synchronize()
     if args.dump_trace:
@@ -271,10 +334,8 @@ def main():
     # the decode ops alone (same inputs, same release chain): the latency without prefill load
     excl = None
     dec_specs = phase_subset(specs, 1)
-    if lat is not None and dec_specs and len(dec_specs) < len(specs):
-        alone = MoEPipeline(dec_specs, decode_quota_wg=args.quota, trace_capacity=1 << 16, fused_gather=fused,
-                       fused_combine=args.fused_combine, masked_decode=masked,
-                            group_row_tiles=args.group_row_tiles)
+    if lat is not None and "tile_p99_us" in lat and dec_specs and len(dec_specs) < len(specs):
+        alone = MoEPipeline(dec_specs, trace_capacity=1 << 16, **pkw)
         alone.run()
         alone.run()
         torch.cuda.synchronize()
@@ -316,11 +377,19 @@ def main():
     roof["kernel_ms"] = round(ffn_ms, 4)
     roof["kernel_ms_p10_p50_p90"] = [round(float(np.percentile(ffn_all, q)), 4) for q in (10, 50, 90)]
     roof["alg_bytes"] = abytes
+    roof["alg_bytes_weights_once_per_op"] = abytes_per_op
     roof["alg_flops"] = flops
+    roof["achieved_tflops"] = round(flops / (ffn_ms * 1e-3) / 1e12, 2)
+    roof["frac_mfma"] = round(flops / (ffn_ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS[dtype], 4)
+    roof["frac_hbm"] = round(abytes / (ffn_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
 
     cpu = None
+    parity = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, layers)
+        want = []
+        cpu = cpu_baseline(cfg, layers, want)
+        parity = output_parity(pipe, want, 3e-2 if dtype == "fp8" else 1e-2)
+        del want
 
     out = {
         "metric": "routed-expert TFLOP/s + HBM GB/s per MI355X (mixed P/D); decode p99 tile latency",
@@ -341,12 +410,14 @@ def main():
                    "hidden": cfg.H, "intermediate": cfg.I, "decode_quota_wg": args.quota,
                    "group_row_tiles": args.group_row_tiles,
                    "gather": args.gather, "combine": "fused" if args.fused_combine else "separate",
-                   "decode_layout": "masked" if masked else "contiguous", "local_rows": rows},
+                   "decode_layout": "masked" if pkw["masked_decode"] else "contiguous",
+                   "prefill_layout": "masked" if pkw["masked_prefill"] else "contiguous", "local_rows": rows},
         "hbm_gbps_alg": round(abytes / (ffn_ms * 1e-3) / 1e9, 1),
         "ffn_tflops": round(flops / (ffn_ms * 1e-3) / 1e12, 2),
         "decode_tile_latency": lat,
         "roofline": roof,
         "cpu_baseline": cpu,
+        "parity_vs_oracle": parity,
         "input_gen_s": round(t_gen, 1),
     }
     print(json.dumps(out))

@@ -101,25 +101,37 @@ typedef struct moe_route_args {
      * a fixed region of `slots` rows per local expert and a per-expert count,
      * filled as routing decides, with no packing pass).  With counts non-NULL
      * the entry also places every local slot a = t*top_k + j of expert e at
-     * row e*slots + (counts[e] before an atomic increment) and writes
-     * assign_to_row[a] (-1 for a slot that is not local) and row_to_assign[row].
-     * counts must be zero on entry; the row order inside a region follows the
-     * atomics (any order is a valid layout: rows are computed independently).
-     * slots: a multiple of 32 and >= T (a token has at most one slot per
-     * expert).  clear (E_local ints, or NULL) is zeroed by the same launch, so
-     * a caller alternating two count arrays never needs a separate reset.
+     * row e*slots + (the number of assignments a' < a of expert e), so the
+     * rows of a region are its assignments in ascending a (deterministic,
+     * bit-exact), and writes assign_to_row[a] (-1 for a slot that is not
+     * local), row_to_assign[row] and counts[e] (no zeroing needed before).
      * The FFN then takes counts, offsets[e] = e*slots (offsets[E_local] =
      * E_local*slots) and capacity E_local*slots; moe_permute is not called.
      * Rows of a region past its count keep stale row_to_assign entries; the
      * FFN's gather bounds every entry by T*top_k and their outputs are never
-     * read.  With counts NULL the remaining fields are ignored. */
+     * read.
+     *  slots     a multiple of 32, >= T (a token has at most one slot per expert)
+     *  place_ws  moe_route_place_workspace_bytes(T, E_local) bytes of device
+     *            memory, 8-byte aligned, zero before its first use (allocate
+     *            it zeroed); the call leaves it ready for the next call with
+     *            the same or a smaller T.  Calls that share it must not
+     *            overlap in time.
+     *  error_flag NULL or a device i32 status word: MOE_ERR_INTERNAL if
+     *            place_ws was not zero before its first use, MOE_ERR_TIMEOUT
+     *            if a wait for another block's counts exceeded its bound
+     * Limits: 1 <= T < 2^29, E_local <= 1024, top_k <= 32.
+     * With counts NULL the remaining fields are ignored. */
     int32_t slots, pad0;
     int32_t* counts;
-    int32_t* clear;
+    void* place_ws;
     int32_t* assign_to_row;
     int32_t* row_to_assign;
+    int32_t* error_flag;
 } moe_route_args;
 moe_status_t moe_topk_route_batch(const moe_route_args* ops, int32_t n_ops, void* stream);
+/* Bytes of place_ws a masked entry with T tokens and E_local experts needs
+ * (0 if T < 1 or E_local < 1). */
+size_t moe_route_place_workspace_bytes(int32_t T, int32_t E_local);
 
 /* ------------------------------------------------------------------------- a2
  * Permutation into per-expert contiguous segments at final offsets
@@ -388,6 +400,25 @@ moe_status_t moe_combine_batch(const moe_combine_args* ops, int32_t n_ops, void*
 int32_t moe_x_moe(const int32_t* counts_host, int32_t E_local, int32_t M_t);
 int32_t moe_decode_quota(int32_t q, int32_t x_moe, int32_t x_moe_expected, int32_t q_max,
                          int32_t round_multiple);
+
+/* The tile layout the persistent kernel builds when it instantiates one
+ * operation ("Tile-Level Scheduling"; Eq. (3)), computed on the host with the
+ * kernel's own index arithmetic, for inspection and testing:
+ *  counts, offsets  [E_local], [E_local] host arrays (as moe_permute writes them)
+ *  M_t              the op class's row-tile height (moe_ffn_tile_shape bm)
+ *  gmax             group_row_tiles (the kernel's default is 8)
+ *  n1, n2           GEMM-1 / GEMM-2 column blocks (I/(bn/2), H/bn)
+ * Writes, for each row tile p < x_moe: row_tiles[4p..4p+3] = expert, row tile
+ * within the expert, valid rows, first row; groups[2p..2p+1] = first row
+ * tile and size of its weight-sharing group; for each XCD queue x < 8:
+ * queues[2x..2x+1] = first row tile, row tiles; and for every tile of every
+ * queue in claim order: tiles[4i..4i+3] = queue, stage (1 or 2), row tile,
+ * column block.  Returns x_moe, -1 on bad arguments or too small arrays
+ * (max_row_tiles entries of row_tiles/groups, max_tiles of tiles), -2 if a
+ * claim would resolve differently on workgroups of different XCDs. */
+int32_t moe_sched_layout(const int32_t* counts, const int32_t* offsets, int32_t E_local, int32_t M_t, int32_t gmax,
+                         int32_t n1, int32_t n2, int32_t max_row_tiles, int32_t* row_tiles, int32_t* groups,
+                         int32_t* queues, int64_t max_tiles, int32_t* tiles);
 
 /* sizeof() of the ABI structs, so bindings can check their layout:
  * 0 moe_op_desc, 1 moe_sched_config, 2 moe_trace_rec, 3 moe_op_stats,

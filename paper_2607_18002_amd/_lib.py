@@ -73,7 +73,8 @@ class RouteArgs(C.Structure):
     _fields_ = [
         ("logits", _p), ("T", _i32), ("E_global", _i32), ("top_k", _i32), ("local_begin", _i32),
         ("E_local", _i32), ("topk_ids", _p), ("topk_w", _p),
-        ("slots", _i32), ("pad0", _i32), ("counts", _p), ("clear", _p), ("assign_to_row", _p), ("row_to_assign", _p),
+        ("slots", _i32), ("pad0", _i32), ("counts", _p), ("place_ws", _p), ("assign_to_row", _p), ("row_to_assign", _p),
+        ("error_flag", _p),
     ]
 
 
@@ -100,6 +101,7 @@ PROTOTYPES = {
     "moe_permute_batch": (_i32, [C.POINTER(PermuteArgs), _i32, _p]),
     "moe_combine_batch": (_i32, [C.POINTER(CombineArgs), _i32, _p]),
     "moe_permute_workspace_bytes": (C.c_size_t, [_i32, _i32, _i32]),
+    "moe_route_place_workspace_bytes": (C.c_size_t, [_i32, _i32]),
     "moe_permute": (_i32, [_p, _i32, _i32, _i32, _p, _i32, _p, _i32, _i32, _i32,
                            _p, _p, _p, _p, _p, _p, _p, _p, _p]),
     "moe_ffn_row_align": (_i32, [_i32, _i32]),
@@ -110,6 +112,7 @@ PROTOTYPES = {
     "moe_pack_weights": (_i32, [_p, _p, _i32, _i32, _i32, _i32, _p]),
     "moe_x_moe": (_i32, [C.POINTER(_i32), _i32, _i32]),
     "moe_decode_quota": (_i32, [_i32, _i32, _i32, _i32, _i32]),
+    "moe_sched_layout": (_i32, [_p, _p, _i32, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _i64, _p]),
     "moe_abi_sizeof": (C.c_size_t, [_i32]),
     "moe_status_string": (C.c_char_p, [_i32]),
     "moe_last_error": (C.c_char_p, []),

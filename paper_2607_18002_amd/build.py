@@ -24,7 +24,8 @@ SOURCES = ["api.cpp", "route.hip", "permute.hip", "combine.hip", "ffn.hip", "pac
 # recorded hardware-counter figures to the kernel they were taken on).
 FFN_KERNEL_SOURCES = ["paper_2607_18002_amd/csrc/ffn.hip", "paper_2607_18002_amd/csrc/tile_bf16.hpp",
                       "paper_2607_18002_amd/csrc/tile_bf16_tall.hpp", "paper_2607_18002_amd/csrc/tile_fp8.hpp",
-                      "paper_2607_18002_amd/csrc/common.hpp", "include/moe_apk.h"]
+                      "paper_2607_18002_amd/csrc/common.hpp", "paper_2607_18002_amd/csrc/sched_index.hpp",
+                      "include/moe_apk.h"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -5,7 +5,10 @@
 #include <cstring>
 #include <mutex>
 
+#include <vector>
+
 #include "common.hpp"
+#include "sched_index.hpp"
 
 namespace {
 thread_local char g_last_error[512] = "";
@@ -101,6 +104,96 @@ int32_t moe_x_moe(const int32_t* counts_host, int32_t E_local, int32_t M_t) {
 
 int32_t moe_decode_quota(int32_t q, int32_t x_moe, int32_t x_moe_expected, int32_t q_max, int32_t c) {
     return moeapk::decode_quota(q, x_moe, x_moe_expected, q_max, c);
+}
+
+int32_t moe_sched_layout(const int32_t* counts, const int32_t* offsets, int32_t E_local, int32_t M_t, int32_t gmax,
+                         int32_t n1, int32_t n2, int32_t max_row_tiles, int32_t* row_tiles, int32_t* groups,
+                         int32_t* queues, int64_t max_tiles, int32_t* tiles) {
+    namespace S = moeapk::sched;
+    if (!counts || !offsets || E_local < 1 || M_t < 1 || gmax < 1 || n1 < 1 || n2 < 1 || max_row_tiles < 0)
+        return -1;
+    std::vector<int32_t> scan(E_local);
+    int total = 0;
+    for (int e = 0; e < E_local; ++e) {
+        if (counts[e] < 0) return -1;
+        scan[e] = total;
+        total += S::row_tiles(counts[e], M_t);
+    }
+    if (total > max_row_tiles || total >= S::kMaxRowTiles || (int64_t)total * (n1 + n2) > max_tiles) return -1;
+    // the instantiation: table and group entries of every row tile
+    std::vector<uint64_t> table(total > 0 ? total : 1);
+    std::vector<uint32_t> grp(total > 0 ? total : 1);
+    for (int e = 0; e < E_local; ++e) {
+        const int c = counts[e], nt = S::row_tiles(c, M_t), pos = scan[e], ng = S::n_groups(nt, gmax);
+        for (int j = 0; j < ng; ++j) {
+            int glo, ghi;
+            S::group_range(nt, ng, j, glo, ghi);
+            for (int mb = glo; mb < ghi; ++mb) {
+                int first, rows;
+                S::tile_rows(c, nt, mb, first, rows);
+                table[pos + mb] = S::pack_entry(e, mb, rows, offsets[e] + first);
+                grp[pos + mb] = S::pack_group(pos + glo, ghi - glo);
+            }
+        }
+    }
+    for (int p = 0; p < total; ++p) {
+        int e, mb, rows, row0;
+        S::unpack_entry(table[p], e, mb, rows, row0);
+        row_tiles[4 * p] = e;
+        row_tiles[4 * p + 1] = mb;
+        row_tiles[4 * p + 2] = rows;
+        row_tiles[4 * p + 3] = row0;
+        groups[2 * p] = (int32_t)(grp[p] & 0xFFFFu);
+        groups[2 * p + 1] = (int32_t)(grp[p] >> 16);
+    }
+    int cut[S::kXcds + 1];
+    cut[0] = 0;
+    cut[S::kXcds] = total;
+    for (int x = 1; x < S::kXcds; ++x) cut[x] = S::queue_cut(x, scan.data(), E_local, total, gmax);
+    for (int x = 0; x < S::kXcds; ++x) {
+        queues[2 * x] = cut[x];
+        queues[2 * x + 1] = cut[x + 1] - cut[x];
+    }
+    // every claim of every queue, resolved as a workgroup of each XCD would
+    // resolve it (its LDS cache holds its own queue's entries when they fit);
+    // all eight must agree, as a claimed tile may be taken by any of them
+    int64_t n = 0;
+    for (int x = 0; x < S::kXcds; ++x) {
+        const int m_lo = cut[x], n_mt = cut[x + 1] - cut[x];
+        for (int t = 0; t < n_mt * (n1 + n2); ++t) {
+            int stage = 0, ref_mtile = -2, ref_nb = -2;
+            for (int y = 0; y < S::kXcds; ++y) {
+                // workgroup of XCD y: its cache holds its own queue's first cnt
+                // entries when cnt fits, and unfilled slots hold garbage
+                const int lo = cut[y], cnt = cut[y + 1] - cut[y];
+                uint32_t cache_g[S::kTabCache];
+                uint64_t cache_e[S::kTabCache];
+                for (int i = 0; i < S::kTabCache; ++i) {
+                    const bool filled = cnt <= S::kTabCache && i < cnt;
+                    cache_g[i] = filled ? grp[lo + i] : 0xA5A5A5A5u;
+                    cache_e[i] = filled ? table[lo + i] : 0xA5A5A5A5A5A5A5A5ull;
+                }
+                int st, u, nn, p, mtile, nb;
+                S::queue_pos(t, n_mt, m_lo, n1, n2, st, u, nn, p);
+                const int cg = S::cache_slot(p, lo, cnt);
+                if (cg >= S::kTabCache) return -2;
+                const uint32_t g = cg >= 0 ? cache_g[cg] : (p >= 0 && p < total ? grp[p] : 0u);
+                S::group_tile(g, u, nn, m_lo, n_mt, p, mtile, nb);
+                if (y == 0) { stage = st; ref_mtile = mtile; ref_nb = nb; }
+                else if (mtile != ref_mtile || nb != ref_nb) return -2;
+                const int ce = S::cache_slot(mtile, lo, cnt);
+                if (ce >= S::kTabCache) return -2;
+                const uint64_t ent = ce >= 0 ? cache_e[ce] : (mtile >= 0 && mtile < total ? table[mtile] : 0ull);
+                if (mtile < 0 || ent != table[mtile]) return -2;
+            }
+            tiles[4 * n] = x;
+            tiles[4 * n + 1] = stage;
+            tiles[4 * n + 2] = ref_mtile;
+            tiles[4 * n + 3] = ref_nb;
+            ++n;
+        }
+    }
+    return total;
 }
 
 }  // extern "C"

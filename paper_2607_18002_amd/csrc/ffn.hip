@@ -42,6 +42,7 @@
 // workgroup that finishes it, before it publishes the done word.
 #include <cstring>
 
+#include "sched_index.hpp"
 #include "tile_bf16.hpp"
 #include "tile_bf16_tall.hpp"
 #include "tile_fp8.hpp"
@@ -49,18 +50,20 @@
 namespace {
 
 using namespace moeapk;
+using sched::kMaxRowTiles;
+using sched::kSegAlign;
+using sched::kTabCache;
+using sched::kXcds;
 
 using ShapeP = TileShape<192, 256, 64>;    // bf16 prefill: 192 x 256 tall tile, K step 64
 using ShapeD = TileShape<128, 256, 64>;    // bf16 decode : 128 x 256 tile, K step 64
 using ShapeF8 = TileShapeF8<128, 256>;     // fp8 (both phases): 128 x 256 tile, K step 128 (one scale block)
 constexpr int kMax2(int a, int b) { return a > b ? a : b; }
 constexpr int kLdsBytes = kMax2(kMax2(TallLds<ShapeP>::bytes, ShapeD::LDS), ShapeF8::LDS);
-constexpr int kMaxRowTiles = 1 << 14;      // per op (14-bit field of a table entry)
 // Expert segments are aligned to 32 rows (one MFMA row block).  An expert's m
 // rows are cut into ceil(m / M_t) row tiles of near-equal height in whole
 // 32-row blocks (M_t = the class's tallest tile), so the row tiles that share
-// a weight slice run about equally long and stay in step.
-constexpr int kSegAlign = 32;
+// a weight slice run about equally long and stay in step (sched_index.hpp).
 
 enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1, CLS_FP8 = 2 };
 enum : int32_t { ST_WAIT = 0, ST_INIT = 1, ST_ACTIVE = 2, ST_DONE = 3, ST_FINISHING = 4, ST_COMBINING = 5 };
@@ -139,7 +142,6 @@ struct Hdr {
 // activation rows and h of a row tile and the weight slices of a group stay
 // in one L2; a workgroup whose queue is empty steals from the others.  claim
 // is an atomic counter; size / m_lo / n_mt are written once at instantiation.
-constexpr int kXcds = 8;
 struct XQueue {
     int32_t claim, size, m_lo, n_mt;
     char pad[128 - 16];
@@ -167,33 +169,6 @@ __device__ __forceinline__ OpDyn* dyn_of(char* ws) { return (OpDyn*)(ws + kDynOf
 __device__ __forceinline__ OpStatic* static_of(char* ws) { return (OpStatic*)(ws + kStaticOff); }
 __device__ __forceinline__ char* arr_of(char* ws) { return ws + kArraysOff; }
 __device__ __forceinline__ XQueue* xq_of(char* ws, int o, int x) { return (XQueue*)(ws + kXqOff) + o * kXcds + x; }
-
-// Tile t of a queue holding n_mt row tiles starting at m_lo: its stage and
-// the row tile p whose group holds it (a group of s row tiles starting at f
-// owns the tile numbers [(f - m_lo) * nn, (f - m_lo + s) * nn) of its stage).
-__device__ __forceinline__ void queue_pos(int t, int n_mt, int m_lo, int n1, int n2, int& stage, int& u, int& nn, int& p) {
-    const int n1x = n_mt * n1;
-    u = t;
-    nn = n1;
-    stage = 1;
-    if (t >= n1x) { stage = 2; u = t - n1x; nn = n2; }
-    p = m_lo + u / nn;
-}
-// ... then, with that group's entry g: column block and row tile (nb < 0: the entry is not a valid group of p).
-__device__ __forceinline__ void group_tile(uint32_t g, int u, int nn, int m_lo, int n_mt, int p, int& mtile, int& nb) {
-    const int f = (int)(g & 0xFFFFu), sz = (int)(g >> 16);
-    if (sz < 1 || f < m_lo || p < f || p >= f + sz || f + sz > m_lo + n_mt) { nb = -1; mtile = -1; return; }
-    const int w = u - (f - m_lo) * nn;
-    nb = w / sz;
-    mtile = f + (w - nb * sz);
-}
-
-// A row-tile table entry packs everything a claim needs into one 64-bit word:
-// bits 0-9 expert, 10-23 row block, 24-31 valid rows, 32-63 first row.
-__device__ __forceinline__ uint64_t pack_entry(int e, int mb, int rows, int row0) {
-    return (uint64_t)(uint32_t)e | ((uint64_t)(uint32_t)mb << 10) | ((uint64_t)(uint32_t)rows << 24) |
-           ((uint64_t)(uint32_t)row0 << 32);
-}
 
 // ----------------------------------------------------------------------------- init
 struct InitArgs {
@@ -388,7 +363,6 @@ __device__ void run_combine(const OpArg& op, int t, char* lds, int32_t* status) 
 // causally after the op became ACTIVE: the range [lo, lo + cnt) of row tiles and,
 // when cnt <= kTabCache, their table entries.  Later claims cost one atomic and
 // an LDS read.  lo = -1: not taken yet.
-constexpr int kTabCache = 64;
 struct TabCache {
     uint64_t ent[MOE_MAX_OPS][kTabCache];
     uint32_t grp[MOE_MAX_OPS][kTabCache];
@@ -503,20 +477,19 @@ __device__ bool take_tile(const KArgs& a, int o, int src, int t, int myx, TabCac
     }
     if (lane == 0) {
         int stage, u, nn, p, mtile, nb;
-        queue_pos(t, n_mt, m_lo, op.n1, op.n2, stage, u, nn, p);
+        sched::queue_pos(t, n_mt, m_lo, op.n1, op.n2, stage, u, nn, p);
         const int lo = tab->lo[o];
         const int cnt = tab->cnt[o];
-        const bool cached = lo >= 0 && cnt <= kTabCache;   // entries of the own queue's row tiles
-        const uint32_t g = (cached && p >= lo && p < lo + cnt) ? tab->grp[o][p - lo]
-                           : (p >= 0 && p < op.max_mtiles ? ld_relaxed_agent(grp + p) : 0u);
-        group_tile(g, u, nn, m_lo, n_mt, p, mtile, nb);
-        const uint64_t ent = (cached && mtile >= lo && mtile < lo + cnt) ? tab->ent[o][mtile - lo]
+        const int cg = sched::cache_slot(p, lo, cnt);          // entries of the own queue's row tiles
+        const uint32_t g = cg >= 0 ? tab->grp[o][cg] : (p >= 0 && p < op.max_mtiles ? ld_relaxed_agent(grp + p) : 0u);
+        sched::group_tile(g, u, nn, m_lo, n_mt, p, mtile, nb);
+        const int ce = sched::cache_slot(mtile, lo, cnt);
+        const uint64_t ent = ce >= 0 ? tab->ent[o][ce]
                              : (mtile >= 0 && mtile < op.max_mtiles ? ld_relaxed_agent(table + mtile) : 0ull);
-        const int rows = (int)((ent >> 24) & 0xFF);
-        const int e = (int)(ent & 0x3FF);
-        const int row0 = (int)(ent >> 32);
+        int e, mblk, rows, row0;
+        sched::unpack_entry(ent, e, mblk, rows, row0);
         cmd->kind = CMD_TILE; cmd->op = o; cmd->stage = stage;
-        cmd->e = e; cmd->mblk = (int)((ent >> 10) & 0x3FFF);
+        cmd->e = e; cmd->mblk = mblk;
         cmd->row0 = row0; cmd->rows = rows; cmd->rows32 = (rows + 31) & ~31;
         // The tile descriptor must address memory inside the op's buffers;
         // if a scheduler invariant broke, stop instead of running the tile.
@@ -798,10 +771,7 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
     uint64_t* table = (uint64_t*)(arr_of(a.ws) + op.table_off);
     uint32_t* grp = (uint32_t*)(arr_of(a.ws) + op.grp_off);
     const int gmax = a.gmax;
-    for (int e = threadIdx.x; e < op.E; e += 256) {
-        const int c = op.counts[e];
-        scan[e] = c > 0 ? (c + op.mt - 1) / op.mt : 0;
-    }
+    for (int e = threadIdx.x; e < op.E; e += 256) scan[e] = sched::row_tiles(op.counts[e], op.mt);
     __syncthreads();
     __shared__ int32_t s_total, s_bad, s_cut[kXcds + 1];
     if (threadIdx.x == 0) {
@@ -813,20 +783,20 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
     __syncthreads();
     for (int e = threadIdx.x; e < op.E; e += 256) {
         const int c = op.counts[e];
-        const int nt = c > 0 ? (c + op.mt - 1) / op.mt : 0;      // Eq. (3): ceil(m_e / M_t) row tiles
+        const int nt = sched::row_tiles(c, op.mt);               // Eq. (3): ceil(m_e / M_t) row tiles
         const int nb32 = (c + kSegAlign - 1) / kSegAlign;        // 32-row blocks of the segment
         const int pos = scan[e];
         const int off = op.offsets[e];
         if (pos + nt > op.max_mtiles || off < 0 || (long)off + (long)nb32 * kSegAlign > op.capacity) { s_bad = 1; continue; }
-        const int ng = (nt + gmax - 1) / gmax;
+        const int ng = sched::n_groups(nt, gmax);
         for (int j = 0; j < ng; ++j) {                     // near-equal groups of this expert's row tiles
-            const int glo = (int)((long)nt * j / ng), ghi = (int)((long)nt * (j + 1) / ng);
+            int glo, ghi;
+            sched::group_range(nt, ng, j, glo, ghi);
             for (int mb = glo; mb < ghi; ++mb) {
-                // near-equal heights in whole 32-row blocks: tile mb holds blocks [b0, b1)
-                const int b0 = (int)((long)nb32 * mb / nt), b1 = (int)((long)nb32 * (mb + 1) / nt);
-                const int rows = (c < b1 * kSegAlign ? c : b1 * kSegAlign) - b0 * kSegAlign;
-                table[pos + mb] = pack_entry(e, mb, rows, off + b0 * kSegAlign);
-                grp[pos + mb] = (uint32_t)(pos + glo) | ((uint32_t)(ghi - glo) << 16);
+                int first, rows;
+                sched::tile_rows(c, nt, mb, first, rows);
+                table[pos + mb] = sched::pack_entry(e, mb, rows, off + first);
+                grp[pos + mb] = sched::pack_group(pos + glo, ghi - glo);
             }
         }
     }
@@ -834,22 +804,7 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
     // Queue cuts: cut x (1..kXcds-1) is the group boundary nearest to x/kXcds
     // of the row tiles (ties: the lower one), so no group spans two queues;
     // cuts are non-decreasing in x.
-    if (threadIdx.x >= 1 && threadIdx.x < kXcds) {
-        const int xm = s_total;
-        const int target = (int)((long)xm * threadIdx.x / kXcds);
-        int best = 0, bestd = 0x7fffffff;
-        for (int e = 0; e < op.E; ++e) {
-            const int pos = scan[e], nt = (e + 1 < op.E ? scan[e + 1] : xm) - pos;
-            if (nt <= 0 || target < pos || target > pos + nt) continue;
-            const int ng = (nt + gmax - 1) / gmax;
-            for (int j = 0; j <= ng; ++j) {
-                const int b = pos + (int)((long)nt * j / ng);
-                const int dd = b > target ? b - target : target - b;
-                if (dd < bestd) { bestd = dd; best = b; }
-            }
-        }
-        s_cut[threadIdx.x] = best;
-    }
+    if (threadIdx.x >= 1 && threadIdx.x < kXcds) s_cut[threadIdx.x] = sched::queue_cut(threadIdx.x, scan, op.E, s_total, gmax);
     __syncthreads();
     if (threadIdx.x == 0) {
         Hdr* hdr = hdr_of(a.ws);

@@ -15,6 +15,8 @@
 
 namespace {
 
+using moeapk::set_status;
+
 constexpr int kTokensPerBlock = 4;  // one wave each
 
 __device__ __forceinline__ uint32_t order_key(float v) {
@@ -96,22 +98,15 @@ __device__ __forceinline__ float wave_sum(float v) {
     return (r0 + r1) + (r2 + r3);
 }
 
-// One op's routing: block `blk` of the op handles tokens [4*blk, 4*blk + 4).
-// Masked layout outputs of an op (counts NULL: none).
-struct MaskedOut {
-    int32_t* counts;
-    int32_t* a2r;
-    int32_t* r2a;
-    int slots;
-};
-
+// One wave's token t: writes its ids and weights and returns, in lanes
+// j < k, the local expert of slot j (-1 if not local; -1 in every lane when
+// t >= T, which writes nothing).
 template <int EPL>
-__device__ __forceinline__ void route_block(const float* __restrict__ logits, int T, int E, int k, int local_begin,
-                                            int E_local, int32_t* __restrict__ ids, float* __restrict__ wts, int blk,
-                                            MaskedOut mo = MaskedOut{nullptr, nullptr, nullptr, 0}) {
+__device__ __forceinline__ int route_wave(const float* __restrict__ logits, int t, int T, int E, int k,
+                                          int local_begin, int E_local, int32_t* __restrict__ ids,
+                                          float* __restrict__ wts) {
     const int lane = threadIdx.x & 63;
-    const int t = blk * kTokensPerBlock + (threadIdx.x >> 6);
-    if (t >= T) return;  // wave-uniform
+    if (t >= T) return -1;  // wave-uniform
     const float* row = logits + (size_t)t * E;
     // all loads first (clamped in-row indices, no branches), so they are in flight together
     float v[EPL];
@@ -177,11 +172,8 @@ __device__ __forceinline__ void route_block(const float* __restrict__ logits, in
         }
     }
     }
-    // masked layout: claim the slot's row now, so the atomic's round trip overlaps the softmax
     const int loc = my_e - local_begin;
     const bool local = lane < k && loc >= 0 && loc < E_local;
-    int slot = 0;
-    if (mo.counts && local) slot = atomicAdd(mo.counts + loc, 1);
     const float my_v = key_value(my_key);
     const float m = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(my_v), 0));   // the largest selected logit
     const float ex = (lane < k) ? expf(my_v - m) : 0.f;
@@ -189,16 +181,143 @@ __device__ __forceinline__ void route_block(const float* __restrict__ logits, in
     if (lane < k) {
         ids[(size_t)t * k + lane] = local ? loc : -1;
         wts[(size_t)t * k + lane] = ex / s;
-        if (mo.counts) {                                 // masked layout: the next free row of the expert's region
-            const int a = t * k + lane;
-            int row = -1;
-            if (local && slot < mo.slots) {              // always, as slots >= T
-                row = loc * mo.slots + slot;
-                mo.r2a[row] = a;
-            }
-            mo.a2r[a] = row;
-        }
     }
+    return local ? loc : -1;
+}
+
+// Unmasked routing: block `blk` of the op handles tokens [4*blk, 4*blk + 4).
+template <int EPL>
+__device__ __forceinline__ void route_block(const float* __restrict__ logits, int T, int E, int k, int local_begin,
+                                            int E_local, int32_t* __restrict__ ids, float* __restrict__ wts,
+                                            int blk) {
+    route_wave<EPL>(logits, blk * kTokensPerBlock + (threadIdx.x >> 6), T, E, k, local_begin, E_local, ids, wts);
+}
+
+// ----------------------------------------------------------------------------- masked placement
+// Masked layout ("Prefill-Decode Disaggregation": a fixed region of `slots`
+// rows per local expert and a count, filled as routing decides): slot
+// a = t*k + j of local expert e goes to row e*slots + (number of earlier
+// assignments of e), so the rows of a region are its assignments in
+// ascending a -- the unique order the permutation uses, bit-exact and
+// independent of scheduling.
+//
+// A routing block of a masked op takes its chunk of 4 tokens from an ordered
+// ticket (so every chunk it waits for belongs to a block that has already
+// started), ranks its slots inside the chunk, publishes the chunk's
+// per-expert counts and finds the counts of all earlier chunks by a
+// decoupled look-back: walking back over the earlier chunks' records, summing
+// aggregates until one holds an inclusive prefix.  Each record is one 64-bit
+// word [generation | status | count], read and written with device-scope
+// atomics, so no fence is needed; the generation (taken with the ticket from
+// one word) makes records of earlier calls invalid without clearing them.
+// The block that draws the last ticket resets the ticket and advances the
+// generation; it also writes the counts (the inclusive prefix of the last
+// chunk).
+constexpr uint64_t kRecAgg = 1ull << 30, kRecIncl = 2ull << 30;
+constexpr uint32_t kRecCountMask = (1u << 30) - 1;
+constexpr int kPlaceHdrWords = 32;          // 256-byte header: the ticket word, alone in its line
+constexpr int kMaskedMaxE = 1024;
+constexpr int64_t kLookbackSpins = 1 << 22;
+
+__device__ __forceinline__ uint64_t rec_word(uint32_t gen, uint64_t status, uint32_t count) {
+    return ((uint64_t)gen << 32) | status | (uint64_t)(count & kRecCountMask);
+}
+
+struct MaskedArgs {
+    int32_t* counts;
+    int32_t* a2r;
+    int32_t* r2a;
+    uint64_t* ws;
+    int32_t* err;
+    int slots, nchunks;
+};
+
+template <int EPL>
+__device__ void route_block_masked(const float* __restrict__ logits, int T, int E, int k, int local_begin,
+                                   int E_local, int32_t* __restrict__ ids, float* __restrict__ wts,
+                                   const MaskedArgs m) {
+    __shared__ int s_chunk;
+    __shared__ uint32_t s_gen;
+    __shared__ int32_t s_sel[kTokensPerBlock][32];
+    __shared__ int32_t s_cnt[kMaskedMaxE];
+    __shared__ int32_t s_excl[kMaskedMaxE];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    if (tid == 0) {
+        const unsigned long long old = atomicAdd((unsigned long long*)m.ws, 1ull);
+        int c = (int)(uint32_t)old;
+        const uint32_t gen = (uint32_t)(old >> 32);
+        // the last ticket of the call: every other block has drawn its ticket already
+        if (c == m.nchunks - 1)
+            __hip_atomic_store(m.ws, (uint64_t)(gen + 1u) << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (c >= m.nchunks) {                     // the workspace was not zero before its first use
+            set_status(m.err, MOE_ERR_INTERNAL);
+            c = -1;
+        }
+        s_chunk = c;
+        s_gen = gen;
+    }
+    for (int e = tid; e < E_local; e += 256) s_cnt[e] = 0;
+    __syncthreads();
+    const int chunk = s_chunk;
+    if (chunk < 0) return;                        // block-uniform
+    const uint32_t gen = s_gen;
+    const int t = chunk * kTokensPerBlock + w;
+    const int loc = route_wave<EPL>(logits, t, T, E, k, local_begin, E_local, ids, wts);
+    if (lane < 32) s_sel[w][lane] = lane < k ? loc : -1;
+    if (loc >= 0) atomicAdd(&s_cnt[loc], 1);
+    __syncthreads();
+    // rank inside the chunk: the earlier tokens of the chunk that chose the same expert
+    int rank = 0;
+    if (loc >= 0)
+        for (int w2 = 0; w2 < w; ++w2)
+            for (int j = 0; j < k; ++j) rank += s_sel[w2][j] == loc;
+    uint64_t* rec = m.ws + kPlaceHdrWords + (size_t)chunk * E_local;
+    // publish first (chunk 0 holds its own inclusive prefix), then look back:
+    // a block waits only on the records of earlier chunks, so no wait is circular
+    for (int e = tid; e < E_local; e += 256)
+        __hip_atomic_store(rec + e, rec_word(gen, chunk == 0 ? kRecIncl : kRecAgg, (uint32_t)s_cnt[e]),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (int e = tid; e < E_local; e += 256) {
+        uint32_t excl = 0;
+        int64_t spins = 0;
+        for (int j = chunk - 1; j >= 0;) {
+            const uint64_t v = __hip_atomic_load(m.ws + kPlaceHdrWords + (size_t)j * E_local + e, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+            const uint64_t st = v & (3ull << 30);
+            if ((uint32_t)(v >> 32) != gen || st == 0) {         // chunk j has not published yet
+                if (++spins > kLookbackSpins) {
+                    set_status(m.err, MOE_ERR_TIMEOUT);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+                continue;
+            }
+            excl += (uint32_t)v & kRecCountMask;
+            if (st == kRecIncl) break;
+            --j;
+        }
+        if (chunk > 0)
+            __hip_atomic_store(rec + e, rec_word(gen, kRecIncl, excl + (uint32_t)s_cnt[e]), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        s_excl[e] = (int32_t)excl;
+    }
+    __syncthreads();
+    if (t < T && lane < k) {
+        const int a = t * k + lane;
+        int row = -1;
+        if (loc >= 0) {
+            const int r = s_excl[loc] + rank;
+            if (r < m.slots) {                    // always, as slots >= T
+                row = loc * m.slots + r;
+                m.r2a[row] = a;
+            } else {
+                set_status(m.err, MOE_ERR_CAPACITY);
+            }
+        }
+        m.a2r[a] = row;
+    }
+    if (chunk == m.nchunks - 1)
+        for (int e = tid; e < E_local; e += 256) m.counts[e] = s_excl[e] + s_cnt[e];
 }
 
 template <int EPL>
@@ -220,10 +339,14 @@ __global__ __launch_bounds__(256) void topk_route_batch_kernel(const RouteBatch 
     int o = 0;
     while (o + 1 < b.n && (int)blockIdx.x >= b.blk0[o + 1]) ++o;      // uniform
     const moe_route_args& a = b.op[o];
-    if (a.clear && (int)blockIdx.x == b.blk0[o])
-        for (int i = threadIdx.x; i < a.E_local; i += 256) a.clear[i] = 0;
+    if (a.counts) {
+        route_block_masked<EPL>(a.logits, a.T, a.E_global, a.top_k, a.local_begin, a.E_local, a.topk_ids, a.topk_w,
+                                MaskedArgs{a.counts, a.assign_to_row, a.row_to_assign, (uint64_t*)a.place_ws, a.error_flag,
+                                           a.slots, b.blk0[o + 1] - b.blk0[o]});
+        return;
+    }
     route_block<EPL>(a.logits, a.T, a.E_global, a.top_k, a.local_begin, a.E_local, a.topk_ids, a.topk_w,
-                     (int)blockIdx.x - b.blk0[o], MaskedOut{a.counts, a.assign_to_row, a.row_to_assign, a.slots});
+                     (int)blockIdx.x - b.blk0[o]);
 }
 
 moe_status_t check_route(const float* logits, int32_t T, int32_t E_global, int32_t top_k, int32_t local_begin,
@@ -264,6 +387,12 @@ extern "C" moe_status_t moe_topk_route(const float* logits, int32_t T, int32_t E
     return MOE_OK;
 }
 
+extern "C" size_t moe_route_place_workspace_bytes(int32_t T, int32_t E_local) {
+    if (T < 1 || E_local < 1) return 0;
+    const size_t chunks = (size_t)((T + kTokensPerBlock - 1) / kTokensPerBlock);
+    return (kPlaceHdrWords + chunks * (size_t)E_local) * sizeof(uint64_t);
+}
+
 extern "C" moe_status_t moe_topk_route_batch(const moe_route_args* ops, int32_t n_ops, void* stream) {
     using moeapk_host::fail;
     if (!ops || n_ops < 1 || n_ops > MOE_MAX_OPS)
@@ -278,14 +407,19 @@ extern "C" moe_status_t moe_topk_route_batch(const moe_route_args* ops, int32_t 
                                             a.topk_ids, a.topk_w);
         if (st != MOE_OK) return st;
         if (a.counts) {
-            if (a.slots < a.T || a.slots % 32 != 0 || (int64_t)a.slots * a.E_local > INT32_MAX)
-                return fail(MOE_ERR_INVALID_ARG, "moe_topk_route_batch: entry %d: slots=%d must be a multiple of 32, "
-                            ">= T=%d, slots*E_local < 2^31", o, a.slots, a.T);
-            if (!a.assign_to_row || !a.row_to_assign || a.clear == a.counts)
+            if (a.T < 1 || a.slots < a.T || a.slots % 32 != 0 || (int64_t)a.slots * a.E_local > INT32_MAX ||
+                a.T >= (1 << 29))
+                return fail(MOE_ERR_INVALID_ARG, "moe_topk_route_batch: entry %d: masked layout needs 1 <= T < 2^29 and "
+                            "slots (%d) a multiple of 32, >= T=%d, slots*E_local < 2^31", o, a.slots, a.T);
+            if (a.E_local > kMaskedMaxE || a.top_k > 32)
+                return fail(MOE_ERR_UNSUPPORTED, "moe_topk_route_batch: entry %d: masked layout needs E_local <= %d",
+                            o, kMaskedMaxE);
+            if (!a.assign_to_row || !a.row_to_assign || !a.place_ws)
                 return fail(MOE_ERR_INVALID_ARG, "moe_topk_route_batch: entry %d: masked layout needs assign_to_row, "
-                            "row_to_assign and a clear array other than counts", o);
+                            "row_to_assign and place_ws", o);
+            if ((uintptr_t)a.place_ws % 8 != 0)
+                return fail(MOE_ERR_INVALID_ARG, "moe_topk_route_batch: entry %d: place_ws must be 8-byte aligned", o);
         }
-        if (a.T == 0 && a.clear) return fail(MOE_ERR_INVALID_ARG, "moe_topk_route_batch: entry %d: clear with T=0", o);
         b.op[o] = a;
         b.blk0[o] = (int32_t)blocks;
         blocks += (a.T + kTokensPerBlock - 1) / kTokensPerBlock;

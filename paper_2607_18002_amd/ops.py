@@ -65,14 +65,19 @@ def moe_topk_route_batch(entries: Sequence[RouteArgs], stream=None) -> None:
 
 def route_args(logits: torch.Tensor, top_k: int, local_begin: int, E_local: int, topk_ids: torch.Tensor,
                topk_w: torch.Tensor, slots: int = 0, counts: Optional[torch.Tensor] = None,
-               clear: Optional[torch.Tensor] = None, assign_to_row: Optional[torch.Tensor] = None,
-               row_to_assign: Optional[torch.Tensor] = None) -> RouteArgs:
+               place_ws: Optional[torch.Tensor] = None, assign_to_row: Optional[torch.Tensor] = None,
+               row_to_assign: Optional[torch.Tensor] = None, error_flag: Optional[torch.Tensor] = None) -> RouteArgs:
     """One entry of moe_topk_route_batch; with counts given it also places the
     local slots in the masked layout (slots rows per local expert)."""
     T, E = logits.shape
     return RouteArgs(logits=_ptr(logits), T=T, E_global=E, top_k=top_k, local_begin=local_begin, E_local=E_local,
                      topk_ids=_ptr(topk_ids), topk_w=_ptr(topk_w), slots=slots, counts=_ptr(counts),
-                     clear=_ptr(clear), assign_to_row=_ptr(assign_to_row), row_to_assign=_ptr(row_to_assign))
+                     place_ws=_ptr(place_ws), assign_to_row=_ptr(assign_to_row), row_to_assign=_ptr(row_to_assign),
+                     error_flag=_ptr(error_flag))
+
+
+def moe_route_place_workspace_bytes(T: int, E_local: int) -> int:
+    return int(load_library().moe_route_place_workspace_bytes(T, E_local))
 
 
 def moe_permute_workspace_bytes(T: int, top_k: int, E_local: int) -> int:
@@ -198,7 +203,29 @@ def status_string(status: int) -> str:
     return load_library().moe_status_string(status).decode()
 
 
-__all__ = ["moe_topk_route", "moe_topk_route_batch", "moe_permute_workspace_bytes", "moe_permute", "moe_permute_batch",
+__all__ = ["moe_topk_route", "moe_topk_route_batch", "moe_route_place_workspace_bytes", "moe_permute_workspace_bytes", "moe_permute", "moe_permute_batch",
            "moe_ffn_row_align", "moe_ffn_tile_shape", "moe_ffn_workspace_bytes", "moe_grouped_ffn_persistent",
            "moe_combine", "moe_combine_batch", "moe_pack_weights", "moe_x_moe", "moe_decode_quota", "status_string",
            "route_args", "permute_args", "combine_args", "OpDesc", "SchedConfig", "_lib"]
+
+
+def moe_sched_layout(counts, offsets, M_t: int, gmax: int, n1: int, n2: int):
+    """The tile layout the persistent kernel builds for one op (host-side, the
+    kernel's own index arithmetic): (row_tiles [x_moe,4], groups [x_moe,2],
+    queues [8,2], tiles [x_moe*(n1+n2),4]) as numpy arrays."""
+    import numpy as np
+    lib = load_library()
+    counts = np.ascontiguousarray(counts, dtype=np.int32)
+    offsets = np.ascontiguousarray(offsets, dtype=np.int32)
+    E = len(counts)
+    cap = int(sum(-(-int(c) // M_t) for c in counts if c > 0))
+    rt = np.zeros((max(cap, 1), 4), np.int32)
+    gr = np.zeros((max(cap, 1), 2), np.int32)
+    qu = np.zeros((8, 2), np.int32)
+    nt = max(cap * (n1 + n2), 1)
+    tl = np.zeros((nt, 4), np.int32)
+    p = lambda a: a.ctypes.data_as(C.c_void_p)  # noqa: E731
+    x = lib.moe_sched_layout(p(counts), p(offsets), E, M_t, gmax, n1, n2, rt.shape[0], p(rt), p(gr), p(qu), nt, p(tl))
+    if x < 0:
+        raise ValueError(f"moe_sched_layout returned {x}")
+    return rt[:x], gr[:x], qu, tl[:x * (n1 + n2)]

@@ -108,7 +108,7 @@ class OpBuffers:
     perm_ws: torch.Tensor
     done_word: torch.Tensor
     slots: int = 0                              # masked layout: rows per local expert (0: contiguous layout)
-    counts_ab: Optional[List[torch.Tensor]] = None   # masked layout: the two count arrays, used alternately
+    place_ws: Optional[torch.Tensor] = None     # masked layout: the routing launch's placement workspace
 
 
 class MoEPipeline:
@@ -116,20 +116,22 @@ class MoEPipeline:
                  decode_quota_max_wg: int = 0, x_moe_expected: int = 0, round_multiple: int = 8,
                  trace_capacity: int = 0, spin_limit: int = 0, abort_word: Optional[torch.Tensor] = None,
                  y_dtype: torch.dtype = torch.bfloat16, fused_gather: bool = False, group_row_tiles: int = 0,
-                 static_partition: bool = False, fused_combine: bool = False, masked_decode: bool = False):
+                 static_partition: bool = False, fused_combine: bool = False, masked_decode: bool = False,
+                 masked_prefill: bool = False):
         """fused_gather: GEMM-1 reads its rows straight from x through row_to_assign
         (permute then only builds the maps), instead of from a permuted copy x_perm.
         fused_combine: the persistent kernel writes y itself (combine tiles after
         each op's GEMM tiles), and combine() launches nothing.
-        masked_decode: decode ops use the masked layout (a region of slots rows
-        per local expert, filled by routing; permute() skips them)."""
+        masked_decode / masked_prefill: ops of that phase use the masked layout
+        (a region of slots rows per local expert, placed by the routing launch;
+        permute() skips them)."""
         if not specs:
             raise ValueError("no operations")
         self.device = specs[0].logits.device
         self.fused_gather = fused_gather
         self.fused_combine = fused_combine
-        if masked_decode and not fused_gather:
-            raise ValueError("the masked decode layout needs fused_gather (nothing copies rows into x_perm)")
+        if (masked_decode or masked_prefill) and not fused_gather:
+            raise ValueError("the masked layout needs fused_gather (nothing copies rows into x_perm)")
         dev = self.device
         self.bufs: List[OpBuffers] = []
         for s in specs:
@@ -139,17 +141,15 @@ class MoEPipeline:
             ra = K.moe_ffn_row_align(s.phase, s.weights.dtype)
             if ra <= 0:
                 raise ValueError(f"no FFN tile class for phase={s.phase} dtype={s.weights.dtype}")
-            masked = masked_decode and s.phase == MOE_DECODE and T > 0
+            masked = (masked_decode if s.phase == MOE_DECODE else masked_prefill) and T > 0
             slots = (T + 31) // 32 * 32 if masked else 0
             cap = s.E_local * slots if masked else T * min(s.top_k, s.E_local) + s.E_local * (ra - 1)
             act = torch.uint8 if fp8 else torch.bfloat16
-            counts_ab = ([torch.zeros(s.E_local, dtype=torch.int32, device=dev) for _ in range(2)]
-                         if masked else None)
             self.bufs.append(OpBuffers(
                 spec=s, T=T, capacity=cap, row_align=ra,
                 topk_ids=torch.empty((T, s.top_k), dtype=torch.int32, device=dev),
                 topk_w=torch.empty((T, s.top_k), dtype=torch.float32, device=dev),
-                counts=counts_ab[0] if masked else torch.zeros(s.E_local, dtype=torch.int32, device=dev),
+                counts=torch.zeros(s.E_local, dtype=torch.int32, device=dev),
                 offsets=(torch.arange(s.E_local + 1, dtype=torch.int32, device=dev) * slots if masked
                          else torch.zeros(s.E_local + 1, dtype=torch.int32, device=dev)),
                 row_to_assign=torch.full((cap,), -1, dtype=torch.int32, device=dev),
@@ -164,7 +164,9 @@ class MoEPipeline:
                 perm_ws=torch.zeros((max(1, K.moe_permute_workspace_bytes(T, s.top_k, s.E_local)),),
                                     dtype=torch.uint8, device=dev),
                 done_word=torch.zeros(1, dtype=torch.int32, device=dev),
-                slots=slots, counts_ab=counts_ab,
+                slots=slots,
+                place_ws=(torch.zeros((K.moe_route_place_workspace_bytes(T, s.E_local),), dtype=torch.uint8,
+                                      device=dev) if masked else None),
             ))
         self.error_flag = torch.zeros(1, dtype=torch.int32, device=dev)
         self.status = torch.zeros(1, dtype=torch.int32, device=dev)
@@ -179,33 +181,22 @@ class MoEPipeline:
                                trace=self.trace.data_ptr() if trace_capacity > 0 else None,
                                trace_capacity=trace_capacity, op_stats=self.stats.data_ptr(),
                                spin_limit=spin_limit, static_partition=int(static_partition))
-        # Masked ops alternate their two count arrays step by step: the routing
-        # of a step fills one (zeroed by the previous step's routing) and clears
-        # the other.  Descriptors and routing arguments exist for both parities.
-        self._parity = 0
-        self._descs, self._route_sets = [], []
-        for par in (0, 1):
-            ds, rs = [], []
-            for i, b in enumerate(self.bufs):
-                if b.counts_ab is not None:
-                    b.counts = b.counts_ab[par]
-                ds.append(self._desc(i, b, fused_gather, fused_combine))
-                s = b.spec
-                if b.counts_ab is None:
-                    rs.append(K.route_args(s.logits, s.top_k, s.local_begin, s.E_local, b.topk_ids, b.topk_w))
-                else:
-                    rs.append(K.route_args(s.logits, s.top_k, s.local_begin, s.E_local, b.topk_ids, b.topk_w,
-                                           slots=b.slots, counts=b.counts_ab[par], clear=b.counts_ab[1 - par],
-                                           assign_to_row=b.assign_to_row, row_to_assign=b.row_to_assign))
-            self._descs.append(ds)
-            self._route_sets.append(rs)
+        self._descs = [self._desc(i, b, fused_gather, fused_combine) for i, b in enumerate(self.bufs)]
+        self._route_args = []
         for b in self.bufs:
-            if b.counts_ab is not None:
-                b.counts = b.counts_ab[0]
+            s = b.spec
+            if b.place_ws is None:
+                self._route_args.append(K.route_args(s.logits, s.top_k, s.local_begin, s.E_local, b.topk_ids,
+                                                     b.topk_w))
+            else:
+                self._route_args.append(K.route_args(s.logits, s.top_k, s.local_begin, s.E_local, b.topk_ids,
+                                                     b.topk_w, slots=b.slots, counts=b.counts, place_ws=b.place_ws,
+                                                     assign_to_row=b.assign_to_row, row_to_assign=b.row_to_assign,
+                                                     error_flag=self.error_flag))
         self._permute_args = [K.permute_args(b.topk_ids, b.spec.E_local, b.spec.x, b.spec.x_scales, b.row_align,
                                              b.capacity, b.counts, b.offsets, b.row_to_assign, b.assign_to_row,
                                              b.x_perm, b.x_perm_scales, b.perm_ws, self.error_flag)
-                              for b in self.bufs if b.counts_ab is None]
+                              for b in self.bufs if b.place_ws is None]
         self._combine_args = [K.combine_args(b.y_perm, b.assign_to_row, b.topk_w, b.T, b.spec.top_k, b.y)
                               for b in self.bufs]
         self.ffn_ws = torch.zeros((K.moe_ffn_workspace_bytes(self.descs, self.cfg),), dtype=torch.uint8, device=dev)
@@ -235,18 +226,14 @@ class MoEPipeline:
     # (moe_*_batch); batched=False issues the per-op calls instead.
     @property
     def descs(self):
-        return self._descs[self._parity]
+        return self._descs
 
     def route(self, stream=None, batched: bool = True):
         if batched:
-            self._parity ^= 1                       # a new step: masked ops switch count arrays
-            for b in self.bufs:
-                if b.counts_ab is not None:
-                    b.counts = b.counts_ab[self._parity]
-            K.moe_topk_route_batch(self._route_sets[self._parity], stream)
+            K.moe_topk_route_batch(self._route_args, stream)
             return
-        if any(b.counts_ab is not None for b in self.bufs):
-            raise ValueError("masked decode ops are routed by the batched call only")
+        if any(b.place_ws is not None for b in self.bufs):
+            raise ValueError("masked ops are routed by the batched call only")
         for b in self.bufs:
             s = b.spec
             K.moe_topk_route(s.logits, s.top_k, s.local_begin, s.E_local, b.topk_ids, b.topk_w, stream)
@@ -257,7 +244,7 @@ class MoEPipeline:
                 K.moe_permute_batch(self._permute_args, stream)
             return
         for b in self.bufs:
-            if b.counts_ab is not None:             # masked: routing placed the rows
+            if b.place_ws is not None:              # masked: routing placed the rows
                 continue
             s = b.spec
             K.moe_permute(b.topk_ids, s.E_local, s.x, s.x_scales, b.row_align, b.capacity, b.counts, b.offsets,

@@ -120,23 +120,35 @@ def test_argument_errors_before_any_launch():
 
 def test_masked_route_argument_errors():
     """The masked-layout fields of moe_topk_route_batch are checked on the host
-    before anything is launched: slots a multiple of 32 and >= T, both maps
-    given, and a clear array other than counts."""
+    before anything is launched: 1 <= T, slots a multiple of 32 and >= T,
+    both maps and the placement workspace given and aligned, E_local within
+    the placement's limit."""
     from paper_2607_18002_amd import _lib
     lib = _lib.load_library()
     fake = 0x10000                                          # never dereferenced: the call fails first
 
     def call(**kw):
         a = dict(logits=fake, T=64, E_global=64, top_k=4, local_begin=0, E_local=8, topk_ids=fake, topk_w=fake,
-                 slots=64, counts=fake, clear=fake + 256, assign_to_row=fake, row_to_assign=fake)
+                 slots=64, counts=fake, place_ws=fake + 256, assign_to_row=fake, row_to_assign=fake)
         a.update(kw)
         arr = (_lib.RouteArgs * 1)(_lib.RouteArgs(**a))
         return lib.moe_topk_route_batch(arr, 1, None)
 
     assert call(slots=40) == _lib.MOE_ERR_INVALID_ARG            # not a multiple of 32
-    assert b"slots=40" in lib.moe_last_error()
+    assert b"slots (40)" in lib.moe_last_error()
     assert call(slots=32) == _lib.MOE_ERR_INVALID_ARG            # fewer slots than tokens
     assert call(assign_to_row=None) == _lib.MOE_ERR_INVALID_ARG
-    assert call(clear=fake) == _lib.MOE_ERR_INVALID_ARG          # clear is counts
-    assert call(T=0, slots=0, counts=None) == _lib.MOE_ERR_INVALID_ARG   # clear with no token to clear it
-    assert call(counts=None, clear=None) != _lib.MOE_ERR_INVALID_ARG     # unmasked entry passes the checks
+    assert call(place_ws=None) == _lib.MOE_ERR_INVALID_ARG
+    assert call(place_ws=fake + 4) == _lib.MOE_ERR_INVALID_ARG   # not 8-byte aligned
+    assert call(T=0, slots=0) == _lib.MOE_ERR_INVALID_ARG         # a masked entry needs a token
+    assert call(E_local=1025, E_global=2048) != _lib.MOE_OK
+    assert call(counts=None, place_ws=None) != _lib.MOE_ERR_INVALID_ARG   # unmasked entry passes the checks
+
+
+def test_route_place_workspace_bytes():
+    """One 64-bit record per (4-token chunk, local expert) after a 256-byte header."""
+    from paper_2607_18002_amd import ops
+    assert ops.moe_route_place_workspace_bytes(0, 32) == 0
+    assert ops.moe_route_place_workspace_bytes(1, 32) == 256 + 32 * 8
+    assert ops.moe_route_place_workspace_bytes(1024, 32) == 256 + 256 * 32 * 8
+    assert ops.moe_route_place_workspace_bytes(1025, 8) == 256 + 257 * 8 * 8
