@@ -201,7 +201,7 @@ __device__ __forceinline__ void route_block(const float* __restrict__ logits, in
 // ascending a -- the unique order the permutation uses, bit-exact and
 // independent of scheduling.
 //
-// A routing block of a masked op takes its chunk of 4 tokens from an ordered
+// A routing block of a masked op takes its chunk of 16 tokens from an ordered
 // ticket (so every chunk it waits for belongs to a block that has already
 // started), ranks its slots inside the chunk, publishes the chunk's
 // per-expert counts and finds the counts of all earlier chunks by a
@@ -216,6 +216,7 @@ __device__ __forceinline__ void route_block(const float* __restrict__ logits, in
 constexpr uint64_t kRecAgg = 1ull << 30, kRecIncl = 2ull << 30;
 constexpr uint32_t kRecCountMask = (1u << 30) - 1;
 constexpr int kPlaceHdrWords = 32;          // 256-byte header: the ticket word, alone in its line
+constexpr int kMaskedChunk = 16;            // tokens per masked block: four per wave
 constexpr int kMaskedMaxE = 1024;
 constexpr int64_t kLookbackSpins = 1 << 22;
 
@@ -238,7 +239,7 @@ __device__ void route_block_masked(const float* __restrict__ logits, int T, int 
                                    const MaskedArgs m) {
     __shared__ int s_chunk;
     __shared__ uint32_t s_gen;
-    __shared__ int32_t s_sel[kTokensPerBlock][32];
+    __shared__ int32_t s_sel[kMaskedChunk][32];
     __shared__ int32_t s_cnt[kMaskedMaxE];
     __shared__ int32_t s_excl[kMaskedMaxE];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -261,16 +262,16 @@ __device__ void route_block_masked(const float* __restrict__ logits, int T, int 
     const int chunk = s_chunk;
     if (chunk < 0) return;                        // block-uniform
     const uint32_t gen = s_gen;
-    const int t = chunk * kTokensPerBlock + w;
-    const int loc = route_wave<EPL>(logits, t, T, E, k, local_begin, E_local, ids, wts);
-    if (lane < 32) s_sel[w][lane] = lane < k ? loc : -1;
-    if (loc >= 0) atomicAdd(&s_cnt[loc], 1);
+    // wave w routes tokens w, w + 4, ... of the chunk (chunk-local index tl = 4*it + w)
+    int loc[kMaskedChunk / kTokensPerBlock];
+#pragma unroll
+    for (int it = 0; it < kMaskedChunk / kTokensPerBlock; ++it) {
+        const int tl = it * kTokensPerBlock + w;
+        loc[it] = route_wave<EPL>(logits, chunk * kMaskedChunk + tl, T, E, k, local_begin, E_local, ids, wts);
+        if (lane < 32) s_sel[tl][lane] = lane < k ? loc[it] : -1;
+        if (loc[it] >= 0) atomicAdd(&s_cnt[loc[it]], 1);
+    }
     __syncthreads();
-    // rank inside the chunk: the earlier tokens of the chunk that chose the same expert
-    int rank = 0;
-    if (loc >= 0)
-        for (int w2 = 0; w2 < w; ++w2)
-            for (int j = 0; j < k; ++j) rank += s_sel[w2][j] == loc;
     uint64_t* rec = m.ws + kPlaceHdrWords + (size_t)chunk * E_local;
     // publish first (chunk 0 holds its own inclusive prefix), then look back:
     // a block waits only on the records of earlier chunks, so no wait is circular
@@ -302,13 +303,20 @@ __device__ void route_block_masked(const float* __restrict__ logits, int T, int 
         s_excl[e] = (int32_t)excl;
     }
     __syncthreads();
-    if (t < T && lane < k) {
+#pragma unroll
+    for (int it = 0; it < kMaskedChunk / kTokensPerBlock; ++it) {
+        const int tl = it * kTokensPerBlock + w;
+        const int t = chunk * kMaskedChunk + tl;
+        if (t >= T || lane >= k) continue;
         const int a = t * k + lane;
         int row = -1;
-        if (loc >= 0) {
-            const int r = s_excl[loc] + rank;
+        if (loc[it] >= 0) {
+            // rank inside the chunk: the chunk's earlier tokens that chose the same expert
+            int r = s_excl[loc[it]];
+            for (int t2 = 0; t2 < tl; ++t2)
+                for (int j = 0; j < k; ++j) r += s_sel[t2][j] == loc[it];
             if (r < m.slots) {                    // always, as slots >= T
-                row = loc * m.slots + r;
+                row = loc[it] * m.slots + r;
                 m.r2a[row] = a;
             } else {
                 set_status(m.err, MOE_ERR_CAPACITY);
@@ -327,7 +335,8 @@ __global__ __launch_bounds__(256) void topk_route_kernel(const float* __restrict
     route_block<EPL>(logits, T, E, k, local_begin, E_local, ids, wts, blockIdx.x);
 }
 
-// Several ops in one launch: op o owns blocks [blk0[o], blk0[o + 1]).
+// Several ops in one launch: entry o owns blocks [blk0[o], blk0[o + 1]); the
+// host puts masked entries first, so their longer blocks are dispatched first.
 struct RouteBatch {
     moe_route_args op[MOE_MAX_OPS];
     int32_t blk0[MOE_MAX_OPS + 1];
@@ -389,7 +398,7 @@ extern "C" moe_status_t moe_topk_route(const float* logits, int32_t T, int32_t E
 
 extern "C" size_t moe_route_place_workspace_bytes(int32_t T, int32_t E_local) {
     if (T < 1 || E_local < 1) return 0;
-    const size_t chunks = (size_t)((T + kTokensPerBlock - 1) / kTokensPerBlock);
+    const size_t chunks = (size_t)((T + kMaskedChunk - 1) / kMaskedChunk);
     return (kPlaceHdrWords + chunks * (size_t)E_local) * sizeof(uint64_t);
 }
 
@@ -420,12 +429,19 @@ extern "C" moe_status_t moe_topk_route_batch(const moe_route_args* ops, int32_t 
             if ((uintptr_t)a.place_ws % 8 != 0)
                 return fail(MOE_ERR_INVALID_ARG, "moe_topk_route_batch: entry %d: place_ws must be 8-byte aligned", o);
         }
-        b.op[o] = a;
-        b.blk0[o] = (int32_t)blocks;
-        blocks += (a.T + kTokensPerBlock - 1) / kTokensPerBlock;
         const int e = (a.E_global + 63) / 64;
         epl = e > epl ? e : epl;
     }
+    int n = 0;
+    for (int pass = 0; pass < 2; ++pass)                  // masked entries first, then the others
+        for (int o = 0; o < n_ops; ++o) {
+            const moe_route_args& a = ops[o];
+            if ((a.counts != nullptr) != (pass == 0)) continue;
+            b.op[n] = a;
+            b.blk0[n] = (int32_t)blocks;
+            blocks += a.counts ? (a.T + kMaskedChunk - 1) / kMaskedChunk : (a.T + kTokensPerBlock - 1) / kTokensPerBlock;
+            ++n;
+        }
     if (blocks > INT32_MAX) return fail(MOE_ERR_UNSUPPORTED, "moe_topk_route_batch: too many tokens");
     b.blk0[n_ops] = (int32_t)blocks;
     b.n = n_ops;

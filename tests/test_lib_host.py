@@ -146,9 +146,9 @@ def test_masked_route_argument_errors():
 
 
 def test_route_place_workspace_bytes():
-    """One 64-bit record per (4-token chunk, local expert) after a 256-byte header."""
+    """One 64-bit record per (16-token chunk, local expert) after a 256-byte header."""
     from paper_2607_18002_amd import ops
     assert ops.moe_route_place_workspace_bytes(0, 32) == 0
     assert ops.moe_route_place_workspace_bytes(1, 32) == 256 + 32 * 8
-    assert ops.moe_route_place_workspace_bytes(1024, 32) == 256 + 256 * 32 * 8
-    assert ops.moe_route_place_workspace_bytes(1025, 8) == 256 + 257 * 8 * 8
+    assert ops.moe_route_place_workspace_bytes(1024, 32) == 256 + 64 * 32 * 8
+    assert ops.moe_route_place_workspace_bytes(1025, 8) == 256 + 65 * 8 * 8
