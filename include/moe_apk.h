@@ -347,6 +347,22 @@ moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32_t n_ops,
                                         const moe_sched_config* cfg, void* workspace,
                                         int32_t* status_word, void* stream);
 
+/* For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation: the same
+ * launch as moe_grouped_ffn_persistent (same kernels, results, readiness and
+ * error reporting), with the scheduler workspace in a static device array of
+ * the library (MOE_FFN_NOALLOC_WORKSPACE_BYTES per GPU, held until the
+ * process ends) instead of a caller-allocated one.  The caller still passes
+ * every input and output buffer.  Returns MOE_ERR_CAPACITY before anything is
+ * launched when moe_ffn_workspace_bytes(ops) exceeds the array (about 16
+ * operations of 250000 rows of capacity each).  Every call on one GPU uses
+ * that GPU's array, which keeps the last call's contents and is re-zeroed by
+ * each launch: calls that overlap in time on one GPU (different streams, or
+ * different threads) race and must not be issued. */
+#define MOE_FFN_NOALLOC_WORKSPACE_BYTES (4u << 20)
+moe_status_t moe_grouped_ffn_persistent_noalloc(const moe_op_desc* ops, int32_t n_ops,
+                                                const moe_sched_config* cfg, int32_t* status_word, void* stream);
+
 /* Weight layout streamed by the FFN kernel (one-time conversion, outside the
  * hot path).  A matrix [N, K] is cut into 32-row blocks of 4 KB chunks, each
  * chunk holding exactly the 16-byte pieces lanes 0..63 feed to the MFMAs of

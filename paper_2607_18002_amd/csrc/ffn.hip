@@ -41,6 +41,7 @@
 // wave that wrote them.  The one acquire per operation is taken by the
 // workgroup that finishes it, before it publishes the done word.
 #include <cstring>
+#include <mutex>
 
 #include "sched_index.hpp"
 #include "tile_bf16.hpp"
@@ -980,8 +981,13 @@ extern "C" size_t moe_ffn_workspace_bytes(const moe_op_desc* ops, int32_t n_ops,
     return ws_bytes_for(ops, n_ops);
 }
 
-extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32_t n_ops, const moe_sched_config* cfg,
-                                                   void* workspace, int32_t* status_word, void* stream) {
+namespace {
+
+// The one launch path of both FFN entry points: checks, kernel arguments,
+// the init kernel (which zeroes the scheduler state with ordinary stores) and
+// the persistent kernel.  `workspace` holds at least ws_bytes_for(ops) bytes.
+moe_status_t launch_ffn(const moe_op_desc* ops, int32_t n_ops, const moe_sched_config* cfg, void* workspace,
+                        int32_t* status_word, void* stream) {
     using moeapk_host::fail;
     if (!ops || !cfg || !workspace || !status_word) return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn_persistent: null pointer");
     if (n_ops < 1 || n_ops > MOE_MAX_OPS)
@@ -1154,4 +1160,59 @@ extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(MOE_ERR_HIP, "moe_grouped_ffn_persistent: launch failed: %s", hipGetErrorString(err));
     return MOE_OK;
+}
+
+// Static scheduler workspace of the allocation-free entry point, one copy per
+// GPU (held until the process ends).  Host code never passes `scratch` itself
+// to a kernel (in host code it names a host-side stand-in): its device address
+// is taken once per device with hipGetSymbolAddress, with that device current.
+static __device__ __align__(256) char scratch[MOE_FFN_NOALLOC_WORKSPACE_BYTES];
+constexpr int kMaxScratchDevices = 64;
+void* g_scratch_ptr[kMaxScratchDevices];
+std::mutex g_scratch_mu;
+
+moe_status_t scratch_address(void** ptr) {
+    using moeapk_host::fail;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return fail(MOE_ERR_HIP, "hipGetDevice failed");
+    if (dev < 0 || dev >= kMaxScratchDevices) return fail(MOE_ERR_UNSUPPORTED, "device index %d out of range", dev);
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(MOE_ERR_HIP, "hipGetSymbolAddress(scratch) failed on device %d: %s", dev, hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32_t n_ops, const moe_sched_config* cfg,
+                                                   void* workspace, int32_t* status_word, void* stream) {
+    return launch_ffn(ops, n_ops, cfg, workspace, status_word, stream);
+}
+
+extern "C" moe_status_t moe_grouped_ffn_persistent_noalloc(const moe_op_desc* ops, int32_t n_ops,
+                                                           const moe_sched_config* cfg, int32_t* status_word,
+                                                           void* stream) {
+    using moeapk_host::fail;
+    if (!ops || n_ops < 1 || n_ops > MOE_MAX_OPS)
+        return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn_persistent_noalloc: n_ops=%d outside [1,%d]", n_ops,
+                    MOE_MAX_OPS);
+    for (int o = 0; o < n_ops; ++o)
+        if (ops[o].capacity < 0) return fail(MOE_ERR_INVALID_ARG, "op %d: capacity < 0", o);
+    const size_t need = ws_bytes_for(ops, n_ops);
+    if (need > (size_t)MOE_FFN_NOALLOC_WORKSPACE_BYTES)
+        return fail(MOE_ERR_CAPACITY, "moe_grouped_ffn_persistent_noalloc: the ops need %zu bytes of scheduler "
+                    "workspace, above the static %u", need, (unsigned)MOE_FFN_NOALLOC_WORKSPACE_BYTES);
+    if (!cfg || !status_word) return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn_persistent_noalloc: null pointer");
+    moe_status_t st = moeapk_host::check_device();
+    if (st != MOE_OK) return st;
+    void* ws = nullptr;
+    st = scratch_address(&ws);
+    if (st != MOE_OK) return st;
+    return launch_ffn(ops, n_ops, cfg, ws, status_word, stream);
 }
