@@ -70,7 +70,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--dump-trace", default=None, help="write the traced launch's per-tile records (.npy)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
-                    help="after the run, copy this many MiB device to device 3 times (counter calibration)")
+                    help="after the run, copy this many MiB device to device 3 times and stream-read as many "
+                         "3 times (counter calibration: kernels of known bytes)")
+    ap.add_argument("--no-peaks", action="store_true", help="skip the measured-peak microbenchmarks")
     return ap.parse_args()
 
 
@@ -356,6 +358,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+        from paper_2607_18002_amd import peaks
+        peaks.stream_read_gbs(gib=args.calib_copy_mib / 1024.0, reps=1)   # 3 launches of known read bytes
+        torch.cuda.synchronize()
 
     dtype = cfg.dtype
     t_mfma = flops / (MFMA_PEAK_TFLOPS[dtype] * 1e12)
@@ -382,6 +387,13 @@ def main():
     roof["achieved_tflops"] = round(flops / (ffn_ms * 1e-3) / 1e12, 2)
     roof["frac_mfma"] = round(flops / (ffn_ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS[dtype], 4)
     roof["frac_hbm"] = round(abytes / (ffn_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+
+    if not args.no_peaks:
+        from paper_2607_18002_amd import peaks
+        meas = peaks.measure()
+        roof["measured_peaks"] = meas
+        roof["frac_of_measured_mfma"] = round(roof["achieved_tflops"] / meas[f"mfma_{dtype}_tflops"], 4)
+        roof["frac_of_measured_hbm"] = round(abytes / (ffn_ms * 1e-3) / 1e9 / meas["hbm_read_gbs"], 4)
 
     cpu = None
     parity = None

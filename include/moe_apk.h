@@ -115,7 +115,8 @@ typedef struct moe_route_args {
      *            memory, 8-byte aligned, zero before its first use (allocate
      *            it zeroed); the call leaves it ready for the next call with
      *            the same or a smaller T.  Calls that share it must not
-     *            overlap in time.
+     *            overlap in time.  (Routing blocks of a masked entry take
+     *            chunks of 4 tokens up to 2048 tokens, of 16 above.)
      *  error_flag NULL or a device i32 status word: MOE_ERR_INTERNAL if
      *            place_ws was not zero before its first use, MOE_ERR_TIMEOUT
      *            if a wait for another block's counts exceeded its bound

@@ -20,6 +20,9 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libmoe_apk.so")
 SOURCES = ["api.cpp", "route.hip", "permute.hip", "combine.hip", "ffn.hip", "pack.hip"]
+# measurement kernels (achievable MFMA and HBM read peaks), a library of their own
+PEAKS_LIB = os.path.join(PKG, "libmoe_peaks.so")
+PEAKS_SOURCES = ["peaks.hip"]
 # Every source file the persistent FFN kernel is compiled from (hashed to tie
 # recorded hardware-counter figures to the kernel they were taken on).
 FFN_KERNEL_SOURCES = ["paper_2607_18002_amd/csrc/ffn.hip", "paper_2607_18002_amd/csrc/tile_bf16.hpp",
@@ -64,18 +67,24 @@ def ffn_kernel_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def build(verbose: bool = False) -> str:
-    if not os.path.exists(HIPCC) and shutil.which("hipcc") is None:
-        raise RuntimeError("hipcc not found")
-    os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, lib: str) -> None:
+    tmp = lib + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed\n" + r.stdout + r.stderr)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    if not os.path.exists(HIPCC) and shutil.which("hipcc") is None:
+        raise RuntimeError("hipcc not found")
+    os.makedirs(BUILD, exist_ok=True)
+    allsrc = SOURCES + PEAKS_SOURCES
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(allsrc))) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose), allsrc))
+    _link(objs[:len(SOURCES)], LIB)
+    _link(objs[len(SOURCES):], PEAKS_LIB)
     return LIB
 
 

@@ -201,7 +201,7 @@ __device__ __forceinline__ void route_block(const float* __restrict__ logits, in
 // ascending a -- the unique order the permutation uses, bit-exact and
 // independent of scheduling.
 //
-// A routing block of a masked op takes its chunk of 16 tokens from an ordered
+// A routing block of a masked op takes its chunk of 4 or 16 tokens from an ordered
 // ticket (so every chunk it waits for belongs to a block that has already
 // started), ranks its slots inside the chunk, publishes the chunk's
 // per-expert counts and finds the counts of all earlier chunks by a
@@ -216,7 +216,12 @@ __device__ __forceinline__ void route_block(const float* __restrict__ logits, in
 constexpr uint64_t kRecAgg = 1ull << 30, kRecIncl = 2ull << 30;
 constexpr uint32_t kRecCountMask = (1u << 30) - 1;
 constexpr int kPlaceHdrWords = 32;          // 256-byte header: the ticket word, alone in its line
-constexpr int kMaskedChunk = 16;            // tokens per masked block: four per wave
+// Tokens per masked block: one per wave up to kMaskedSmallT tokens (the
+// block's latency is one token's routing), four per wave above (a quarter of
+// the tickets on the op's ordered counter).
+constexpr int kMaskedChunk = 16;
+constexpr int kMaskedSmallT = 2048;
+__host__ __device__ __forceinline__ int masked_chunk(int T) { return T <= kMaskedSmallT ? 4 : kMaskedChunk; }
 constexpr int kMaskedMaxE = 1024;
 constexpr int64_t kLookbackSpins = 1 << 22;
 
@@ -233,7 +238,7 @@ struct MaskedArgs {
     int slots, nchunks;
 };
 
-template <int EPL>
+template <int EPL, int CPW>
 __device__ void route_block_masked(const float* __restrict__ logits, int T, int E, int k, int local_begin,
                                    int E_local, int32_t* __restrict__ ids, float* __restrict__ wts,
                                    const MaskedArgs m) {
@@ -263,11 +268,12 @@ __device__ void route_block_masked(const float* __restrict__ logits, int T, int 
     if (chunk < 0) return;                        // block-uniform
     const uint32_t gen = s_gen;
     // wave w routes tokens w, w + 4, ... of the chunk (chunk-local index tl = 4*it + w)
-    int loc[kMaskedChunk / kTokensPerBlock];
+    int loc[CPW];
 #pragma unroll
-    for (int it = 0; it < kMaskedChunk / kTokensPerBlock; ++it) {
+    for (int it = 0; it < CPW; ++it) {
         const int tl = it * kTokensPerBlock + w;
-        loc[it] = route_wave<EPL>(logits, chunk * kMaskedChunk + tl, T, E, k, local_begin, E_local, ids, wts);
+        loc[it] = route_wave<EPL>(logits, chunk * CPW * kTokensPerBlock + tl, T, E, k, local_begin, E_local, ids,
+                                  wts);
         if (lane < 32) s_sel[tl][lane] = lane < k ? loc[it] : -1;
         if (loc[it] >= 0) atomicAdd(&s_cnt[loc[it]], 1);
     }
@@ -304,9 +310,9 @@ __device__ void route_block_masked(const float* __restrict__ logits, int T, int 
     }
     __syncthreads();
 #pragma unroll
-    for (int it = 0; it < kMaskedChunk / kTokensPerBlock; ++it) {
+    for (int it = 0; it < CPW; ++it) {
         const int tl = it * kTokensPerBlock + w;
-        const int t = chunk * kMaskedChunk + tl;
+        const int t = chunk * CPW * kTokensPerBlock + tl;
         if (t >= T || lane >= k) continue;
         const int a = t * k + lane;
         int row = -1;
@@ -349,9 +355,14 @@ __global__ __launch_bounds__(256) void topk_route_batch_kernel(const RouteBatch 
     while (o + 1 < b.n && (int)blockIdx.x >= b.blk0[o + 1]) ++o;      // uniform
     const moe_route_args& a = b.op[o];
     if (a.counts) {
-        route_block_masked<EPL>(a.logits, a.T, a.E_global, a.top_k, a.local_begin, a.E_local, a.topk_ids, a.topk_w,
-                                MaskedArgs{a.counts, a.assign_to_row, a.row_to_assign, (uint64_t*)a.place_ws, a.error_flag,
-                                           a.slots, b.blk0[o + 1] - b.blk0[o]});
+        const MaskedArgs m{a.counts, a.assign_to_row, a.row_to_assign, (uint64_t*)a.place_ws, a.error_flag, a.slots,
+                           b.blk0[o + 1] - b.blk0[o]};
+        if (masked_chunk(a.T) == 4)
+            route_block_masked<EPL, 1>(a.logits, a.T, a.E_global, a.top_k, a.local_begin, a.E_local, a.topk_ids,
+                                       a.topk_w, m);
+        else
+            route_block_masked<EPL, kMaskedChunk / kTokensPerBlock>(a.logits, a.T, a.E_global, a.top_k,
+                                                                     a.local_begin, a.E_local, a.topk_ids, a.topk_w, m);
         return;
     }
     route_block<EPL>(a.logits, a.T, a.E_global, a.top_k, a.local_begin, a.E_local, a.topk_ids, a.topk_w,
@@ -398,7 +409,10 @@ extern "C" moe_status_t moe_topk_route(const float* logits, int32_t T, int32_t E
 
 extern "C" size_t moe_route_place_workspace_bytes(int32_t T, int32_t E_local) {
     if (T < 1 || E_local < 1) return 0;
-    const size_t chunks = (size_t)((T + kMaskedChunk - 1) / kMaskedChunk);
+    // the most chunks of any call with up to T tokens (4-token chunks reach
+    // kMaskedSmallT / 4 of them before the chunk grows to 16 tokens)
+    size_t chunks = (size_t)((T + masked_chunk(T) - 1) / masked_chunk(T));
+    if (T > kMaskedSmallT && chunks < (size_t)(kMaskedSmallT / 4)) chunks = kMaskedSmallT / 4;
     return (kPlaceHdrWords + chunks * (size_t)E_local) * sizeof(uint64_t);
 }
 
@@ -439,7 +453,8 @@ extern "C" moe_status_t moe_topk_route_batch(const moe_route_args* ops, int32_t 
             if ((a.counts != nullptr) != (pass == 0)) continue;
             b.op[n] = a;
             b.blk0[n] = (int32_t)blocks;
-            blocks += a.counts ? (a.T + kMaskedChunk - 1) / kMaskedChunk : (a.T + kTokensPerBlock - 1) / kTokensPerBlock;
+            const int per = a.counts ? masked_chunk(a.T) : kTokensPerBlock;
+            blocks += (a.T + per - 1) / per;
             ++n;
         }
     if (blocks > INT32_MAX) return fail(MOE_ERR_UNSUPPORTED, "moe_topk_route_batch: too many tokens");

@@ -3,6 +3,7 @@
     python -m paper_2607_18002_amd.profsum stats DB --skip W --take K --cmd "..."
     python -m paper_2607_18002_amd.profsum traffic --fetch DB1 --write DB2 --skip W --take K \
         --copy-bytes B --workload NAME --cmd-fetch "..." --cmd-write "..."
+    python -m paper_2607_18002_amd.profsum counters DB --counters A,B --skip W --take K --cmd "..."
 
 ``stats`` reads a ``rocprofv3 --kernel-trace --stats`` database and prints
 per-kernel call counts and durations, plus the average of the persistent
@@ -25,6 +26,7 @@ from typing import Dict, List, Tuple
 
 FFN_KERNEL = "apk_kernel"
 COPY_KERNEL = "__amd_rocclr_copyBuffer"
+STREAM_KERNEL = "stream_read"            # libmoe_peaks.so: reads a known number of bytes, writes ~nothing
 
 
 def _short(name: str) -> str:
@@ -88,23 +90,68 @@ def traffic(args) -> str:
         cal = [v for v in copy if v >= 0.9 * big]
         kib_copy = sum(cal) / len(cal)
         factor = args.copy_bytes / (kib_copy * 1024.0)
+        # the streaming read (same byte count, read only) backs the read-side factor
+        stream = [v for n, _, v in ev if STREAM_KERNEL in n]
+        kib_stream = sum(stream) / len(stream) if stream else float("nan")
+        f_stream = args.copy_bytes / (kib_stream * 1024.0) if stream else float("nan")
+        if key == "fetch" and stream:
+            factor = f_stream
         sel = _timed(ffn, args.skip, args.take)
         kib = sum(sel) / len(sel)
-        res[key] = dict(kib=kib, kib_copy=kib_copy, factor=factor, bytes=kib * 1024.0 * factor, n=len(cal))
+        res[key] = dict(kib=kib, kib_copy=kib_copy, factor=factor, bytes=kib * 1024.0 * factor, n=len(cal),
+                        kib_stream=kib_stream, f_copy=args.copy_bytes / (kib_copy * 1024.0), f_stream=f_stream)
     tot = res["fetch"]["bytes"] + res["write"]["bytes"]
     out = ["# HBM traffic of the persistent FFN kernel (rocprofv3 --pmc)", "",
            f"Workload: {args.workload}", "", "Commands (one counter per run):", "", "```", args.cmd_fetch,
            args.cmd_write, "```", "",
-           f"Calibration: a device-to-device copy of {args.copy_bytes} bytes ({COPY_KERNEL}) in the same runs "
-           "reads and writes exactly that many bytes; factor = bytes / (counter KiB * 1024).", "",
-           "| counter | kernel KiB/dispatch (timed avg) | copy KiB | factor | bytes/launch |", "|---|---|---|---|---|"]
+           f"Calibration, in the same runs: a device-to-device copy of {args.copy_bytes:.0f} bytes ({COPY_KERNEL}) "
+           f"reads and writes exactly that many bytes, and a streaming read of as many bytes ({STREAM_KERNEL}, "
+           "libmoe_peaks.so) reads them and writes one word per workgroup; factor = bytes / (counter KiB * 1024). "
+           "FETCH_SIZE takes the streaming read's factor (a read-only kernel of known bytes), WRITE_SIZE the copy's.",
+           "", "| counter | kernel KiB/dispatch (timed avg) | copy KiB | copy factor | stream-read KiB | stream factor "
+           "| factor used | bytes/launch |", "|---|---|---|---|---|---|---|---|"]
     for key, c in (("fetch", "FETCH_SIZE"), ("write", "WRITE_SIZE")):
         r = res[key]
-        out.append(f"| {c} | {r['kib']:.0f} | {r['kib_copy']:.0f} | {r['factor']:.4f} | {r['bytes']:.4g} |")
+        fs = f"{r['f_stream']:.4f}" if key == "fetch" else "n/a (writes ~0)"
+        out.append(f"| {c} | {r['kib']:.0f} | {r['kib_copy']:.0f} | {r['f_copy']:.4f} | {r['kib_stream']:.0f} | "
+                   f"{fs} | {r['factor']:.4f} | {r['bytes']:.4g} |")
     out += ["", f"source_hash = {ffn_kernel_hash()}", f"workload = {args.workload}",
             f"fetch_bytes_per_launch = {res['fetch']['bytes']:.6g}",
             f"write_bytes_per_launch = {res['write']['bytes']:.6g}",
             f"traffic_bytes_per_launch = {tot:.6g}"]
+    return "\n".join(out) + "\n"
+
+
+def counters(args) -> str:
+    """Timed-region average per dispatch of each counter in a --pmc database,
+    for the persistent kernel and the other kernels of the run."""
+    names = args.counters.split(",")
+    out = ["# rocprofv3 counters", "", f"Workload: {args.workload}", "", "Command:", "", "```", args.cmd, "```", "",
+           "| kernel | dispatches | " + " | ".join(names) + " |", "|---|---|" + "---|" * len(names)]
+    vals = {}
+    for c in names:
+        ev = _pmc(args.db, c)
+        # raw block counters come as one row per hardware instance (e.g. 32
+        # shader engines): sum them per dispatch
+        by_disp: Dict[int, List] = {}
+        for n, d, v in ev:
+            by_disp.setdefault(d, [n, 0.0])[1] += v
+        per: Dict[str, List[float]] = {}
+        for d in sorted(by_disp):
+            n, v = by_disp[d]
+            per.setdefault(_short(n), []).append(v)
+        for k, v in per.items():
+            if FFN_KERNEL in k and "init" not in k:
+                v = _timed(v, args.skip, args.take)
+            vals.setdefault(k, {})[c] = (len(v), sum(v) / len(v))
+    for k in sorted(vals, key=lambda k: (FFN_KERNEL not in k, k)):
+        row = vals[k]
+        n = max(x[0] for x in row.values())
+        out.append(f"| {k} | {n} | " + " | ".join(f"{row[c][1]:.6g}" if c in row else "" for c in names) + " |")
+    ffn = next((vals[k] for k in vals if FFN_KERNEL in k and "init" not in k), None)
+    if ffn:
+        out += ["", f"source_hash = {__import__('paper_2607_18002_amd.build', fromlist=['x']).ffn_kernel_hash()}"]
+        out += [f"{c} = {ffn[c][1]:.6g}" for c in names if c in ffn]
     return "\n".join(out) + "\n"
 
 
@@ -125,8 +172,15 @@ def main(argv=None) -> int:
     b.add_argument("--workload", required=True)
     b.add_argument("--cmd-fetch", default="")
     b.add_argument("--cmd-write", default="")
+    c = sub.add_parser("counters")
+    c.add_argument("db")
+    c.add_argument("--counters", required=True)
+    c.add_argument("--skip", type=int, default=0)
+    c.add_argument("--take", type=int, default=1)
+    c.add_argument("--workload", default="")
+    c.add_argument("--cmd", default="")
     args = ap.parse_args(argv)
-    sys.stdout.write(stats(args) if args.mode == "stats" else traffic(args))
+    sys.stdout.write({"stats": stats, "traffic": traffic, "counters": counters}[args.mode](args))
     return 0
 
 

@@ -686,7 +686,7 @@ def test_masked_layout(dev, dtype, prefill_too):
 
 
 @pytest.mark.parametrize("T_seq,E,E_l,k", [((1000, 300, 1000, 5, 1), 64, 16, 8), ((257, 64), 1000, 300, 32),
-                                           ((3, 130), 8, 8, 2)])
+                                           ((3, 130), 8, 8, 2), ((5000, 2048, 2049, 700, 5000), 64, 8, 4)])
 def test_masked_placement_calls_share_a_workspace(dev, T_seq, E, E_l, k):
     """Routing with masked placement, called repeatedly on one placement
     workspace with changing token counts (the workspace sized for the

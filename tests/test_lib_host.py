@@ -146,9 +146,12 @@ def test_masked_route_argument_errors():
 
 
 def test_route_place_workspace_bytes():
-    """One 64-bit record per (16-token chunk, local expert) after a 256-byte header."""
+    """One 64-bit record per (chunk, local expert) after a 256-byte header;
+    chunks of 4 tokens up to 2048 tokens, of 16 above."""
     from paper_2607_18002_amd import ops
     assert ops.moe_route_place_workspace_bytes(0, 32) == 0
     assert ops.moe_route_place_workspace_bytes(1, 32) == 256 + 32 * 8
-    assert ops.moe_route_place_workspace_bytes(1024, 32) == 256 + 64 * 32 * 8
-    assert ops.moe_route_place_workspace_bytes(1025, 8) == 256 + 65 * 8 * 8
+    assert ops.moe_route_place_workspace_bytes(1024, 32) == 256 + 256 * 32 * 8
+    assert ops.moe_route_place_workspace_bytes(1025, 8) == 256 + 257 * 8 * 8
+    assert ops.moe_route_place_workspace_bytes(2049, 8) == 256 + 512 * 8 * 8     # covers T = 2048 in 4-token chunks
+    assert ops.moe_route_place_workspace_bytes(16384, 8) == 256 + 1024 * 8 * 8
