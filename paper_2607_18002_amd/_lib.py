@@ -7,7 +7,9 @@ import ctypes as C
 import os
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libmoe_apk.so")
+# MOE_APK_LIBRARY: path of another build of the library to load instead (to
+# compare builds in one process environment); default: the in-tree build.
+LIB_PATH = os.environ.get("MOE_APK_LIBRARY") or os.path.join(PKG, "libmoe_apk.so")
 
 MOE_OK = 0
 MOE_ERR_INVALID_ARG = -1

@@ -41,9 +41,9 @@ FLAGS = [
 ]
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
+def _compile(src: str, verbose: bool, build_dir: str = BUILD, defines=()) -> str:
+    obj = os.path.join(build_dir, os.path.splitext(src)[0] + ".o")
+    cmd = [HIPCC, *FLAGS, *[f"-D{d}" for d in defines], "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
     if verbose:
         cmd.insert(1, "-Rpass-analysis=kernel-resource-usage")
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -76,22 +76,29 @@ def _link(objs, lib: str) -> None:
     os.replace(tmp, lib)
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, out_dir: str = "", defines=()) -> str:
+    """Build both libraries in-tree; with out_dir, build only the hot-path
+    library there (with extra -D defines), e.g. to compare two builds."""
     if not os.path.exists(HIPCC) and shutil.which("hipcc") is None:
         raise RuntimeError("hipcc not found")
-    os.makedirs(BUILD, exist_ok=True)
-    allsrc = SOURCES + PEAKS_SOURCES
+    bdir = os.path.join(out_dir, "_obj") if out_dir else BUILD
+    os.makedirs(bdir, exist_ok=True)
+    allsrc = SOURCES if out_dir else SOURCES + PEAKS_SOURCES
     with cf.ThreadPoolExecutor(max_workers=min(8, len(allsrc))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), allsrc))
-    _link(objs[:len(SOURCES)], LIB)
-    _link(objs[len(SOURCES):], PEAKS_LIB)
-    return LIB
+        objs = list(ex.map(lambda s: _compile(s, verbose, bdir, defines), allsrc))
+    lib = os.path.join(out_dir, "libmoe_apk.so") if out_dir else LIB
+    _link(objs[:len(SOURCES)], lib)
+    if not out_dir:
+        _link(objs[len(SOURCES):], PEAKS_LIB)
+    return lib
 
 
 if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("--verbose", action="store_true")
+    ap.add_argument("--out-dir", default="", help="build only the hot-path library into this directory")
+    ap.add_argument("-D", dest="defines", action="append", default=[], help="extra preprocessor define")
     args = ap.parse_args()
-    path = build(args.verbose)
+    path = build(args.verbose, args.out_dir, args.defines)
     print(path)
     sys.exit(0)

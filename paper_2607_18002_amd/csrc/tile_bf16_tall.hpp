@@ -16,8 +16,10 @@
 //    ring of D = 2 K steps (full tiles ran alike with D = 2..6; deeper rings
 //    for short tiles made the mixed workload slower);
 //  * A (activation rows, shared by the 4 waves) is loaded into registers one
-//    K step ahead and staged through double-buffered LDS (rows padded by 16
-//    bytes: the fragment reads are free of bank conflicts);
+//    K step ahead (AP = 2, two steps ahead, measured slower in situ) and
+//    staged through double-buffered LDS (rows padded by 16 bytes: the
+//    fragment reads are free of bank conflicts; a third stage, which lets a
+//    step's first fragments be read before the barrier, also measured slower);
 //  * A fragments are read from LDS two MFMA pairs ahead of their use.
 // K order, GLU layout, row maps and the epilogue follow the 128-row tile; the
 // epilogue runs in parts of at most 4 row blocks so its LDS staging stays at
@@ -66,7 +68,7 @@ __device__ __forceinline__ void mma_step_tall(f32x16 (&acc)[MACT][2], const bf16
 
 // Arguments as gemm_tile_bf16 (tile_bf16.hpp), with rows [0, 32*MACT) of a
 // BM-row tile; weights must be packed (moe_pack_weights).
-template <class S, bool GLU, int MACT, int D = 2, class Hook = NoHook>
+template <class S, bool GLU, int MACT, int D = 2, int AP = 1, class Hook = NoHook>
 __device__ __forceinline__ void gemm_tile_tall(const uint16_t* __restrict__ A, int lda,
                                                const uint16_t* __restrict__ B, int ldb, int up_rows, int K,
                                                uint16_t* __restrict__ out, int ldo, char* lds,
@@ -112,31 +114,33 @@ __device__ __forceinline__ void gemm_tile_tall(const uint16_t* __restrict__ A, i
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    u32x4 ra[CA];                                     // A of step s+1
+    u32x4 ra[AP][CA];                                 // A of steps s+1 .. s+AP (slot = step % AP)
     bf16x8 rb[D][2][4];                               // B of steps s .. s+D-1 (slot = step % D)
     const int nk = K / S::BK;                         // a multiple of D and of 2
     constexpr int KB = S::BK * 2;                     // bytes per K step of a row-major A row
     constexpr int KBB = S::BK * 64;                   // bytes per K step of a packed weight block
     static_assert(D % 2 == 0, "the LDS stages (step & 1) repeat within one pass of the B ring");
+    static_assert(AP == 1 || AP == 2, "A is loaded one or two K steps ahead of its LDS store");
 
     // Branch-free K loop (loads past the last step are clamped to it), so the
     // compiler's wait counts stay exact.  A loads go before the B loads of the
     // same step, so waiting for A leaves later B loads in flight.
     const int last = nk - 1;
-    load_a<CA>(ra, Ab, aoff, 0);
+    load_a<CA>(ra[0], Ab, aoff, 0);
 #pragma unroll
     for (int d = 0; d < D; ++d) load_b<S, true>(rb[d], Bb, boff, d * KBB);
-    store_a<CA>(lds0, ra, alds);
-    load_a<CA>(ra, Ab, aoff, (1 < last ? 1 : last) * KB);
+    store_a<CA>(lds0, ra[0], alds);
+#pragma unroll
+    for (int j = 1; j <= AP; ++j) load_a<CA>(ra[j % AP], Ab, aoff, (j < last ? j : last) * KB);
     __syncthreads();
     for (int s0 = 0; s0 < nk; s0 += D) {
 #pragma unroll
         for (int d = 0; d < D; ++d) {
-            const int s = s0 + d;
+            const int s = s0 + d;                     // s % AP == d % AP: D is even
             mma_step_tall<S, MACT>(acc, rb[d], (d & 1) ? lds1 : lds0, lane);
-            store_a<CA>((d & 1) ? lds0 : lds1, ra, alds);
-            const int sb = s + D < last ? s + D : last, sa = s + 2 < last ? s + 2 : last;
-            load_a<CA>(ra, Ab, aoff, sa * KB);
+            store_a<CA>((d & 1) ? lds0 : lds1, ra[(d + 1) % AP], alds);
+            const int sb = s + D < last ? s + D : last, sa = s + 1 + AP < last ? s + 1 + AP : last;
+            load_a<CA>(ra[(d + 1) % AP], Ab, aoff, sa * KB);
             load_b<S, true>(rb[d], Bb, boff, sb * KBB);
             __syncthreads();
         }
