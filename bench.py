@@ -157,7 +157,7 @@ def decode_latency(pipe, specs):
     st = pipe.op_stats()
     tr = pipe.trace_records()
     t0 = pipe.kernel_t0()
-    lat, waits, op_lat = [], [], []
+    lat, waits, op_lat, parts = [], [], [], []
     for i, s in enumerate(specs):
         if s.phase != 1:
             continue
@@ -173,6 +173,10 @@ def decode_latency(pipe, specs):
         us = lambda t: (t.astype(np.float64) - rel) * TICK_NS / 1000.0  # noqa: E731
         lat.extend(us(mine["t_end"]).tolist())
         waits.append(float(us(mine["t_start"]).min()))
+        # the wait in parts: release seen at a boundary, instantiation, first tile start
+        parts.append([round(float((st["t_seen"][i] - rel) * TICK_NS / 1000.0), 1),
+                      round(float((st["t_ready"][i] - st["t_seen"][i]) * TICK_NS / 1000.0), 1),
+                      round(float(us(mine["t_start"]).min() - (st["t_ready"][i] - rel) * TICK_NS / 1000.0), 1)])
         op_lat.append(float(us(mine["t_end"]).max()))
     tiles = {}
     for ph, pname in ((0, "prefill"), (1, "decode")):
@@ -193,6 +197,8 @@ def decode_latency(pipe, specs):
             "tile_p50_us": round(float(np.percentile(lat, 50)), 2),
             "tile_p99_us": round(float(np.percentile(lat, 99)), 2),
             "preempt_wait_max_us": round(max(waits), 2), "preempt_wait_mean_us": round(float(np.mean(waits)), 2),
+            "preempt_wait_parts_us": {"per_decode_op": parts,
+                                      "legend": "release->seen at a tile boundary, instantiation, ->first tile start"},
             "decode_op_latency_us": [round(v, 1) for v in op_lat],
             "prefill_tile_max_us": round(float(ptd.max()), 2) if len(ptd) else None,
             "prefill_tile_p50_us": round(float(np.percentile(ptd, 50)), 2) if len(ptd) else None}

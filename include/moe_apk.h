@@ -276,16 +276,24 @@ typedef struct moe_op_desc {
  * words had returned at t_polled, the tile was claimed at t_claim, its
  * dependencies were met at t_start, and its outputs were committed at t_end. */
 typedef struct moe_trace_rec {
-    int16_t op, stage;        /* stage 1 = GEMM-1 (+activation), 2 = GEMM-2             */
+    int16_t op, stage;        /* stage 1 = GEMM-1 (+activation), 2 = GEMM-2, 3 = combine */
     int16_t wg, xcc;          /* workgroup index and the XCD it ran on                  */
-    int32_t expert, mblk;     /* local expert and row-block within its segment          */
-    int32_t nblk, rows;       /* column block and valid rows in the tile               */
+    int32_t expert, mblk;     /* local expert and row tile within its segment          */
+    int16_t nblk, rows;       /* column block and valid rows in the tile               */
+    /* The inputs of the decision that picked the tile: the quota q' it used,
+     * which phases had claimable work in its polls (bit 0 decode, bit 1
+     * prefill), and how it was taken: 0 from the workgroup's preferred phase,
+     * 1 from the other phase (the preferred phase had no tile left to claim),
+     * 2 claimed ahead during the previous tile, 3 a combine tile.           */
+    int16_t quota_seen;
+    uint8_t phases_seen, how;
     uint64_t t_boundary, t_polled, t_claim, t_start, t_end;
 } moe_trace_rec;
 
 /* Per-op statistics written by the persistent kernel (times in wall-clock ticks). */
 typedef struct moe_op_stats {
-    uint64_t t_ready;         /* instantiation (release observed)                       */
+    uint64_t t_seen;          /* the ready signal was observed (at a tile boundary)    */
+    uint64_t t_ready;         /* instantiation done: the op's tiles became claimable    */
     uint64_t t_first;         /* first tile started                                     */
     uint64_t t_done;          /* op finished: its last tile (combine tile, if fused) committed */
     int32_t x_moe;            /* Eq. (3) footprint: row tiles at the class's tile height */

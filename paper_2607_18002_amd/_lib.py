@@ -58,7 +58,8 @@ class SchedConfig(C.Structure):
 class TraceRec(C.Structure):
     _fields_ = [
         ("op", C.c_int16), ("stage", C.c_int16), ("wg", C.c_int16), ("xcc", C.c_int16),
-        ("expert", _i32), ("mblk", _i32), ("nblk", _i32), ("rows", _i32),
+        ("expert", _i32), ("mblk", _i32), ("nblk", C.c_int16), ("rows", C.c_int16),
+        ("quota_seen", C.c_int16), ("phases_seen", C.c_uint8), ("how", C.c_uint8),
         ("t_boundary", C.c_uint64), ("t_polled", C.c_uint64), ("t_claim", C.c_uint64),
         ("t_start", C.c_uint64), ("t_end", C.c_uint64),
     ]
@@ -66,7 +67,7 @@ class TraceRec(C.Structure):
 
 class OpStats(C.Structure):
     _fields_ = [
-        ("t_ready", C.c_uint64), ("t_first", C.c_uint64), ("t_done", C.c_uint64),
+        ("t_seen", C.c_uint64), ("t_ready", C.c_uint64), ("t_first", C.c_uint64), ("t_done", C.c_uint64),
         ("x_moe", _i32), ("n_tiles", _i32), ("quota", _i32), ("reserved", _i32),
     ]
 

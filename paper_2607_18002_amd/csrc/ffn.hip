@@ -98,7 +98,7 @@ struct KArgs {
     int32_t pre_wg;            // prefill tiles are claimed ahead only by workgroups >= pre_wg
     int32_t pre_dec_all;       // no prefill op in the launch: every workgroup claims decode tiles ahead
     int32_t split;             // static partition: decode only below pre_wg, prefill only at or above
-    int32_t pad_k;
+    int32_t inst_wg;           // decode templates are instantiated by workgroups below this (0: any)
     int64_t spin_limit;
     const uint32_t* abort_word;
     moe_trace_rec* trace;
@@ -117,8 +117,8 @@ struct KArgs {
 struct OpDyn {
     int32_t state, cclaim, left, x_moe;
     int32_t total, pad_b, quota, pad0;
-    unsigned long long t_ready, t_first, t_done;
-    char pad[128 - 56];
+    unsigned long long t_ready, t_first, t_done, t_seen;
+    char pad[128 - 64];
 };
 static_assert(sizeof(OpDyn) == 128, "one L2 line per op");
 
@@ -375,8 +375,10 @@ struct TabCache {
 struct Cmd {
     int32_t kind, op, stage, e, row0, rows32, nb, mtile, mblk, rows, t;
     int32_t pre_next;          // op whose next tile wave 0 claims ahead during this tile, or -1
+    int32_t q_seen, phases, how;   // the decision's inputs and path (recorded in the trace)
     unsigned long long t_boundary, t_polled, t_claim, t_start;
 };
+enum : int32_t { HOW_PREFERRED = 0, HOW_OTHER = 1, HOW_AHEAD = 2, HOW_COMBINE = 3 };
 
 // Lane 0: an op's last tile has committed.  The acquire takes in every other
 // workgroup's released writes of this op before the done word publishes them.
@@ -393,6 +395,7 @@ __device__ void finish_op(const KArgs& a, int o, int total) {
         s.t_ready = ld_relaxed_agent(&d->t_ready);
         s.t_first = ld_relaxed_agent(&d->t_first);
         s.t_done = t;
+        s.t_seen = ld_relaxed_agent(&d->t_seen);
         s.x_moe = ld_relaxed_agent(&d->x_moe);
         s.n_tiles = total;
         s.quota = ld_relaxed_agent(&d->quota);
@@ -593,8 +596,10 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
                 if (idx < a.trace_cap) {
                     moe_trace_rec r;
                     r.op = (int16_t)prev.op; r.stage = (int16_t)prev.stage; r.wg = (int16_t)wg;
-                    r.xcc = (int16_t)xcc_id(); r.expert = prev.e; r.mblk = prev.mblk; r.nblk = prev.nb;
-                    r.rows = prev.rows; r.t_boundary = prev.t_boundary; r.t_polled = prev.t_polled;
+                    r.xcc = (int16_t)xcc_id(); r.expert = prev.e; r.mblk = prev.mblk; r.nblk = (int16_t)prev.nb;
+                    r.rows = (int16_t)prev.rows; r.quota_seen = (int16_t)prev.q_seen;
+                    r.phases_seen = (uint8_t)prev.phases; r.how = (uint8_t)prev.how;
+                    r.t_boundary = prev.t_boundary; r.t_polled = prev.t_polled;
                     r.t_claim = prev.t_claim; r.t_start = prev.t_start; r.t_end = t_end;
                     a.trace[idx] = r;
                 }
@@ -658,6 +663,11 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
         return;
     }
     const uint64_t now = wall_ticks();
+    // phases with claimable work in the polls this decision uses (recorded in the trace)
+    const bool active = state == ST_ACTIVE || (COMB && state == ST_COMBINING);
+    const uint64_t dmask = __ballot(active && phase == MOE_DECODE);
+    const uint64_t pmask = __ballot(active && phase == MOE_PREFILL);
+    const int phases_seen = (dmask ? 1 : 0) | (pmask ? 2 : 0);
 
     // 3b. a claim made ahead during the previous tile (the hook claimed in this
     //     XCD's queue of op prev.pre_next): take it if it landed inside the queue
@@ -667,15 +677,23 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
         if (pt < __shfl(own_size, pre_op_u, 64)) {
             finish_prev();
             const bool more = take_tile(a, pre_op_u, myx, pt, myx, tab, cmd, t_boundary, now);
-            if (lane == 0) cmd->pre_next = more && pre_allowed(a, wg, q, phase_of(a, pre_op_u)) ? pre_op_u : -1;
+            if (lane == 0) {
+                cmd->pre_next = more && pre_allowed(a, wg, q, phase_of(a, pre_op_u)) ? pre_op_u : -1;
+                cmd->q_seen = q; cmd->phases = phases_seen; cmd->how = HOW_AHEAD;
+            }
             idle = 0;
             return;
         }
     }
 
-    // 4. ready signals of waiting operation templates -> instantiate one of them
+    // 4. ready signals of waiting operation templates -> instantiate one of them.
+    //    A decode template is instantiated only by a workgroup below the
+    //    smallest q' the launch can produce, which therefore prefers decode and
+    //    takes the op's first tile at its very next boundary: a decode op waits
+    //    for one tile boundary of those workgroups plus its instantiation.
     bool ready = false;
-    if (state == ST_WAIT) {
+    const bool may_inst = phase == MOE_PREFILL || a.inst_wg == 0 || wg < a.inst_wg;
+    if (state == ST_WAIT && may_inst) {
         ready = true;
         const uint32_t* rw = sta[o_l].rel_word;
         if (rw) ready = __hip_atomic_load(rw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != 0u;
@@ -690,7 +708,10 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
     if (rmask) {
         const int o = __ffsll((long long)rmask) - 1;
         int won = 0;
-        if (lane == o) won = atomicCAS(&dyn[o].state, ST_WAIT, ST_INIT) == ST_WAIT;
+        if (lane == o) {
+            won = atomicCAS(&dyn[o].state, ST_WAIT, ST_INIT) == ST_WAIT;
+            if (won) __hip_atomic_store(&dyn[o].t_seen, (unsigned long long)now, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
         if (__ballot(won)) {
             finish_prev();
             if (lane == 0) { cmd->kind = CMD_INST; cmd->op = o; }
@@ -701,10 +722,7 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
 
     // 5. claim: decode first on workgroups below q', prefill first elsewhere;
     //    within a phase: the own XCD's queue first, then steal from the others
-    const bool active = state == ST_ACTIVE || (COMB && state == ST_COMBINING);
     const uint64_t combining = COMB ? __ballot(state == ST_COMBINING) : 0ull;
-    const uint64_t dmask = __ballot(active && phase == MOE_DECODE);
-    const uint64_t pmask = __ballot(active && phase == MOE_PREFILL);
     const uint64_t own_avail = __ballot(active && own_claim < own_size);
     const bool prefer_decode = a.split ? wg < a.pre_wg : wg < q;
     const uint64_t order[2] = {prefer_decode ? dmask : pmask, prefer_decode ? pmask : dmask};
@@ -720,6 +738,7 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
                 if (t >= n3s[o]) continue;
                 finish_prev();
                 take_combine(o, t, cmd, t_boundary, now);
+                if (lane == 0) { cmd->q_seen = q; cmd->phases = phases_seen; cmd->how = HOW_COMBINE; }
                 idle = 0;
                 return;
             }
@@ -754,7 +773,10 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
             if (src < 0) continue;
             finish_prev();
             const bool more = take_tile(a, o, src, t, myx, tab, cmd, t_boundary, now);
-            if (lane == 0) cmd->pre_next = more && pre_allowed(a, wg, q, phase_of(a, o)) ? o : -1;
+            if (lane == 0) {
+                cmd->pre_next = more && pre_allowed(a, wg, q, phase_of(a, o)) ? o : -1;
+                cmd->q_seen = q; cmd->phases = phases_seen; cmd->how = p == 0 ? HOW_PREFERRED : HOW_OTHER;
+            }
             idle = 0;
             return;
         }
@@ -765,29 +787,47 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
 }
 
 // Whole workgroup: build the row-tile table of an operation whose ready signal was seen.
-__device__ void instantiate(const KArgs& a, int o, int32_t* scan) {
+__device__ void instantiate(const KArgs& a, int o, int32_t* scan, int32_t* s_cnt, int32_t* s_off) {
     const OpArg& op = a.op[o];
     OpDyn* d = dyn_of(a.ws) + o;
     if (static_of(a.ws)[o].rel_word) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");  // system scope: peer-written inputs
     uint64_t* table = (uint64_t*)(arr_of(a.ws) + op.table_off);
     uint32_t* grp = (uint32_t*)(arr_of(a.ws) + op.grp_off);
     const int gmax = a.gmax;
-    for (int e = threadIdx.x; e < op.E; e += 256) scan[e] = sched::row_tiles(op.counts[e], op.mt);
+    // one round trip for the op's inputs: counts and offsets together, into LDS
+    for (int e = threadIdx.x; e < op.E; e += 256) {
+        const int c = op.counts[e], off = op.offsets[e];
+        s_cnt[e] = c;
+        s_off[e] = off;
+        scan[e] = sched::row_tiles(c, op.mt);
+    }
     __syncthreads();
     __shared__ int32_t s_total, s_bad, s_cut[kXcds + 1];
-    if (threadIdx.x == 0) {
-        int run = 0;
-        for (int e = 0; e < op.E; ++e) { const int v = scan[e]; scan[e] = run; run += v; }
-        s_total = run;
-        s_bad = 0;
+    if (threadIdx.x < 64) {
+        // exclusive scan of the row-tile counts by wave 0: each lane sums a run
+        // of up to 16 experts, the run totals are scanned across the wave
+        const int lane = threadIdx.x, per = (op.E + 63) / 64, e0 = lane * per;
+        const int e1 = e0 + per < op.E ? e0 + per : op.E;
+        int sum = 0;
+        for (int e = e0; e < e1; ++e) sum += scan[e];
+        int incl = sum;
+#pragma unroll
+        for (int d = 1; d < 64; d <<= 1) {
+            const int v = __shfl_up(incl, d, 64);
+            if (lane >= d) incl += v;
+        }
+        int run = incl - sum;
+        for (int e = e0; e < e1; ++e) { const int v = scan[e]; scan[e] = run; run += v; }
+        if (lane == 63) s_total = incl;
+        if (lane == 0) s_bad = 0;
     }
     __syncthreads();
     for (int e = threadIdx.x; e < op.E; e += 256) {
-        const int c = op.counts[e];
+        const int c = s_cnt[e];
         const int nt = sched::row_tiles(c, op.mt);               // Eq. (3): ceil(m_e / M_t) row tiles
         const int nb32 = (c + kSegAlign - 1) / kSegAlign;        // 32-row blocks of the segment
         const int pos = scan[e];
-        const int off = op.offsets[e];
+        const int off = s_off[e];
         if (pos + nt > op.max_mtiles || off < 0 || (long)off + (long)nb32 * kSegAlign > op.capacity) { s_bad = 1; continue; }
         const int ng = sched::n_groups(nt, gmax);
         for (int j = 0; j < ng; ++j) {                     // near-equal groups of this expert's row tiles
@@ -851,6 +891,7 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
     extern __shared__ __align__(16) char lds[];
     __shared__ Cmd cmd;
     __shared__ int32_t scan[1024];
+    __shared__ int32_t s_cnt[1024], s_off[1024];              // instantiation: the op's counts and offsets
     __shared__ unsigned long long s_t0;
     __shared__ TabCache tab;
     __shared__ int32_t s_n3[MOE_MAX_OPS];                     // combine tiles per op
@@ -888,7 +929,7 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
         if (kind == CMD_INST) {
             const int o = __builtin_amdgcn_readfirstlane(cmd.op);
             __syncthreads();
-            instantiate(a, o, scan);
+            instantiate(a, o, scan, s_cnt, s_off);
             __syncthreads();
             continue;
         }
@@ -1126,6 +1167,8 @@ moe_status_t launch_ffn(const moe_op_desc* ops, int32_t n_ops, const moe_sched_c
             return fail(MOE_ERR_INVALID_ARG, "static_partition needs a fixed quota 0 < q' < n_workgroups");
     }
     a.pre_wg = !any_decode ? 0 : (a.x_star <= 0 ? moeapk::decode_quota(a.q, 0, 0, a.q_max, a.c) : a.q_max);
+    // the smallest q' of any decode op (Eq. (4) is non-decreasing in x_moe >= 1)
+    a.inst_wg = a.x_star <= 0 ? a.pre_wg : moeapk::decode_quota(a.q, 1, a.x_star, a.q_max, a.c);
     a.spin_limit = cfg->spin_limit > 0 ? cfg->spin_limit : (int64_t)2000000;
     a.abort_word = cfg->abort_word;
     a.trace = cfg->trace;

@@ -108,14 +108,61 @@ def test_lone_phase_uses_every_workgroup(dev):
     assert set(np.unique(tr["xcc"]).tolist()) == set(range(8))
 
 
+HOW_PREFERRED, HOW_OTHER, HOW_AHEAD, HOW_COMBINE = 0, 1, 2, 3
+
+
+def _claim_lower_bounds(tr):
+    """A time no later than each tile's claim atomic: its boundary's polls
+    returned (t_polled) before the claim; a tile claimed ahead was claimed
+    during the workgroup's previous tile, after that tile started."""
+    lb = tr["t_polled"].astype(np.int64).copy()
+    ahead = np.nonzero(tr["how"] == HOW_AHEAD)[0]
+    for i in ahead:
+        m = (tr["wg"] == tr["wg"][i]) & (tr["t_start"] < tr["t_start"][i])
+        lb[i] = int(tr["t_start"][m].max())
+    return lb
+
+
+def _check_policy(tr, st, phases_of_op):
+    """Every tile's recorded decision inputs (q' used, phases with claimable
+    work in its polls, path) against the policy: a workgroup below q' prefers
+    decode, the others prefill; a tile of the non-preferred phase is taken only
+    when the preferred phase had no tile left to claim -- and then every tile of
+    the preferred phase's active op had been claimed before that decision
+    (a claim's atomic precedes the stamp of the failed attempt that followed it).
+    Returns the number of decode tiles claimed while both phases were active."""
+    lb = _claim_lower_bounds(tr)
+    phase = phases_of_op[tr["op"]]
+    contended = 0
+    for i in range(len(tr)):
+        how = int(tr["how"][i])
+        if how in (HOW_AHEAD, HOW_COMBINE):
+            continue
+        pref = 1 if tr["wg"][i] < tr["quota_seen"][i] else 0     # 1 decode, 0 prefill
+        if how == HOW_PREFERRED:
+            assert phase[i] == pref, ("tile of the non-preferred phase recorded as preferred", tr[i])
+        else:
+            assert phase[i] != pref, tr[i]
+            if tr["phases_seen"][i] & (1 if pref == 1 else 2):
+                # the preferred phase was active: all its active op's tiles had been claimed
+                ops = [o for o in np.nonzero(phases_of_op == pref)[0]
+                       if st["t_ready"][o] <= tr["t_polled"][i] and st["t_done"][o] >= tr["t_polled"][i]]
+                for o in ops:
+                    mine = tr["op"] == o
+                    assert np.all(lb[mine] < int(tr["t_claim"][i])), (
+                        "the other phase was taken while the preferred phase still had unclaimed tiles", tr[i])
+        if phase[i] == 1 and tr["phases_seen"][i] == 3:
+            contended += 1
+            if how == HOW_PREFERRED:
+                assert tr["wg"][i] < tr["quota_seen"][i]
+    return contended
+
+
 def test_decode_quota_under_contention(dev):
-    """While prefill still has unclaimed tiles, decode tiles run only on
-    workgroups below q'.  Only decode tiles whose claim decision was taken
-    after prefill became claimable count: before that, decode was the lone
-    active phase and every workgroup may take it.  Decode is released 40 us
-    after the launch, well past the workgroups' first boundaries, so prefill is
-    claimable first (a release inside the launch-start window can let decode be
-    instantiated first and be claimed whole as the lone phase)."""
+    """While prefill has claimable tiles, decode tiles run only on workgroups
+    below q' (decided from the inputs each decision recorded, no time windows),
+    and workgroups at or above q' take decode tiles only once every prefill
+    tile has been claimed."""
     cfg = custom_config(2, cfg_id=404, H=1024, I=1024, prefill_tokens=8192, decode_tokens=256, E_global=64,
                         E_local=16, top_k=8)
     specs, _, _ = layer_specs(cfg, 0, dev, decode=dict(release_after_ns=40_000))
@@ -124,13 +171,53 @@ def test_decode_quota_under_contention(dev):
     tr = pipe.trace_records()
     st = pipe.op_stats()
     assert st["quota"][1] == 64
-    first_prefill_claim = tr[tr["op"] == 0]["t_claim"].min()
-    last_prefill_claim = tr[tr["op"] == 0]["t_claim"].max()
-    # 5 us margins: the polled words a decision uses are older than t_polled by up to an epilogue
-    dec = tr[(tr["op"] == 1) & (tr["t_polled"] > first_prefill_claim + 500) &
-             (tr["t_claim"] + 500 < last_prefill_claim)]
-    assert len(dec) > 0
-    assert dec["wg"].max() < 64
+    contended = _check_policy(tr, st, np.array([s.phase for s in specs]))
+    assert contended > 0, "no decode tile ran while prefill was active: the test checked nothing"
+    dec = tr[(tr["op"] == 1) & (tr["phases_seen"] == 3) & (tr["how"] != HOW_OTHER)]
+    assert len(dec) and dec["wg"].max() < 64
+
+
+@pytest.mark.parametrize("release_us", [10, 45, 130])
+def test_bounded_preemption(dev, release_us):
+    """Bounded tile-level preemption, term by term from the trace: a decode op
+    released while prefill tiles run is seen at the first tile boundary of a
+    workgroup below q' after its release (so no later than the remaining time
+    of those workgroups' prefill tiles, plus one boundary), is instantiated
+    by that workgroup, which takes the op's first tile at its very next
+    boundary.  The epoch (one boundary's decision) is the longest boundary
+    measured in the same launch."""
+    cfg = custom_config(2, cfg_id=405, H=1024, I=1024, prefill_tokens=8192, decode_tokens=256, E_global=64,
+                        E_local=16, top_k=8)
+    specs, _, _ = layer_specs(cfg, 0, dev, decode=dict(release_after_ns=release_us * 1000))
+    pipe = _pipe(dev, specs, trace_capacity=1 << 17, decode_quota_wg=64)
+    assert pipe.statuses() == (0, 0)
+    tr = pipe.trace_records()
+    st = pipe.op_stats()
+    t0 = pipe.kernel_t0()
+    R = t0 + int(release_us * 1000 / TICK_NS)
+    q = int(st["quota"][1])
+    epoch = int((tr["t_claim"] - tr["t_boundary"]).max())
+    pre = tr[tr["op"] == 0]
+    # each decode-preferring workgroup decides again right after the first of
+    # its tiles to end after the release (a tile in flight at the release, or
+    # one it claimed at a decision taken just before it)
+    rem = []
+    for w in range(q):
+        m = tr[(tr["wg"] == w) & (tr["t_end"] > R)]
+        if len(m):
+            rem.append(int(m["t_end"].min()) - R)
+    seen, ready = int(st["t_seen"][1]), int(st["t_ready"][1])
+    first = int(tr[tr["op"] == 1]["t_start"].min())
+    us = lambda t: t * TICK_NS / 1000.0  # noqa: E731
+    print(f"release {release_us} us: seen +{us(seen - R):.1f} us (bound {us(min(rem) + epoch):.1f}), instantiated "
+          f"in {us(ready - seen):.1f} us, first tile +{us(first - ready):.1f} us after (epoch {us(epoch):.1f}); "
+          f"wait {us(first - R):.1f} us, longest prefill tile {us(int((pre['t_end'] - pre['t_start']).max())):.1f} us")
+    assert seen >= R
+    assert seen - R <= min(rem) + epoch
+    assert first - ready <= epoch
+    # the first decode tile ran on the workgroup that instantiated the op, or on another below q'
+    fd = tr[(tr["op"] == 1)]
+    assert fd[np.argmin(fd["t_start"])]["wg"] < q
 
 
 def test_results_independent_of_schedule(dev):
