@@ -356,6 +356,18 @@ moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32_t n_ops,
                                         const moe_sched_config* cfg, void* workspace,
                                         int32_t* status_word, void* stream);
 
+/* Comparison baseline (Evaluation, "Overhead of Tile-Level Scheduling": the
+ * persistent kernel against plain grouped-GEMM launches): the same tiles as
+ * moe_grouped_ffn_persistent with no device scheduler.  Per op, in op order:
+ * one planning kernel (the row-tile table of Eq. (3)), one GEMM-1 grid and one
+ * GEMM-2 grid (the kernel boundary is the dependency between them), each grid
+ * one workgroup per CU taking tiles round robin, column block major.  Readiness
+ * fields, the decode quota and the fused combine (moe_op_desc.y) are ignored;
+ * h and y_perm equal the persistent kernel's bit for bit.  workspace:
+ * moe_ffn_workspace_bytes() bytes; status_word is reset by the first launch. */
+moe_status_t moe_grouped_ffn_plain(const moe_op_desc* ops, int32_t n_ops, void* workspace, int32_t* status_word,
+                                   void* stream);
+
 /* For callers that cannot allocate device memory -- code under HIP graph
  * capture, tight serving loops, harnesses that forbid allocation: the same
  * launch as moe_grouped_ffn_persistent (same kernels, results, readiness and

@@ -112,6 +112,7 @@ PROTOTYPES = {
     "moe_ffn_workspace_bytes": (C.c_size_t, [C.POINTER(OpDesc), _i32, C.POINTER(SchedConfig)]),
     "moe_grouped_ffn_persistent": (_i32, [C.POINTER(OpDesc), _i32, C.POINTER(SchedConfig), _p, _p, _p]),
     "moe_grouped_ffn_persistent_noalloc": (_i32, [C.POINTER(OpDesc), _i32, C.POINTER(SchedConfig), _p, _p]),
+    "moe_grouped_ffn_plain": (_i32, [C.POINTER(OpDesc), _i32, _p, _p, _p]),
     "moe_combine": (_i32, [_p, _p, _p, _i32, _i32, _i32, _p, _i32, _p]),
     "moe_pack_weights": (_i32, [_p, _p, _i32, _i32, _i32, _i32, _p]),
     "moe_x_moe": (_i32, [C.POINTER(_i32), _i32, _i32]),

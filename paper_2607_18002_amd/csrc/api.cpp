@@ -123,19 +123,8 @@ int32_t moe_sched_layout(const int32_t* counts, const int32_t* offsets, int32_t 
     // the instantiation: table and group entries of every row tile
     std::vector<uint64_t> table(total > 0 ? total : 1);
     std::vector<uint32_t> grp(total > 0 ? total : 1);
-    for (int e = 0; e < E_local; ++e) {
-        const int c = counts[e], nt = S::row_tiles(c, M_t), pos = scan[e], ng = S::n_groups(nt, gmax);
-        for (int j = 0; j < ng; ++j) {
-            int glo, ghi;
-            S::group_range(nt, ng, j, glo, ghi);
-            for (int mb = glo; mb < ghi; ++mb) {
-                int first, rows;
-                S::tile_rows(c, nt, mb, first, rows);
-                table[pos + mb] = S::pack_entry(e, mb, rows, offsets[e] + first);
-                grp[pos + mb] = S::pack_group(pos + glo, ghi - glo);
-            }
-        }
-    }
+    for (int p = 0; p < total; ++p)
+        if (!S::row_tile_entry(scan.data(), counts, offsets, E_local, total, M_t, gmax, p, table[p], grp[p])) return -2;
     for (int p = 0; p < total; ++p) {
         int e, mb, rows, row0;
         S::unpack_entry(table[p], e, mb, rows, row0);

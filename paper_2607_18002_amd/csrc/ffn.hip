@@ -787,13 +787,12 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
 }
 
 // Whole workgroup: build the row-tile table of an operation whose ready signal was seen.
-__device__ void instantiate(const KArgs& a, int o, int32_t* scan, int32_t* s_cnt, int32_t* s_off) {
-    const OpArg& op = a.op[o];
-    OpDyn* d = dyn_of(a.ws) + o;
-    if (static_of(a.ws)[o].rel_word) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");  // system scope: peer-written inputs
-    uint64_t* table = (uint64_t*)(arr_of(a.ws) + op.table_off);
-    uint32_t* grp = (uint32_t*)(arr_of(a.ws) + op.grp_off);
-    const int gmax = a.gmax;
+// Whole workgroup: the row-tile table and group entries of an op from its
+// counts and offsets (Eq. (3) row tiles of near-equal height, weight-sharing
+// groups), with scan[e] = the first row tile of expert e; *s_total = x_moe,
+// *s_bad = 1 if the offsets or counts do not fit the op's buffers.
+__device__ void build_row_tiles(const OpArg& op, uint64_t* table, uint32_t* grp, int gmax, int32_t* scan,
+                                int32_t* s_cnt, int32_t* s_off, int32_t* s_total, int32_t* s_bad) {
     // one round trip for the op's inputs: counts and offsets together, into LDS
     for (int e = threadIdx.x; e < op.E; e += 256) {
         const int c = op.counts[e], off = op.offsets[e];
@@ -802,7 +801,6 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan, int32_t* s_cnt
         scan[e] = sched::row_tiles(c, op.mt);
     }
     __syncthreads();
-    __shared__ int32_t s_total, s_bad, s_cut[kXcds + 1];
     if (threadIdx.x < 64) {
         // exclusive scan of the row-tile counts by wave 0: each lane sums a run
         // of up to 16 experts, the run totals are scanned across the wave
@@ -818,30 +816,42 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan, int32_t* s_cnt
         }
         int run = incl - sum;
         for (int e = e0; e < e1; ++e) { const int v = scan[e]; scan[e] = run; run += v; }
-        if (lane == 63) s_total = incl;
-        if (lane == 0) s_bad = 0;
+        if (lane == 63) *s_total = incl;
+        if (lane == 0) *s_bad = 0;
     }
     __syncthreads();
+    // every expert's segment must fit the op's buffers and tables
     for (int e = threadIdx.x; e < op.E; e += 256) {
-        const int c = s_cnt[e];
-        const int nt = sched::row_tiles(c, op.mt);               // Eq. (3): ceil(m_e / M_t) row tiles
+        const int c = s_cnt[e], nt = sched::row_tiles(c, op.mt), off = s_off[e];
         const int nb32 = (c + kSegAlign - 1) / kSegAlign;        // 32-row blocks of the segment
-        const int pos = scan[e];
-        const int off = s_off[e];
-        if (pos + nt > op.max_mtiles || off < 0 || (long)off + (long)nb32 * kSegAlign > op.capacity) { s_bad = 1; continue; }
-        const int ng = sched::n_groups(nt, gmax);
-        for (int j = 0; j < ng; ++j) {                     // near-equal groups of this expert's row tiles
-            int glo, ghi;
-            sched::group_range(nt, ng, j, glo, ghi);
-            for (int mb = glo; mb < ghi; ++mb) {
-                int first, rows;
-                sched::tile_rows(c, nt, mb, first, rows);
-                table[pos + mb] = sched::pack_entry(e, mb, rows, off + first);
-                grp[pos + mb] = sched::pack_group(pos + glo, ghi - glo);
-            }
-        }
+        if (scan[e] + nt > op.max_mtiles || off < 0 || (long)off + (long)nb32 * kSegAlign > op.capacity) *s_bad = 1;
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");       // each wave's entries, before ACTIVE is published
+    // one thread per row tile: its expert, its row blocks (Eq. (3): ceil(m_e / M_t)
+    // row tiles of near-equal height) and its weight-sharing group
+    const int total = *s_total < op.max_mtiles ? *s_total : op.max_mtiles;
+    for (int p = threadIdx.x; p < total; p += 256) {
+        uint64_t ent;
+        uint32_t g;
+        if (!sched::row_tile_entry(scan, s_cnt, s_off, op.E, total, op.mt, gmax, p, ent, g)) continue;
+        // device-coherent stores: a reader on any XCD that has seen the op
+        // ACTIVE reads them from the coherence point
+        __hip_atomic_store(table + p, ent, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(grp + p, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+__device__ void instantiate(const KArgs& a, int o, int32_t* scan, int32_t* s_cnt, int32_t* s_off) {
+    const OpArg& op = a.op[o];
+    OpDyn* d = dyn_of(a.ws) + o;
+    if (static_of(a.ws)[o].rel_word) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");  // system scope: peer-written inputs
+    const int gmax = a.gmax;
+    __shared__ int32_t s_total, s_bad, s_cut[kXcds + 1];
+    build_row_tiles(op, (uint64_t*)(arr_of(a.ws) + op.table_off), (uint32_t*)(arr_of(a.ws) + op.grp_off), gmax, scan,
+                    s_cnt, s_off, &s_total, &s_bad);
+    // Each wave's entries have reached the coherence point before the barrier
+    // that precedes ACTIVE; no L2 write-back is needed (an agent-scope release
+    // would write back the XCD's whole L2, dirtied by the kernels before).
+    wait_own_stores();
     // Queue cuts: cut x (1..kXcds-1) is the group boundary nearest to x/kXcds
     // of the row tiles (ties: the lower one), so no group spans two queues;
     // cuts are non-decreasing in x.
@@ -879,7 +889,8 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan, int32_t* s_cnt
             if (op.n3 > 0) st_release_agent(&d->state, (int32_t)ST_COMBINING);   // its combine writes zeros
             else finish_op(a, o, 0);
         } else {
-            st_release_agent(&d->state, (int32_t)ST_ACTIVE);   // table entries written before this
+            wait_own_stores();                                  // queue ranges and counters, before ACTIVE
+            __hip_atomic_store(&d->state, (int32_t)ST_ACTIVE, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
 }
@@ -1024,24 +1035,12 @@ extern "C" size_t moe_ffn_workspace_bytes(const moe_op_desc* ops, int32_t n_ops,
 
 namespace {
 
-// The one launch path of both FFN entry points: checks, kernel arguments,
-// the init kernel (which zeroes the scheduler state with ordinary stores) and
-// the persistent kernel.  `workspace` holds at least ws_bytes_for(ops) bytes.
-moe_status_t launch_ffn(const moe_op_desc* ops, int32_t n_ops, const moe_sched_config* cfg, void* workspace,
-                        int32_t* status_word, void* stream) {
+// Checks every op descriptor and fills the kernel's per-op arguments and the
+// init kernel's readiness fields; off = the ops' array bytes.  Shared by the
+// persistent launch and the plain-grid baseline.
+moe_status_t fill_ops(const moe_op_desc* ops, int32_t n_ops, int wc_khz, KArgs& a, InitArgs& ia, size_t& off) {
     using moeapk_host::fail;
-    if (!ops || !cfg || !workspace || !status_word) return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn_persistent: null pointer");
-    if (n_ops < 1 || n_ops > MOE_MAX_OPS)
-        return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn_persistent: n_ops=%d outside [1,%d]", n_ops, MOE_MAX_OPS);
-    int cu = 0, wc_khz = 0;
-    moe_status_t st = moeapk_host::check_device(&cu, &wc_khz);
-    if (st != MOE_OK) return st;
-
-    KArgs a;
-    memset(&a, 0, sizeof(a));
-    InitArgs ia;
-    memset(&ia, 0, sizeof(ia));
-    size_t off = 0;                                   // bytes from the arrays base
+    off = 0;                                          // bytes from the arrays base
     for (int o = 0; o < n_ops; ++o) {
         const moe_op_desc& d = ops[o];
         if (d.phase != MOE_PREFILL && d.phase != MOE_DECODE) return fail(MOE_ERR_INVALID_ARG, "op %d: bad phase %d", o, d.phase);
@@ -1139,6 +1138,29 @@ moe_status_t launch_ffn(const moe_op_desc* ops, int32_t n_ops, const moe_sched_c
         ia.deps[o] = d.depends_on_op;
         ia.phases[o] = d.phase;
     }
+    return MOE_OK;
+}
+
+// The one launch path of both FFN entry points: checks, kernel arguments,
+// the init kernel (which zeroes the scheduler state with ordinary stores) and
+// the persistent kernel.  `workspace` holds at least ws_bytes_for(ops) bytes.
+moe_status_t launch_ffn(const moe_op_desc* ops, int32_t n_ops, const moe_sched_config* cfg, void* workspace,
+                        int32_t* status_word, void* stream) {
+    using moeapk_host::fail;
+    if (!ops || !cfg || !workspace || !status_word) return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn_persistent: null pointer");
+    if (n_ops < 1 || n_ops > MOE_MAX_OPS)
+        return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn_persistent: n_ops=%d outside [1,%d]", n_ops, MOE_MAX_OPS);
+    int cu = 0, wc_khz = 0;
+    moe_status_t st = moeapk_host::check_device(&cu, &wc_khz);
+    if (st != MOE_OK) return st;
+
+    KArgs a;
+    memset(&a, 0, sizeof(a));
+    InitArgs ia;
+    memset(&ia, 0, sizeof(ia));
+    size_t off = 0;
+    st = fill_ops(ops, n_ops, wc_khz, a, ia, off);
+    if (st != MOE_OK) return st;
     if (kArraysOff + off > (size_t)INT32_MAX) return fail(MOE_ERR_UNSUPPORTED, "scheduler workspace too large");
     int n_wg = cfg->n_workgroups > 0 ? cfg->n_workgroups : cu;
     a.n_ops = n_ops;
@@ -1231,7 +1253,103 @@ moe_status_t scratch_address(void** ptr) {
     return MOE_OK;
 }
 
+// ----------------------------------------------------------------------------- plain-grid baseline
+// The same tiles with no device scheduler: per op, a planning kernel builds the
+// row-tile table (one workgroup), then one grid per GEMM runs its tiles round
+// robin over one workgroup per CU, column block major so that consecutive
+// workgroups share a weight slice; the kernel boundary is the GEMM-1 -> GEMM-2
+// dependency.  For measuring what the persistent scheduler costs or saves.
+struct PlainArgs {
+    OpArg op;
+    char* ws;
+    int32_t o, gmax, reset_status;
+    int32_t* status;
+};
+
+__global__ __launch_bounds__(256) void plain_plan_kernel(const PlainArgs p) {
+    __shared__ int32_t scan[1024], s_cnt[1024], s_off[1024];
+    __shared__ int32_t s_total, s_bad;
+    if (p.reset_status && threadIdx.x == 0) *p.status = MOE_OK;
+    __syncthreads();
+    build_row_tiles(p.op, (uint64_t*)(arr_of(p.ws) + p.op.table_off), (uint32_t*)(arr_of(p.ws) + p.op.grp_off),
+                    p.gmax, scan, s_cnt, s_off, &s_total, &s_bad);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        if (s_bad) set_status(p.status, MOE_ERR_CAPACITY);
+        dyn_of(p.ws)[p.o].x_moe = s_bad ? 0 : s_total;
+    }
+}
+
+template <int STAGE>
+__global__ __launch_bounds__(256, 1) void plain_gemm_kernel(const PlainArgs p) {
+    extern __shared__ __align__(16) char lds[];
+    const OpArg& op = p.op;
+    const int xm = __builtin_amdgcn_readfirstlane(*(volatile const int32_t*)&dyn_of(p.ws)[p.o].x_moe);
+    const int n = STAGE == 1 ? op.n1 : op.n2;
+    const uint64_t* table = (const uint64_t*)(arr_of(p.ws) + op.table_off);
+    for (int t = blockIdx.x; t < xm * n; t += gridDim.x) {
+        const int nb = t / xm, mtile = t - nb * xm;
+        int e, mblk, rows, row0;
+        sched::unpack_entry(table[mtile], e, mblk, rows, row0);
+        e = __builtin_amdgcn_readfirstlane(e);
+        rows = __builtin_amdgcn_readfirstlane(rows);
+        row0 = __builtin_amdgcn_readfirstlane(row0);
+        const int rows32 = (rows + 31) & ~31;
+        if (e >= op.E || rows < 1 || rows > op.mt || row0 < 0 || (long)row0 + rows32 > (long)op.capacity) {
+            if (threadIdx.x == 0) set_status(p.status, MOE_ERR_INTERNAL);
+            return;
+        }
+        run_tile(op, STAGE, row0, rows32, nb, e, lds, NoHook{});
+        wait_own_stores();
+        __syncthreads();                                      // the next tile reuses the LDS
+    }
+}
+
 }  // namespace
+
+extern "C" moe_status_t moe_grouped_ffn_plain(const moe_op_desc* ops, int32_t n_ops, void* workspace,
+                                              int32_t* status_word, void* stream) {
+    using moeapk_host::fail;
+    if (!ops || !workspace || !status_word) return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn_plain: null pointer");
+    if (n_ops < 1 || n_ops > MOE_MAX_OPS)
+        return fail(MOE_ERR_INVALID_ARG, "moe_grouped_ffn_plain: n_ops=%d outside [1,%d]", n_ops, MOE_MAX_OPS);
+    int cu = 0, wc_khz = 0;
+    moe_status_t st = moeapk_host::check_device(&cu, &wc_khz);
+    if (st != MOE_OK) return st;
+    KArgs a;
+    memset(&a, 0, sizeof(a));
+    InitArgs ia;
+    memset(&ia, 0, sizeof(ia));
+    size_t off = 0;
+    st = fill_ops(ops, n_ops, wc_khz, a, ia, off);
+    if (st != MOE_OK) return st;
+    static bool attr_set = false;
+    if (!attr_set) {
+        if (hipFuncSetAttribute((const void*)plain_gemm_kernel<1>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                kLdsBytes) != hipSuccess ||
+            hipFuncSetAttribute((const void*)plain_gemm_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                kLdsBytes) != hipSuccess)
+            return fail(MOE_ERR_HIP, "hipFuncSetAttribute(LDS=%d) failed", kLdsBytes);
+        attr_set = true;
+    }
+    hipStream_t s = (hipStream_t)stream;
+    for (int o = 0; o < n_ops; ++o) {
+        PlainArgs p;
+        memset(&p, 0, sizeof(p));
+        p.op = a.op[o];
+        p.ws = (char*)workspace;
+        p.o = o;
+        p.gmax = kDefaultGroup;
+        p.reset_status = o == 0;
+        p.status = status_word;
+        hipLaunchKernelGGL(plain_plan_kernel, dim3(1), dim3(256), 0, s, p);
+        hipLaunchKernelGGL(plain_gemm_kernel<1>, dim3(cu), dim3(256), kLdsBytes, s, p);
+        hipLaunchKernelGGL(plain_gemm_kernel<2>, dim3(cu), dim3(256), kLdsBytes, s, p);
+    }
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return fail(MOE_ERR_HIP, "moe_grouped_ffn_plain: launch failed: %s", hipGetErrorString(err));
+    return MOE_OK;
+}
 
 extern "C" moe_status_t moe_grouped_ffn_persistent(const moe_op_desc* ops, int32_t n_ops, const moe_sched_config* cfg,
                                                    void* workspace, int32_t* status_word, void* stream) {

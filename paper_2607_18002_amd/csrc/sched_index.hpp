@@ -29,9 +29,12 @@ MOE_HD int row_tiles(int m, int mt) { return m > 0 ? (m + mt - 1) / mt : 0; }
 // Row tile mb (of nt) of an expert with m rows: near-equal heights in whole
 // 32-row blocks; tile mb holds blocks [b0, b1) of the segment, so its first
 // row is 32*b0 and it has min(m, 32*b1) - 32*b0 valid rows.
+// (Products of two row-tile or block counts stay below 2^32: both are below
+// kMaxRowTiles = 2^16, so unsigned 32-bit arithmetic is exact; 64-bit
+// division is emulated in software on the GPU.)
 MOE_HD void tile_rows(int m, int nt, int mb, int& first, int& rows) {
-    const int nb32 = (m + kSegAlign - 1) / kSegAlign;
-    const int b0 = (int)((long)nb32 * mb / nt), b1 = (int)((long)nb32 * (mb + 1) / nt);
+    const uint32_t nb32 = (uint32_t)(m + kSegAlign - 1) / kSegAlign;
+    const int b0 = (int)(nb32 * (uint32_t)mb / (uint32_t)nt), b1 = (int)(nb32 * (uint32_t)(mb + 1) / (uint32_t)nt);
     first = b0 * kSegAlign;
     rows = (m < b1 * kSegAlign ? m : b1 * kSegAlign) - first;
 }
@@ -40,8 +43,8 @@ MOE_HD void tile_rows(int m, int nt, int mb, int& first, int& rows) {
 // groups of near-equal size; group j holds row tiles [glo, ghi) of the expert.
 MOE_HD int n_groups(int nt, int gmax) { return (nt + gmax - 1) / gmax; }
 MOE_HD void group_range(int nt, int ng, int j, int& glo, int& ghi) {
-    glo = (int)((long)nt * j / ng);
-    ghi = (int)((long)nt * (j + 1) / ng);
+    glo = (int)((uint32_t)nt * (uint32_t)j / (uint32_t)ng);
+    ghi = (int)((uint32_t)nt * (uint32_t)(j + 1) / (uint32_t)ng);
 }
 
 // Queue cut x (1..kXcds-1) of an op with `total` row tiles: the group
@@ -49,19 +52,33 @@ MOE_HD void group_range(int nt, int ng, int j, int& glo, int& ghi) {
 // group spans two queues; cuts are non-decreasing in x.  scan[e] = first row
 // tile of expert e (exclusive prefix of row_tiles over the experts).
 MOE_HD int queue_cut(int x, const int32_t* scan, int E, int total, int gmax) {
-    const int target = (int)((long)total * x / kXcds);
+    const int target = (int)((uint32_t)total * (uint32_t)x / kXcds);
     int best = 0, bestd = 0x7fffffff;
     for (int e = 0; e < E; ++e) {
         const int pos = scan[e], nt = (e + 1 < E ? scan[e + 1] : total) - pos;
         if (nt <= 0 || target < pos || target > pos + nt) continue;
         const int ng = n_groups(nt, gmax);
         for (int j = 0; j <= ng; ++j) {
-            const int b = pos + (int)((long)nt * j / ng);
+            const int b = pos + (int)((uint32_t)nt * (uint32_t)j / (uint32_t)ng);
             const int dd = b > target ? b - target : target - b;
             if (dd < bestd) { bestd = dd; best = b; }
         }
     }
     return best;
+}
+
+// The expert whose row tiles include row tile p (scan[e] = first row tile of
+// expert e, non-decreasing; p < total): the last e with scan[e] <= p among
+// experts that have row tiles.
+MOE_HD int expert_of_tile(const int32_t* scan, int E, int total, int p) {
+    int lo = 0, hi = E - 1;
+    while (lo < hi) {                    // last e with scan[e] <= p
+        const int mid = (lo + hi + 1) >> 1;
+        if (scan[mid] <= p) lo = mid;
+        else hi = mid - 1;
+    }
+    (void)total;          // an expert with no row tile shares its scan value with the next one, which wins
+    return lo;
 }
 
 // A row-tile table entry packs everything a claim needs into one 64-bit word:
@@ -79,6 +96,28 @@ MOE_HD void unpack_entry(uint64_t ent, int& e, int& mb, int& rows, int& row0) {
 }
 // Group entry of a row tile: first row tile of its group | group size << 16.
 MOE_HD uint32_t pack_group(int first, int size) { return (uint32_t)first | ((uint32_t)size << 16); }
+
+// Row tile p of an op (p < total = x_moe): its table and group entries, from
+// the experts' counts and segment offsets and scan[e] = first row tile of
+// expert e.  Returns false if p does not belong to any expert's tiles (an
+// inconsistent count).
+MOE_HD bool row_tile_entry(const int32_t* scan, const int32_t* counts, const int32_t* offsets, int E, int total,
+                           int mt, int gmax, int p, uint64_t& ent, uint32_t& grp) {
+    const int e = expert_of_tile(scan, E, total, p);
+    const int c = counts[e], nt = row_tiles(c, mt), pos = scan[e], mb = p - pos;
+    if (mb < 0 || mb >= nt) return false;
+    const int ng = n_groups(nt, gmax);
+    int glo = 0, ghi = nt;
+    for (int j = 0; j < ng; ++j) {                   // the near-equal group holding mb
+        group_range(nt, ng, j, glo, ghi);
+        if (mb < ghi) break;
+    }
+    int first, rows;
+    tile_rows(c, nt, mb, first, rows);
+    ent = pack_entry(e, mb, rows, offsets[e] + first);
+    grp = pack_group(pos + glo, ghi - glo);
+    return true;
+}
 
 // Tile t of a queue holding n_mt row tiles starting at m_lo: its stage and
 // the row tile p whose group holds it (a group of s row tiles starting at f

@@ -156,6 +156,14 @@ def moe_grouped_ffn_persistent_noalloc(ops: Sequence[OpDesc], cfg: SchedConfig, 
                                                  _stream(stream)), "moe_grouped_ffn_persistent_noalloc")
 
 
+def moe_grouped_ffn_plain(ops: Sequence[OpDesc], workspace: torch.Tensor, status_word: torch.Tensor,
+                          stream=None) -> None:
+    """The same tiles as plain grids per op (planning, GEMM-1, GEMM-2 launches): a baseline."""
+    lib = load_library()
+    check(lib.moe_grouped_ffn_plain(_op_array(ops), len(ops), _ptr(workspace), _ptr(status_word), _stream(stream)),
+          "moe_grouped_ffn_plain")
+
+
 def moe_combine(y_perm: torch.Tensor, assign_to_row: torch.Tensor, topk_w: torch.Tensor, T: int, top_k: int,
                 y: Optional[torch.Tensor] = None, out_dtype: torch.dtype = torch.bfloat16, stream=None):
     lib = load_library()
@@ -213,7 +221,7 @@ def status_string(status: int) -> str:
 
 __all__ = ["moe_topk_route", "moe_topk_route_batch", "moe_route_place_workspace_bytes", "moe_permute_workspace_bytes", "moe_permute", "moe_permute_batch",
            "moe_ffn_row_align", "moe_ffn_tile_shape", "moe_ffn_workspace_bytes", "moe_grouped_ffn_persistent",
-           "moe_grouped_ffn_persistent_noalloc", "moe_combine", "moe_combine_batch", "moe_pack_weights", "moe_x_moe", "moe_decode_quota", "status_string",
+           "moe_grouped_ffn_persistent_noalloc", "moe_grouped_ffn_plain", "moe_combine", "moe_combine_batch", "moe_pack_weights", "moe_x_moe", "moe_decode_quota", "status_string",
            "route_args", "permute_args", "combine_args", "OpDesc", "SchedConfig", "_lib"]
 
 

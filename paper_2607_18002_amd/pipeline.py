@@ -255,6 +255,10 @@ class MoEPipeline:
     def ffn(self, stream=None):
         K.moe_grouped_ffn_persistent(self.descs, self.cfg, self.ffn_ws, self.status, stream)
 
+    def ffn_plain(self, stream=None):
+        """The comparison baseline: the same tiles as plain grids, op after op."""
+        K.moe_grouped_ffn_plain(self.descs, self.ffn_ws, self.status, stream)
+
     def combine(self, stream=None, batched: bool = True):
         if self.fused_combine:                     # the persistent kernel wrote y
             return

@@ -19,9 +19,15 @@ Mechanisms, all on the same two ops (one layer's prefill and decode share the
   * sequential : prefill then decode on one stream (time-sharing)
 Reported per mechanism: decode op latency (its arrival, 10 us after the
 prefill work started, to its last tile committed), prefill op latency (start
-to done) and the makespan of both, from the kernels' device wall clock.
+to done) and the makespan of both, from the kernels' device wall clock, and
+each against the op alone.
 
-    python -m paper_2607_18002_amd.sharing [--prefill 8192] [--decode 128]
+Routing: Zipf-skewed logits over all 32 local experts (default), or, with
+--active N, the paper's microbenchmark condition: both ops activate the same N
+local experts (each token routes --local-slots of its k slots to them, round
+robin, the rest to non-local experts).
+
+    python -m paper_2607_18002_amd.sharing [--prefill 8192] [--decode 128] [--active 8]
 """
 from __future__ import annotations
 
@@ -33,9 +39,12 @@ import numpy as np
 TICK_US = 0.01          # 100 MHz device wall clock
 
 
-def _ops(T_p: int, T_d: int, H: int, I: int, E_g: int, E_l: int, k: int, seed: int, device):
+def _ops(T_p: int, T_d: int, H: int, I: int, E_g: int, E_l: int, k: int, seed: int, device, active: int = 0,
+         local_slots: int = 1):
     """One layer's prefill and decode ops on shared random bf16 weights, with
-    Zipf-skewed router logits (popularity rank r gets a bias of r^-1.1)."""
+    Zipf-skewed router logits (popularity rank r gets a bias of r^-1.1), or
+    with `active` > 0, logits that route every token's `local_slots` local
+    slots to the first `active` local experts."""
     import torch
 
     from ._lib import MOE_BF16, MOE_DECODE, MOE_PREFILL
@@ -51,7 +60,11 @@ def _ops(T_p: int, T_d: int, H: int, I: int, E_g: int, E_l: int, k: int, seed: i
     bias = (rank ** -1.1).to(device)
     specs = {}
     for name, T, ph in (("prefill", T_p, MOE_PREFILL), ("decode", T_d, MOE_DECODE)):
-        logits = torch.randn((T, E_g), generator=g, device=device) + bias[None, :]
+        if active > 0:
+            from .latency_model import routed_logits
+            logits = torch.from_numpy(routed_logits(T, active, local_slots, E_g, E_l, k)).to(device)
+        else:
+            logits = torch.randn((T, E_g), generator=g, device=device) + bias[None, :]
         x = torch.randn((T, H), generator=g, device=device).to(torch.bfloat16)
         specs[name] = dict(phase=ph, layer=0, logits=logits, x=x, weights=w, E_local=E_l, top_k=k, local_begin=0)
     return specs, OpSpec
@@ -73,7 +86,7 @@ ARRIVE = int(10.0 / TICK_US)     # decode arrives 10 us after the prefill work s
 
 def run(T_p: int = 8192, T_d: int = 128, H: int = 3072, I: int = 1536, E_g: int = 256, E_l: int = 32, k: int = 8,
         quotas=(32, 64, 128), x_star: int = 0, partition_cus=(32, 64, 128), reps: int = 5,
-        seed: int = 7) -> List[Dict]:
+        seed: int = 7, active: int = 0, local_slots: int = 1, q_max: int = 0, warmup: int = 20) -> List[Dict]:
     import torch
 
     from . import load_library
@@ -82,11 +95,19 @@ def run(T_p: int = 8192, T_d: int = 128, H: int = 3072, I: int = 1536, E_g: int 
     load_library()
     dev = torch.device("cuda:0")
     n_cu = torch.cuda.get_device_properties(dev).multi_processor_count
-    sp, OpSpec = _ops(T_p, T_d, H, I, E_g, E_l, k, seed, dev)
+    sp, OpSpec = _ops(T_p, T_d, H, I, E_g, E_l, k, seed, dev, active, local_slots)
     rows = []
 
     def med(vals):
         return float(np.median(vals))
+
+    # warm-up (clocks and caches settle before the first measured mechanism)
+    pw = MoEPipeline([OpSpec(**sp["prefill"]), OpSpec(**sp["decode"], release_after_ns=10_000)], fused_gather=True)
+    _prepare(pw)
+    for _ in range(warmup):
+        pw.ffn()
+    torch.cuda.synchronize()
+    del pw
 
     # alone
     for name in ("prefill", "decode"):
@@ -103,7 +124,7 @@ def run(T_p: int = 8192, T_d: int = 128, H: int = 3072, I: int = 1536, E_g: int 
     # APK: one launch, decode released 10 us after the start
     for q in quotas:
         specs = [OpSpec(**sp["prefill"]), OpSpec(**sp["decode"], release_after_ns=10_000)]
-        p = MoEPipeline(specs, decode_quota_wg=q, x_moe_expected=x_star, fused_gather=True)
+        p = MoEPipeline(specs, decode_quota_wg=q, decode_quota_max_wg=q_max, x_moe_expected=x_star, fused_gather=True)
         _prepare(p)
         d, pf, mk = [], [], []
         for _ in range(reps + 1):
@@ -158,14 +179,28 @@ def main(argv=None) -> int:
     ap.add_argument("--prefill", type=int, default=8192)
     ap.add_argument("--decode", type=int, default=128)
     ap.add_argument("--x-star", type=int, default=0, help="x*_moe of Eq. (4); <= 0 for the fixed quota")
+    ap.add_argument("--active", type=int, default=0, help="both ops activate this many local experts (0: Zipf)")
+    ap.add_argument("--local-slots", type=int, default=1, help="with --active: local slots per token")
+    ap.add_argument("--quotas", default="32,64,128")
+    ap.add_argument("--qmax", type=int, default=0, help="Q_max of Eq. (4) in workgroups (0: half of them)")
+    ap.add_argument("--partitions", default="32,64,128")
     args = ap.parse_args(argv)
-    rows = run(T_p=args.prefill, T_d=args.decode, x_star=args.x_star)
-    print(f"prefill {args.prefill} tokens + decode {args.decode} tokens, H 3072, I 1536, 32 of 256 experts, top-8, bf16")
-    print("| mechanism | decode op latency us | prefill op latency us | makespan us |")
-    print("|---|---|---|---|")
+    rows = run(T_p=args.prefill, T_d=args.decode, x_star=args.x_star, active=args.active,
+               local_slots=args.local_slots, quotas=[int(v) for v in args.quotas.split(",")], q_max=args.qmax,
+               partition_cus=[int(v) for v in args.partitions.split(",")])
+    route = (f"{args.active} active local experts, {args.local_slots} local slot(s) per token" if args.active
+             else "Zipf-skewed over 32 local experts")
+    print(f"prefill {args.prefill} tokens + decode {args.decode} tokens, H 3072, I 1536, 32 of 256 experts, top-8, "
+          f"bf16, {route}")
+    alone_d = next(r["decode_us"] for r in rows if r["mechanism"].startswith("decode alone"))
+    alone_p = next(r["prefill_us"] for r in rows if r["mechanism"].startswith("prefill alone"))
+    print("| mechanism | decode op latency us | vs decode alone | prefill op latency us | vs prefill alone | makespan us |")
+    print("|---|---|---|---|---|---|")
     f = lambda v: "-" if v is None else f"{v:.1f}"  # noqa: E731
+    g = lambda v, base: "-" if v is None else f"{v / base:.2f}x"  # noqa: E731
     for r in rows:
-        print(f"| {r['mechanism']} | {f(r['decode_us'])} | {f(r['prefill_us'])} | {f(r['makespan_us'])} |")
+        print(f"| {r['mechanism']} | {f(r['decode_us'])} | {g(r['decode_us'], alone_d)} | {f(r['prefill_us'])} | "
+              f"{g(r['prefill_us'], alone_p)} | {f(r['makespan_us'])} |")
     return 0
 
 

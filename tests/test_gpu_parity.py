@@ -720,3 +720,41 @@ def test_masked_placement_calls_share_a_workspace(dev, T_seq, E, E_l, k):
         valid = o.row_to_assign >= 0
         np.testing.assert_array_equal(got[valid], o.row_to_assign[valid])
         assert np.all(got[~valid] == -9)                     # rows past a region's count are not written
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_plain_grid_baseline_matches_persistent_bitwise(dev, dtype):
+    """The comparison baseline (the same tiles as plain per-op grids, no device
+    scheduler) computes h and y_perm bit for bit like the persistent kernel,
+    for a 2-layer mixed launch with the masked decode layout."""
+    from paper_2607_18002_amd.pipeline import MoEPipeline
+    base = 2 if dtype == "bf16" else 5
+    cfg = custom_config(base, cfg_id=760 + base, H=512, I=512, prefill_tokens=700, decode_tokens=90, E_global=64,
+                        E_local=12, top_k=6, zipf_s=(1.2, 0.7), n_layers=2)
+    specs = []
+    for layer in range(2):
+        s, _, _ = layer_specs(cfg, layer, dev)
+        specs += s
+    pipe = MoEPipeline(specs, fused_gather=True, masked_decode=True)
+    pipe.route()
+    pipe.permute()
+    outs = []
+    for plain in (False, True):
+        for b in pipe.bufs:
+            b.h.zero_()
+            b.y_perm.zero_()
+        if plain:
+            pipe.ffn_plain()
+        else:
+            pipe.ffn()
+        torch.cuda.synchronize()
+        assert pipe.statuses() == (0, 0)
+        outs.append([(b.h.view(torch.uint8).clone(), b.y_perm.view(torch.int16).clone()) for b in pipe.bufs])
+    for (h0, y0), (h1, y1), b in zip(outs[0], outs[1], pipe.bufs):
+        valid = (b.row_to_assign >= 0)
+        if b.slots:                                          # masked: rows past a region's count are not outputs
+            r = torch.arange(b.capacity, device=dev)
+            e = r // b.slots
+            valid = (r - e * b.slots) < b.counts.long()[e]
+        assert torch.equal(h0[valid], h1[valid])
+        assert torch.equal(y0[valid], y1[valid])
