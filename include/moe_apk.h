@@ -319,7 +319,12 @@ typedef struct moe_sched_config {
                                  weight slice serves all of them; 0 = 8, max 64     */
     const uint32_t* abort_word;   /* NULL, or host/peer-writable: non-zero stops the
                                      kernel at the next tile boundary (MOE_ERR_ABORTED) */
-    moe_trace_rec* trace;     /* NULL, or [trace_capacity] records                      */
+    moe_trace_rec* trace;     /* NULL, or [trace_capacity] records, split into one block
+                                 of trace_capacity / W records per workgroup (W = the
+                                 launch's workgroups): workgroup w writes its tiles in
+                                 order into block w and, if the block has room left,
+                                 ends them with a record whose op is -1; tiles past a
+                                 full block are not recorded.  trace_capacity >= W.  */
     int64_t trace_capacity;
     moe_op_stats* op_stats;   /* NULL, or [n_ops]                                       */
     int64_t spin_limit;       /* bounded waits, in polls; 0 = default (about 2 s)       */

@@ -102,7 +102,7 @@ struct KArgs {
     int64_t spin_limit;
     const uint32_t* abort_word;
     moe_trace_rec* trace;
-    int64_t trace_cap;
+    int64_t trace_per_wg;      // records per workgroup block (trace: n_wg blocks of this many)
     moe_op_stats* stats;
     int32_t* status;
     char* ws;
@@ -133,7 +133,7 @@ static_assert(sizeof(OpStatic) == 128, "one L2 line per op");
 
 struct Hdr {
     unsigned long long t0;
-    int32_t ops_done, quota, trace_count, stop;
+    int32_t ops_done, quota, n_wg, stop;     // n_wg: the launch's workgroups (the trace's block count)
 };
 
 // One tile queue per (op, XCD): the op's row tiles are cut into kXcds
@@ -560,7 +560,7 @@ __device__ __forceinline__ int phase_of(const KArgs& a, int o) { return a.op[o].
 // completion count, so the commit and the claim share one round trip.
 template <bool COMB>
 __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool have_prev, int64_t& idle,
-                         TabCache* tab, bool have_pre, Polls pre, int pre_t, const int32_t* n3s) {
+                         TabCache* tab, bool have_pre, Polls pre, int pre_t, const int32_t* n3s, int& n_traced) {
     const int lane = threadIdx.x;
     Hdr* hdr = hdr_of(a.ws);
     OpDyn* dyn = dyn_of(a.ws);
@@ -588,12 +588,14 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
         }
         __hip_atomic_fetch_add(&dyn[prev.op].left, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    // 3. trace the previous tile
+    // 3. trace the previous tile, into this workgroup's own block of records
+    //    (no shared counter, so tracing adds no round trip to a boundary)
     auto finish_prev = [&]() {
         if (have_prev && lane == 0) {
             if (a.trace) {
-                const int idx = add_relaxed_agent(&hdr->trace_count, 1);
-                if (idx < a.trace_cap) {
+                const int64_t idx = (int64_t)wg * a.trace_per_wg + n_traced;
+                if (n_traced < a.trace_per_wg) {
+                    ++n_traced;
                     moe_trace_rec r;
                     r.op = (int16_t)prev.op; r.stage = (int16_t)prev.stage; r.wg = (int16_t)wg;
                     r.xcc = (int16_t)xcc_id(); r.expert = prev.e; r.mblk = prev.mblk; r.nblk = (int16_t)prev.nb;
@@ -917,21 +919,31 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
         const unsigned long long now = wall_ticks();
         const unsigned long long prev = atomicCAS(&hdr_of(a.ws)->t0, 0ull, now);
         s_t0 = prev ? prev : now;
+        if (wg == 0) __hip_atomic_store(&hdr_of(a.ws)->n_wg, (int32_t)gridDim.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
     const uint64_t t0 = s_t0;
     int64_t idle = 0;
+    int n_traced = 0;                                         // lane 0: records written to this workgroup's block
     bool have_prev = false;
     bool have_pre = false;                                    // polls issued during the last tile (GEMM tiles only)
     Polls polls = {};                                         // wave 0: issued after the last tile's K loop
     int pre_t = 0;                                            // lane 0: a claim issued ahead, during the tile
     for (;;) {
-        if (tid < 64) boundary<COMB>(a, t0, wg, &cmd, have_prev, idle, &tab, have_pre, polls, pre_t, s_n3);
+        if (tid < 64) boundary<COMB>(a, t0, wg, &cmd, have_prev, idle, &tab, have_pre, polls, pre_t, s_n3, n_traced);
         __syncthreads();
         const int kind = cmd.kind;
         have_prev = false;
         have_pre = false;                                     // set again only by a GEMM tile's hook
-        if (kind == CMD_EXIT) break;
+        if (kind == CMD_EXIT) {
+            if (tid == 0 && a.trace && n_traced < a.trace_per_wg) {      // end of this workgroup's records
+                moe_trace_rec r = {};
+                r.op = -1;
+                r.wg = (int16_t)wg;
+                a.trace[(int64_t)wg * a.trace_per_wg + n_traced] = r;
+            }
+            break;
+        }
         if (kind == CMD_IDLE) {
             __builtin_amdgcn_s_sleep(8);
             __syncthreads();                                  // cmd is rewritten next iteration
@@ -1194,7 +1206,10 @@ moe_status_t launch_ffn(const moe_op_desc* ops, int32_t n_ops, const moe_sched_c
     a.spin_limit = cfg->spin_limit > 0 ? cfg->spin_limit : (int64_t)2000000;
     a.abort_word = cfg->abort_word;
     a.trace = cfg->trace;
-    a.trace_cap = cfg->trace ? cfg->trace_capacity : 0;
+    a.trace_per_wg = cfg->trace ? cfg->trace_capacity / n_wg : 0;
+    if (cfg->trace && a.trace_per_wg < 1)
+        return fail(MOE_ERR_INVALID_ARG, "trace_capacity=%lld holds no record per workgroup (%d workgroups)",
+                    (long long)cfg->trace_capacity, n_wg);
     a.stats = cfg->op_stats;
     a.status = status_word;
     a.ws = (char*)workspace;

@@ -26,6 +26,19 @@ STATS_DTYPE = np.dtype([("t_seen", "<u8"), ("t_ready", "<u8"), ("t_first", "<u8"
 assert TRACE_DTYPE.itemsize == C.sizeof(TraceRec) and STATS_DTYPE.itemsize == C.sizeof(OpStats)
 
 
+def split_trace(recs: np.ndarray, n_wg: int) -> np.ndarray:
+    """The records of a trace buffer's per-workgroup blocks, each block taken up
+    to its terminator (op = -1) or its end, in order of tile start."""
+    per = len(recs) // n_wg
+    out = []
+    for w in range(n_wg):
+        blk = recs[w * per:(w + 1) * per]
+        end = np.nonzero(blk["op"] < 0)[0]
+        out.append(blk[: end[0] if len(end) else per])
+    allr = np.concatenate(out) if out else recs[:0]
+    return allr[np.argsort(allr["t_start"], kind="stable")]
+
+
 def bf16_tensor(bits: np.ndarray, device) -> torch.Tensor:
     """bf16 bit patterns (uint16 numpy) -> device bf16 tensor (same bits)."""
     return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).to(device)
@@ -279,9 +292,13 @@ class MoEPipeline:
         return int(self.error_flag.item()), int(self.status.item())
 
     def trace_records(self) -> np.ndarray:
-        n = min(self.trace_capacity, int(self.ffn_ws[16:20].view(torch.int32).item()))
-        raw = self.trace[: n * TRACE_DTYPE.itemsize].cpu().numpy()
-        return raw.view(TRACE_DTYPE)
+        """The last launch's tile records: workgroup w wrote its tiles in order
+        into block w of trace_capacity // n_wg records, ended by a record with
+        op = -1 unless the block is full."""
+        n_wg = int(self.ffn_ws[16:20].view(torch.int32).item())
+        if self.trace_capacity <= 0 or n_wg <= 0:
+            return np.zeros(0, dtype=TRACE_DTYPE)
+        return split_trace(self.trace.cpu().numpy().view(TRACE_DTYPE), n_wg)
 
     def kernel_t0(self) -> int:
         """Device wall-clock tick at which the last persistent launch started."""

@@ -155,3 +155,24 @@ def test_route_place_workspace_bytes():
     assert ops.moe_route_place_workspace_bytes(1025, 8) == 256 + 257 * 8 * 8
     assert ops.moe_route_place_workspace_bytes(2049, 8) == 256 + 512 * 8 * 8     # covers T = 2048 in 4-token chunks
     assert ops.moe_route_place_workspace_bytes(16384, 8) == 256 + 1024 * 8 * 8
+
+
+def test_split_trace_blocks():
+    """Trace buffers hold one block per workgroup; a block ends at its first
+    op = -1 record or at its end, and the records come back in start order."""
+    from paper_2607_18002_amd.pipeline import TRACE_DTYPE, split_trace
+    recs = np.zeros(12, dtype=TRACE_DTYPE)
+    recs["op"] = -7                                           # stale contents past a terminator
+    # block 0 (records 0-3): two tiles then the terminator
+    recs["op"][0:2] = 0
+    recs["t_start"][0:2] = [30, 10]
+    recs["op"][2] = -1
+    # block 1 (records 4-7): full, no terminator
+    recs["op"][4:8] = 1
+    recs["t_start"][4:8] = [5, 15, 25, 35]
+    # block 2 (records 8-11): terminator first
+    recs["op"][8] = -1
+    got = split_trace(recs, 3)
+    assert got["t_start"].tolist() == [5, 10, 15, 25, 30, 35]
+    assert got["op"].tolist() == [1, 0, 1, 1, 0, 1]
+    assert len(split_trace(recs[:0], 3)) == 0
