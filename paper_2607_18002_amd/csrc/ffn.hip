@@ -90,6 +90,7 @@ struct OpArg {
     void* yc;
     int32_t cls, phase, layer, E, H, I, capacity, mt, n1, n2, max_mtiles, table_off, g1_off, grp_off, T, top_k;
     int32_t ct, ck, y_f32, n3;  // combine: tokens, slots per token, fp32 output, combine tiles
+    int32_t rel, qtab_off;      // rel: the op has a release word; qtab_off: per-queue copies of table entries
 };
 
 struct KArgs {
@@ -132,8 +133,9 @@ struct OpStatic {
 static_assert(sizeof(OpStatic) == 128, "one L2 line per op");
 
 struct Hdr {
-    unsigned long long t0;
+    unsigned long long t0;                   // first workgroup's entry (wall-clock ticks)
     int32_t ops_done, quota, n_wg, stop;     // n_wg: the launch's workgroups (the trace's block count)
+    unsigned long long t_init, t_exit;       // init kernel done; last workgroup's exit
 };
 
 // One tile queue per (op, XCD): the op's row tiles are cut into kXcds
@@ -202,6 +204,7 @@ __global__ __launch_bounds__(256) void apk_init_kernel(const InitArgs a) {
             dyn_of(a.ws)[o].left = INT32_MIN;
         }
         *a.status = MOE_OK;
+        hdr_of(a.ws)->t_init = wall_ticks();
     }
 }
 
@@ -445,6 +448,41 @@ __device__ __forceinline__ Polls mask_polls(const KArgs& a, Polls p) {
     return p;
 }
 
+// Wave 0: the own queue's range and its first kTabCache table and group
+// entries (the copies written at instantiation), loaded with one round trip;
+// issue() only starts the loads, so a claim issued after them shares their
+// round trip, and commit() puts them into the workgroup's LDS cache.
+struct TabFill {
+    uint64_t ent;
+    uint32_t grp;
+    int m_lo, n_mt;
+    bool on;
+};
+__device__ __forceinline__ TabFill tab_fill_issue(const KArgs& a, int o, int myx, const TabCache* tab) {
+    TabFill f = {};
+    f.on = tab->lo[o] < 0;                                     // not cached yet (uniform)
+    if (f.on) {
+        const OpArg& op = a.op[o];
+        const XQueue* qs = xq_of(a.ws, o, myx);
+        const int lane = threadIdx.x;
+        const char* qt = arr_of(a.ws) + op.qtab_off;
+        f.m_lo = ld_relaxed_agent(&qs->m_lo);
+        f.n_mt = ld_relaxed_agent(&qs->n_mt);
+        f.ent = ld_relaxed_agent((const uint64_t*)qt + myx * kTabCache + lane);
+        f.grp = ld_relaxed_agent((const uint32_t*)(qt + kXcds * kTabCache * 8) + myx * kTabCache + lane);
+    }
+    return f;
+}
+__device__ __forceinline__ void tab_fill_commit(TabCache* tab, int o, const TabFill& f) {
+    if (!f.on) return;
+    const int lane = threadIdx.x;
+    if (f.n_mt <= kTabCache && lane < f.n_mt) {
+        tab->ent[o][lane] = f.ent;
+        tab->grp[o][lane] = f.grp;
+    }
+    if (lane == 0) { tab->lo[o] = f.m_lo; tab->cnt[o] = f.n_mt; }
+}
+
 // Wave 0: turn claim t of op o's queue on XCD src into the command block
 // (table lookup, validation of the descriptor, GEMM-1 dependency of a GEMM-2
 // tile).  The own queue's range and entries are cached in LDS at the first
@@ -461,19 +499,9 @@ __device__ bool take_tile(const KArgs& a, int o, int src, int t, int myx, TabCac
     const uint32_t* grp = (const uint32_t*)(arr_of(a.ws) + op.grp_off);
     int m_lo, n_mt;
     if (src == myx) {
-        if (tab->lo[o] < 0) {                                 // first claim from this op's own queue
-            const XQueue* qs = xq_of(a.ws, o, myx);
-            m_lo = ld_relaxed_agent(&qs->m_lo);
-            n_mt = ld_relaxed_agent(&qs->n_mt);
-            if (n_mt <= kTabCache && lane < n_mt) {
-                tab->ent[o][lane] = ld_relaxed_agent(table + m_lo + lane);
-                tab->grp[o][lane] = ld_relaxed_agent(grp + m_lo + lane);
-            }
-            if (lane == 0) { tab->lo[o] = m_lo; tab->cnt[o] = n_mt; }
-        } else {
-            m_lo = tab->lo[o];
-            n_mt = tab->cnt[o];
-        }
+        tab_fill_commit(tab, o, tab_fill_issue(a, o, myx, tab));   // first claim from this op's own queue
+        m_lo = tab->lo[o];
+        n_mt = tab->cnt[o];
     } else {
         const XQueue* qs = xq_of(a.ws, o, src);
         m_lo = ld_relaxed_agent(&qs->m_lo);
@@ -745,8 +773,10 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
                 return;
             }
             if ((own_avail >> o) & 1) {                             // own queue
+                const TabFill f = tab_fill_issue(a, o, myx, tab);   // shares the claim's round trip
                 if (lane == 0) t = atomicAdd(&xq_of(a.ws, o, myx)->claim, 1);
                 t = __shfl(t, 0, 64);
+                tab_fill_commit(tab, o, f);
                 if (t < __shfl(own_size, o, 64)) src = myx;
             }
             // steal: the queue with most tiles left; a lost race tries again,
@@ -788,13 +818,12 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
     ++idle;
 }
 
-// Whole workgroup: build the row-tile table of an operation whose ready signal was seen.
-// Whole workgroup: the row-tile table and group entries of an op from its
-// counts and offsets (Eq. (3) row tiles of near-equal height, weight-sharing
-// groups), with scan[e] = the first row tile of expert e; *s_total = x_moe,
-// *s_bad = 1 if the offsets or counts do not fit the op's buffers.
-__device__ void build_row_tiles(const OpArg& op, uint64_t* table, uint32_t* grp, int gmax, int32_t* scan,
-                                int32_t* s_cnt, int32_t* s_off, int32_t* s_total, int32_t* s_bad) {
+// Whole workgroup, first half of building an op's row tiles: its counts and
+// offsets into LDS and scan[e] = the first row tile of expert e (Eq. (3) row
+// tiles per expert); *s_total = x_moe, *s_bad = 1 if the offsets or counts do
+// not fit the op's buffers.  Ends with the workgroup synchronised.
+__device__ void scan_row_tiles(const OpArg& op, int32_t* scan, int32_t* s_cnt, int32_t* s_off, int32_t* s_total,
+                               int32_t* s_bad) {
     // one round trip for the op's inputs: counts and offsets together, into LDS
     for (int e = threadIdx.x; e < op.E; e += 256) {
         const int c = op.counts[e], off = op.offsets[e];
@@ -828,9 +857,19 @@ __device__ void build_row_tiles(const OpArg& op, uint64_t* table, uint32_t* grp,
         const int nb32 = (c + kSegAlign - 1) / kSegAlign;        // 32-row blocks of the segment
         if (scan[e] + nt > op.max_mtiles || off < 0 || (long)off + (long)nb32 * kSegAlign > op.capacity) *s_bad = 1;
     }
-    // one thread per row tile: its expert, its row blocks (Eq. (3): ceil(m_e / M_t)
-    // row tiles of near-equal height) and its weight-sharing group
-    const int total = *s_total < op.max_mtiles ? *s_total : op.max_mtiles;
+    __syncthreads();
+}
+
+// Whole workgroup, second half: one thread per row tile stores its table
+// entry (expert, row blocks of near-equal height, first row) and its
+// weight-sharing group entry.  With queue cuts (cut[x] = first row tile of
+// queue x, cut[kXcds] = x_moe), a row tile among the first kTabCache of its
+// queue is also stored in that queue's block of copies, which a workgroup
+// loads together with its first claim from the queue.
+__device__ void store_row_tiles(const OpArg& op, uint64_t* table, uint32_t* grp, int gmax, const int32_t* scan,
+                                const int32_t* s_cnt, const int32_t* s_off, int total, const int32_t* cut,
+                                uint64_t* qent, uint32_t* qgrp) {
+    total = total < op.max_mtiles ? total : op.max_mtiles;
     for (int p = threadIdx.x; p < total; p += 256) {
         uint64_t ent;
         uint32_t g;
@@ -839,35 +878,49 @@ __device__ void build_row_tiles(const OpArg& op, uint64_t* table, uint32_t* grp,
         // ACTIVE reads them from the coherence point
         __hip_atomic_store(table + p, ent, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_store(grp + p, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (cut) {
+            int x = 0;
+            for (int y = 1; y < kXcds; ++y)
+                if (cut[y] <= p) x = y;                         // the last queue starting at or before p
+            const int slot = p - cut[x];
+            if (slot < kTabCache) {
+                __hip_atomic_store(qent + x * kTabCache + slot, ent, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(qgrp + x * kTabCache + slot, g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
     }
+}
+
+// Whole workgroup: the row-tile table and group entries of an op (the plain
+// grids' planning step).
+__device__ void build_row_tiles(const OpArg& op, uint64_t* table, uint32_t* grp, int gmax, int32_t* scan,
+                                int32_t* s_cnt, int32_t* s_off, int32_t* s_total, int32_t* s_bad) {
+    scan_row_tiles(op, scan, s_cnt, s_off, s_total, s_bad);
+    store_row_tiles(op, table, grp, gmax, scan, s_cnt, s_off, *s_total, nullptr, nullptr, nullptr);
 }
 
 __device__ void instantiate(const KArgs& a, int o, int32_t* scan, int32_t* s_cnt, int32_t* s_off) {
     const OpArg& op = a.op[o];
     OpDyn* d = dyn_of(a.ws) + o;
-    if (static_of(a.ws)[o].rel_word) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");  // system scope: peer-written inputs
+    if (op.rel) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");  // system scope: peer-written inputs
     const int gmax = a.gmax;
     __shared__ int32_t s_total, s_bad, s_cut[kXcds + 1];
-    build_row_tiles(op, (uint64_t*)(arr_of(a.ws) + op.table_off), (uint32_t*)(arr_of(a.ws) + op.grp_off), gmax, scan,
-                    s_cnt, s_off, &s_total, &s_bad);
-    // Each wave's entries have reached the coherence point before the barrier
-    // that precedes ACTIVE; no L2 write-back is needed (an agent-scope release
-    // would write back the XCD's whole L2, dirtied by the kernels before).
-    wait_own_stores();
+    scan_row_tiles(op, scan, s_cnt, s_off, &s_total, &s_bad);
     // Queue cuts: cut x (1..kXcds-1) is the group boundary nearest to x/kXcds
     // of the row tiles (ties: the lower one), so no group spans two queues;
     // cuts are non-decreasing in x.
-    if (threadIdx.x >= 1 && threadIdx.x < kXcds) s_cut[threadIdx.x] = sched::queue_cut(threadIdx.x, scan, op.E, s_total, gmax);
+    const int xm = s_total < op.max_mtiles ? s_total : op.max_mtiles;
+    if (threadIdx.x < kXcds + 1)
+        s_cut[threadIdx.x] = threadIdx.x == 0 ? 0 : threadIdx.x == kXcds ? xm : sched::queue_cut(threadIdx.x, scan, op.E, xm, gmax);
     __syncthreads();
-    if (threadIdx.x == 0) {
+    const bool bad = s_bad != 0;
+    if (!bad) {
+        char* arr = arr_of(a.ws);
+        store_row_tiles(op, (uint64_t*)(arr + op.table_off), (uint32_t*)(arr + op.grp_off), gmax, scan, s_cnt, s_off,
+                        xm, s_cut, (uint64_t*)(arr + op.qtab_off), (uint32_t*)(arr + op.qtab_off + kXcds * kTabCache * 8));
+    }
+    if (threadIdx.x == 0 && !bad) {
         Hdr* hdr = hdr_of(a.ws);
-        if (s_bad) {
-            set_status(a.status, MOE_ERR_CAPACITY);
-            st_release_agent(&hdr->stop, 1);
-            return;
-        }
-        const int xm = s_total;
-        const unsigned long long t = wall_ticks();
         int qd = 0;
         if (op.phase == MOE_DECODE) {
             qd = decode_quota(a.q, xm, a.x_star, a.q_max, a.c);
@@ -879,19 +932,32 @@ __device__ void instantiate(const KArgs& a, int o, int32_t* scan, int32_t* s_cnt
         __hip_atomic_store(&d->left, -(xm * (op.n1 + op.n2) + op.n3), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         for (int x = 0; x < kXcds; ++x) {                      // contiguous row-tile ranges, cut between groups
             XQueue* qx = xq_of(a.ws, o, x);
-            const int lo = x == 0 ? 0 : s_cut[x], hi = x + 1 == kXcds ? xm : s_cut[x + 1];
+            const int lo = s_cut[x], hi = s_cut[x + 1];
             __hip_atomic_store(&qx->m_lo, lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_store(&qx->n_mt, hi - lo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             __hip_atomic_store(&qx->size, (hi - lo) * (op.n1 + op.n2), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         __hip_atomic_store(&d->quota, qd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    // Every wave's table entries and wave 0's queue words have reached the
+    // coherence point before the barrier that precedes ACTIVE; no L2
+    // write-back is needed (an agent-scope release would write back the XCD's
+    // whole L2, dirtied by the kernels before).
+    wait_own_stores();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        if (bad) {
+            set_status(a.status, MOE_ERR_CAPACITY);
+            st_release_agent(&hdr_of(a.ws)->stop, 1);
+            return;
+        }
+        const unsigned long long t = wall_ticks();
         __hip_atomic_store(&d->t_ready, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (xm == 0) {                                   // nothing routed here: done at once
             __hip_atomic_store(&d->t_first, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             if (op.n3 > 0) st_release_agent(&d->state, (int32_t)ST_COMBINING);   // its combine writes zeros
             else finish_op(a, o, 0);
         } else {
-            wait_own_stores();                                  // queue ranges and counters, before ACTIVE
             __hip_atomic_store(&d->state, (int32_t)ST_ACTIVE, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
     }
@@ -936,6 +1002,9 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
         have_prev = false;
         have_pre = false;                                     // set again only by a GEMM tile's hook
         if (kind == CMD_EXIT) {
+            if (tid == 0)
+                __hip_atomic_fetch_max(&hdr_of(a.ws)->t_exit, (unsigned long long)wall_ticks(), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
             if (tid == 0 && a.trace && n_traced < a.trace_per_wg) {      // end of this workgroup's records
                 moe_trace_rec r = {};
                 r.op = -1;
@@ -1004,18 +1073,22 @@ int class_of(int phase, int dtype) {
 
 // Per op: a row-tile table (8 bytes per row tile), GEMM-1 counters and group
 // entries (4 bytes per row tile each), each padded to 256 bytes so no L2 line
-// is shared between ops.
-size_t op_array_bytes(int capacity, int mt, size_t* table_bytes) {
+// is shared between ops, then per queue the copies of its first kTabCache
+// table and group entries.
+constexpr size_t kQtabBytes = (size_t)kXcds * kTabCache * (8 + 4);
+static_assert(kQtabBytes % 256 == 0, "whole L2 lines");
+size_t op_array_bytes(int capacity, int mt, size_t* table_bytes, size_t* group_bytes) {
     const size_t mm = (size_t)((capacity + mt - 1) / mt) + 1;
     const size_t tb = (mm * 8 + 255) & ~(size_t)255;
     const size_t gb = (mm * 4 + 255) & ~(size_t)255;
     if (table_bytes) *table_bytes = tb;
-    return tb + 2 * gb;
+    if (group_bytes) *group_bytes = gb;
+    return tb + 2 * gb + kQtabBytes;
 }
 
 size_t ws_bytes_for(const moe_op_desc* ops, int n_ops) {
     size_t bytes = kArraysOff;
-    for (int o = 0; o < n_ops; ++o) bytes += op_array_bytes(ops[o].capacity, kSegAlign, nullptr);
+    for (int o = 0; o < n_ops; ++o) bytes += op_array_bytes(ops[o].capacity, kSegAlign, nullptr, nullptr);
     return (bytes + 255) & ~(size_t)255;
 }
 
@@ -1138,11 +1211,13 @@ moe_status_t fill_ops(const moe_op_desc* ops, int32_t n_ops, int wc_khz, KArgs& 
         p.n1 = d.I / (ci.bn / 2);
         p.n2 = d.H / ci.bn;
         p.max_mtiles = (d.capacity + kSegAlign - 1) / kSegAlign + 1;   // row tiles never outnumber 32-row blocks
-        size_t tb = 0;
-        const size_t ob = op_array_bytes(d.capacity, kSegAlign, &tb);
+        size_t tb = 0, gb = 0;
+        const size_t ob = op_array_bytes(d.capacity, kSegAlign, &tb, &gb);
         p.table_off = (int32_t)off;
         p.g1_off = (int32_t)(off + tb);
-        p.grp_off = (int32_t)(off + tb + (ob - tb) / 2);
+        p.grp_off = (int32_t)(off + tb + gb);
+        p.qtab_off = (int32_t)(off + tb + 2 * gb);
+        p.rel = d.release_word != nullptr;
         off += ob;
         ia.rel_words[o] = d.release_word;
         ia.rel_after[o] = d.release_after_ns < 0 ? -1 : d.release_after_ns * (int64_t)wc_khz / 1000000;

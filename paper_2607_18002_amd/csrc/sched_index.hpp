@@ -47,26 +47,6 @@ MOE_HD void group_range(int nt, int ng, int j, int& glo, int& ghi) {
     ghi = (int)((uint32_t)nt * (uint32_t)(j + 1) / (uint32_t)ng);
 }
 
-// Queue cut x (1..kXcds-1) of an op with `total` row tiles: the group
-// boundary nearest to x/kXcds of the row tiles (ties: the lower one), so no
-// group spans two queues; cuts are non-decreasing in x.  scan[e] = first row
-// tile of expert e (exclusive prefix of row_tiles over the experts).
-MOE_HD int queue_cut(int x, const int32_t* scan, int E, int total, int gmax) {
-    const int target = (int)((uint32_t)total * (uint32_t)x / kXcds);
-    int best = 0, bestd = 0x7fffffff;
-    for (int e = 0; e < E; ++e) {
-        const int pos = scan[e], nt = (e + 1 < E ? scan[e + 1] : total) - pos;
-        if (nt <= 0 || target < pos || target > pos + nt) continue;
-        const int ng = n_groups(nt, gmax);
-        for (int j = 0; j <= ng; ++j) {
-            const int b = pos + (int)((uint32_t)nt * (uint32_t)j / (uint32_t)ng);
-            const int dd = b > target ? b - target : target - b;
-            if (dd < bestd) { bestd = dd; best = b; }
-        }
-    }
-    return best;
-}
-
 // The expert whose row tiles include row tile p (scan[e] = first row tile of
 // expert e, non-decreasing; p < total): the last e with scan[e] <= p among
 // experts that have row tiles.
@@ -79,6 +59,27 @@ MOE_HD int expert_of_tile(const int32_t* scan, int E, int total, int p) {
     }
     (void)total;          // an expert with no row tile shares its scan value with the next one, which wins
     return lo;
+}
+
+// Queue cut x (1..kXcds-1) of an op with `total` row tiles: the group
+// boundary nearest to target = x/kXcds of the row tiles (ties: the lower
+// one), so no group spans two queues; cuts are non-decreasing in x.
+// scan[e] = first row tile of expert e (exclusive prefix of row_tiles over
+// the experts); 0 when no expert has a row tile.  The target lies in the row
+// tiles [pos, pos + nt) of one expert, whose group boundaries
+// b_j = pos + floor(nt * j / ng) grow with j; with j0 = floor((target - pos) *
+// ng / nt), b_j0 <= target <= b_(j0+1), so the nearest boundary is one of the
+// two (a boundary of another expert lies at or beyond pos or pos + nt).
+MOE_HD int queue_cut(int x, const int32_t* scan, int E, int total, int gmax) {
+    if (total <= 0) return 0;
+    const int target = (int)((uint32_t)total * (uint32_t)x / kXcds);     // < total
+    const int e = expert_of_tile(scan, E, total, target);
+    const int pos = scan[e], nt = (e + 1 < E ? scan[e + 1] : total) - pos;
+    const int ng = n_groups(nt, gmax);
+    const uint32_t j0 = (uint32_t)(target - pos) * (uint32_t)ng / (uint32_t)nt;   // < ng
+    const int b0 = pos + (int)((uint32_t)nt * j0 / (uint32_t)ng);
+    const int b1 = pos + (int)((uint32_t)nt * (j0 + 1) / (uint32_t)ng);
+    return target - b0 <= b1 - target ? b0 : b1;
 }
 
 // A row-tile table entry packs everything a claim needs into one 64-bit word:

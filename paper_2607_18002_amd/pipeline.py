@@ -304,5 +304,11 @@ class MoEPipeline:
         """Device wall-clock tick at which the last persistent launch started."""
         return int(self.ffn_ws[:8].view(torch.int64).item())
 
+    def launch_ticks(self):
+        """(init kernel done, first workgroup entry, last workgroup exit) of the
+        last launch, in device wall-clock ticks."""
+        h = self.ffn_ws[:40].view(torch.int64).cpu().numpy()
+        return int(h[3]), int(h[0]), int(h[4])
+
     def op_stats(self) -> np.ndarray:
         return self.stats.cpu().numpy().view(STATS_DTYPE)

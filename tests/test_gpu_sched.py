@@ -317,3 +317,32 @@ def test_fused_combine_tiles_follow_gemm_and_precede_dependants(dev):
         dep = specs[o].depends_on_op
         if dep >= 0:
             assert m["t_claim"].min() >= int(st["t_done"][dep])
+
+
+# Queue words of the scheduler workspace: a 256-byte header, 16 op states and
+# 16 op statics of 128 bytes, then one 128-byte queue per (op, XCD) holding
+# claim, size, first row tile and row-tile count.
+_XQ_OFF = 256 + 16 * 128 + 16 * 128
+
+
+@pytest.mark.parametrize("zipf", [0.6, 1.1, 1.6])
+def test_queue_ranges_match_host_layout(dev, zipf):
+    """The device's per-XCD queue ranges (cut between weight-sharing groups,
+    nearest to each eighth of the row tiles) equal the host build of the same
+    index functions, for both phases of a mixed launch."""
+    from paper_2607_18002_amd import ops
+    cfg = custom_config(2, cfg_id=402, H=512, I=512, prefill_tokens=3000, decode_tokens=300, E_global=64,
+                        E_local=32, top_k=8, zipf_s=(zipf,))
+    specs, lay, _ = layer_specs(cfg, 0, dev)
+    pipe = _pipe(dev, specs)
+    assert pipe.statuses() == (0, 0)
+    ws = pipe.ffn_ws.cpu().numpy()
+    for i, b in enumerate(pipe.bufs):
+        bm, bn, _ = ops.moe_ffn_tile_shape(b.spec.phase, b.spec.weights.dtype)
+        n1, n2 = b.spec.weights.I // (bn // 2), b.spec.weights.H // bn
+        counts, offsets = b.counts.cpu().numpy(), b.offsets.cpu().numpy()
+        _, _, qu, _ = ops.moe_sched_layout(counts, offsets[:-1], bm, 8, n1, n2)
+        dq = ws[_XQ_OFF + i * 8 * 128: _XQ_OFF + (i + 1) * 8 * 128].view(np.int32).reshape(8, 32)
+        np.testing.assert_array_equal(dq[:, 2], qu[:, 0])
+        np.testing.assert_array_equal(dq[:, 3], qu[:, 1])
+        np.testing.assert_array_equal(dq[:, 1], qu[:, 1] * (n1 + n2))

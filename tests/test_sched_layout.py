@@ -61,6 +61,8 @@ def _check(counts, offsets, M_t, gmax, n1, n2):
     gsize = int(gr[:, 1].max()) if x else 0
     for q in range(8):
         assert abs(int(qu[q, 0]) - x * q // 8) <= gsize
+        # exactly the group boundary nearest to q/8 of the row tiles, ties to the lower one
+        assert int(qu[q, 0]) == min(sorted(starts), key=lambda b: (abs(b - x * q // 8), b))
     # tiles: every (stage, row tile, column block) exactly once, inside its
     # queue's range, GEMM-1 tiles before GEMM-2 tiles, and each group run column
     # block by column block with its row tiles back to back
