@@ -20,9 +20,12 @@ that receives a row, once per launch -- a layer's prefill and decode ops share
 them -- plus the activation rows in and y_perm rows out; flops 6*H*I per row),
 its mean duration over the timed steps from HIP events on its stream; traffic
 = HBM bytes per launch from the committed rocprofv3 counter record when it was
-taken on the current kernel sources, else null.  decode_tile_latency comes
-from one extra traced launch, and from a launch of the decode ops alone (same
-inputs and release chain) for the latency without prefill load.
+taken on the current kernel sources, else null.  The timed launches carry the
+per-tile trace (no round trip per tile); decode_tile_latency and the clock
+the GEMM tiles ran at (shader clock counter over wall clock, reported with the
+MFMA fraction at that clock) come from the last timed launch, and a launch
+of the decode ops alone (same inputs and release chain) gives the latency
+without prefill load.
 cpu_baseline = the float64 CPU oracle over the whole workload, on this host's
 cores; its outputs are then compared with the GPU's outputs of the last timed
 step (parity: per-token normwise error and the whole-tensor figure).
@@ -46,6 +49,7 @@ DEFAULTS = dict(quota=64, decode_layout="masked", prefill_layout="contiguous", f
 
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0}
+NOMINAL_CLOCK_GHZ = 2.4          # peak engine clock the dense MFMA peaks are quoted at
 TICK_NS = 10.0
 
 
@@ -114,6 +118,16 @@ def pipeline_kwargs(quota=DEFAULTS["quota"], decode_layout=DEFAULTS["decode_layo
     return dict(decode_quota_wg=quota, fused_gather=fused, fused_combine=fused_combine,
                 masked_decode=decode_layout == "masked" and fused, masked_prefill=prefill_layout == "masked" and fused,
                 group_row_tiles=group_row_tiles)
+
+
+def tile_clock(tr):
+    """Shader clock the GEMM tiles of a traced launch ran at (GHz, p10/p50/p90):
+    shader clock counter over wall-clock ticks (100 MHz) per tile."""
+    tr = tr[(tr["stage"] < 3) & (tr["t_end"] > tr["t_start"])]
+    if len(tr) == 0:
+        return None
+    f = (tr["c_end"] - tr["c_start"]).astype(np.float64) / ((tr["t_end"] - tr["t_start"]).astype(np.float64) * 10.0)
+    return [round(float(np.percentile(f, q)), 3) for q in (10, 50, 90)]
 
 
 def algorithmic_work(pipe, cfg):
@@ -300,7 +314,10 @@ def main():
     t_gen = time.perf_counter() - t_gen
     pkw = pipeline_kwargs(args.quota, args.decode_layout, args.prefill_layout, args.fused_combine,
                           args.group_row_tiles, args.gather)
-    pipe = MoEPipeline(specs, **pkw)
+    # the per-tile trace costs no round trip (each workgroup writes its own
+    # block), so the timed launches carry it: the last one gives the decode
+    # latency and clock figures in the timed loop's own steady state
+    pipe = MoEPipeline(specs, trace_capacity=1 << 18, **pkw)
     stream = torch.cuda.current_stream()
 
     for _ in range(args.warmup):
@@ -327,10 +344,7 @@ def main():
     ms_step = wall * 1000.0 / args.steps
 
     flops, abytes, rows, abytes_per_op = algorithmic_work(pipe, cfg)
-    # one more launch with the per-tile trace for the decode latency figures
-    traced = MoEPipeline(specs, trace_capacity=1 << 18, **pkw)
-    traced.run()
-    torch.cuda.synchronize()
+    traced = pipe                                      # its last timed launch
     if args.dump_trace:
         np.save(args.dump_trace, traced.trace_records())
         np.save(args.dump_trace.replace(".npy", "_stats.npy"), traced.op_stats())
@@ -338,7 +352,7 @@ def main():
     if err or status:
         raise SystemExit(f"device status of the traced launch: permute={err} ffn={status}")
     lat = decode_latency(traced, specs)
-    del traced
+    clock = tile_clock(traced.trace_records())
     # the decode ops alone (same inputs, same release chain): the latency without prefill load
     excl = None
     dec_specs = phase_subset(specs, 1)
@@ -393,6 +407,10 @@ def main():
     roof["achieved_tflops"] = round(flops / (ffn_ms * 1e-3) / 1e12, 2)
     roof["frac_mfma"] = round(flops / (ffn_ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS[dtype], 4)
     roof["frac_hbm"] = round(abytes / (ffn_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+    if clock is not None:
+        # the MFMA peak scales with the shader clock (2.5 PFLOP/s bf16 dense is quoted at 2.4 GHz)
+        roof["tile_clock_ghz_p10_p50_p90"] = clock
+        roof["frac_mfma_at_tile_clock"] = round(roof["frac_mfma"] * NOMINAL_CLOCK_GHZ / clock[1], 4)
 
     if not args.no_peaks:
         from paper_2607_18002_amd import peaks

@@ -239,6 +239,9 @@ typedef struct moe_op_desc {
     int64_t release_after_ns;     /* < 0: no time condition; else device wall clock >=
                                      kernel start + release_after_ns                     */
     int32_t depends_on_op;        /* -1, or an EARLIER op index that must be done...     */
+                                  /* (an order of start times: an op's inputs are ready
+                                     when the launch starts or when its release word is
+                                     set, never outputs of another op of the launch)    */
     moe_layout_t weight_layout;   /* layout of w_gate_up / w_down: MOE_LAYOUT_PACKED      */
     int64_t gap_ns;               /* ...for at least gap_ns                              */
     uint32_t* done_word;          /* NULL, or set to 1 (system-scope release) when the
@@ -274,7 +277,9 @@ typedef struct moe_op_desc {
  * A tile's life: the scheduling step that picked it began at t_boundary (it
  * first committed the workgroup's previous tile), its polls of the scheduler
  * words had returned at t_polled, the tile was claimed at t_claim, its
- * dependencies were met at t_start, and its outputs were committed at t_end. */
+ * dependencies were met at t_start, and its outputs were committed at t_end.
+ * c_start / c_end: the shader clock counter (s_memtime) at t_start / t_end, so
+ * (c_end - c_start) / (t_end - t_start) is the clock the tile ran at. */
 typedef struct moe_trace_rec {
     int16_t op, stage;        /* stage 1 = GEMM-1 (+activation), 2 = GEMM-2, 3 = combine */
     int16_t wg, xcc;          /* workgroup index and the XCD it ran on                  */
@@ -288,6 +293,7 @@ typedef struct moe_trace_rec {
     int16_t quota_seen;
     uint8_t phases_seen, how;
     uint64_t t_boundary, t_polled, t_claim, t_start, t_end;
+    uint64_t c_start, c_end;
 } moe_trace_rec;
 
 /* Per-op statistics written by the persistent kernel (times in wall-clock ticks). */

@@ -61,7 +61,7 @@ class TraceRec(C.Structure):
         ("expert", _i32), ("mblk", _i32), ("nblk", C.c_int16), ("rows", C.c_int16),
         ("quota_seen", C.c_int16), ("phases_seen", C.c_uint8), ("how", C.c_uint8),
         ("t_boundary", C.c_uint64), ("t_polled", C.c_uint64), ("t_claim", C.c_uint64),
-        ("t_start", C.c_uint64), ("t_end", C.c_uint64),
+        ("t_start", C.c_uint64), ("t_end", C.c_uint64), ("c_start", C.c_uint64), ("c_end", C.c_uint64),
     ]
 
 

@@ -379,20 +379,25 @@ struct Cmd {
     int32_t kind, op, stage, e, row0, rows32, nb, mtile, mblk, rows, t;
     int32_t pre_next;          // op whose next tile wave 0 claims ahead during this tile, or -1
     int32_t q_seen, phases, how;   // the decision's inputs and path (recorded in the trace)
-    unsigned long long t_boundary, t_polled, t_claim, t_start;
+    unsigned long long t_boundary, t_polled, t_claim, t_start, c_start;
 };
 enum : int32_t { HOW_PREFERRED = 0, HOW_OTHER = 1, HOW_AHEAD = 2, HOW_COMBINE = 3 };
 
-// Lane 0: an op's last tile has committed.  The acquire takes in every other
-// workgroup's released writes of this op before the done word publishes them.
+// Lane 0: an op's last tile has committed.  Its outputs were stored
+// device-coherent before each tile's commit, and the in-kernel readers of
+// DONE (the exit test, a dependent op's start) read no data of the op, so
+// DONE itself is a plain store.  With a done word, the acquire takes in every
+// other workgroup's writes of this op before the word's system-scope release
+// publishes them.
 __device__ void finish_op(const KArgs& a, int o, int total) {
     Hdr* hdr = hdr_of(a.ws);
     OpDyn* d = dyn_of(a.ws) + o;
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    uint32_t* dw = a.op[o].done_word;
+    if (dw) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     const unsigned long long t = wall_ticks();
     __hip_atomic_store(&d->t_done, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    st_release_agent(&d->state, (int32_t)ST_DONE);
-    if (a.op[o].done_word) st_release_system(a.op[o].done_word, 1u);
+    __hip_atomic_store(&d->state, (int32_t)ST_DONE, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (dw) st_release_system(dw, 1u);
     if (a.stats) {
         moe_op_stats s;
         s.t_ready = ld_relaxed_agent(&d->t_ready);
@@ -554,6 +559,7 @@ __device__ bool take_tile(const KArgs& a, int o, int src, int t, int myx, TabCac
             }
         }
         cmd->t_start = wall_ticks();
+        cmd->c_start = __builtin_amdgcn_s_memtime();
         more = src == myx && t + 1 < n_mt * (op.n1 + op.n2);
     }
     return more;
@@ -569,6 +575,7 @@ __device__ void take_combine(int o, int t, Cmd* cmd, unsigned long long t_bounda
         cmd->t_polled = now;
         cmd->t_claim = wall_ticks();
         cmd->t_start = cmd->t_claim;
+        cmd->c_start = __builtin_amdgcn_s_memtime();
     }
 }
 
@@ -607,9 +614,10 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
     //    boundary never waits for their round trip; whether the op is complete
     //    is read from the polled counts (step 2b), by whichever workgroup
     //    first sees them full.
-    unsigned long long t_end = 0;
+    unsigned long long t_end = 0, c_end = 0;
     if (have_prev && lane == 0) {
         t_end = wall_ticks();
+        c_end = __builtin_amdgcn_s_memtime();
         if (prev.stage == 1) {
             int32_t* g1 = (int32_t*)(arr_of(a.ws) + a.op[prev.op].g1_off);
             __hip_atomic_fetch_add(g1 + prev.mtile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -631,6 +639,7 @@ __device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool hav
                     r.phases_seen = (uint8_t)prev.phases; r.how = (uint8_t)prev.how;
                     r.t_boundary = prev.t_boundary; r.t_polled = prev.t_polled;
                     r.t_claim = prev.t_claim; r.t_start = prev.t_start; r.t_end = t_end;
+                    r.c_start = prev.c_start; r.c_end = c_end;
                     a.trace[idx] = r;
                 }
             }

@@ -20,7 +20,8 @@ from ._lib import (MOE_BF16, MOE_DECODE, MOE_F32, MOE_FP8_E4M3, MOE_LAYOUT_PACKE
 TRACE_DTYPE = np.dtype([("op", "<i2"), ("stage", "<i2"), ("wg", "<i2"), ("xcc", "<i2"), ("expert", "<i4"),
                         ("mblk", "<i4"), ("nblk", "<i2"), ("rows", "<i2"), ("quota_seen", "<i2"),
                         ("phases_seen", "u1"), ("how", "u1"), ("t_boundary", "<u8"),
-                        ("t_polled", "<u8"), ("t_claim", "<u8"), ("t_start", "<u8"), ("t_end", "<u8")])
+                        ("t_polled", "<u8"), ("t_claim", "<u8"), ("t_start", "<u8"), ("t_end", "<u8"),
+                        ("c_start", "<u8"), ("c_end", "<u8")])
 STATS_DTYPE = np.dtype([("t_seen", "<u8"), ("t_ready", "<u8"), ("t_first", "<u8"), ("t_done", "<u8"), ("x_moe", "<i4"),
                         ("n_tiles", "<i4"), ("quota", "<i4"), ("reserved", "<i4")])
 assert TRACE_DTYPE.itemsize == C.sizeof(TraceRec) and STATS_DTYPE.itemsize == C.sizeof(OpStats)

@@ -42,7 +42,7 @@ def test_binding_layouts_match_library():
     lib = _lib.load_library()
     assert lib.moe_abi_sizeof(0) == C.sizeof(_lib.OpDesc)
     assert lib.moe_abi_sizeof(1) == C.sizeof(_lib.SchedConfig)
-    assert lib.moe_abi_sizeof(2) == C.sizeof(_lib.TraceRec) == 64
+    assert lib.moe_abi_sizeof(2) == C.sizeof(_lib.TraceRec) == 80
     assert lib.moe_abi_sizeof(3) == C.sizeof(_lib.OpStats) == 48
     assert lib.moe_abi_sizeof(4) == C.sizeof(_lib.RouteArgs)
     assert lib.moe_abi_sizeof(5) == C.sizeof(_lib.PermuteArgs)
