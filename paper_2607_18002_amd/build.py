@@ -10,6 +10,7 @@ from __future__ import annotations
 import argparse
 import concurrent.futures as cf
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -41,10 +42,33 @@ FLAGS = [
 ]
 
 
+# Per-lane scratch the persistent kernels may use (register spills).  A larger
+# figure means the compiler copied the kernel arguments to scratch (an index
+# into them that differs per lane, or their address passed to a function it
+# did not inline), which slows every tile; the build refuses it.
+SCRATCH_LIMIT = {"apk_kernel": 512, "plain_gemm_kernel": 512}
+
+
+def _scratch_check(src: str, lines) -> None:
+    fn = None
+    for ln in lines:
+        m = re.search(r"Function Name: (\S+)", ln)
+        if m:
+            fn = m.group(1)
+            continue
+        m = re.search(r"ScratchSize \[bytes/lane\]: (\d+)", ln)
+        if m and fn:
+            for key, limit in SCRATCH_LIMIT.items():
+                if key in fn and int(m.group(1)) > limit:
+                    raise RuntimeError(f"{src}: {fn} uses {m.group(1)} bytes of scratch per lane (limit {limit}): "
+                                       "its kernel arguments were copied to scratch")
+
+
 def _compile(src: str, verbose: bool, build_dir: str = BUILD, defines=()) -> str:
     obj = os.path.join(build_dir, os.path.splitext(src)[0] + ".o")
     cmd = [HIPCC, *FLAGS, *[f"-D{d}" for d in defines], "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
-    if verbose:
+    check = src == "ffn.hip"
+    if verbose or check:
         cmd.insert(1, "-Rpass-analysis=kernel-resource-usage")
     r = subprocess.run(cmd, capture_output=True, text=True)
     out = (r.stdout + r.stderr).strip()
@@ -52,6 +76,9 @@ def _compile(src: str, verbose: bool, build_dir: str = BUILD, defines=()) -> str
     lines = [ln for ln in out.splitlines() if "packed-fp32-ops" not in ln and "not a recognized feature" not in ln]
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {src}\n" + "\n".join(lines))
+    if check:
+        _scratch_check(src, lines)
+    lines = [ln for ln in lines if verbose or "kernel-resource-usage" not in ln]
     if verbose and lines:
         print("\n".join(lines))
     return obj

@@ -291,7 +291,7 @@ __device__ __forceinline__ void st_dev16(void* p, uint4 v) {
     __hip_atomic_store(q + 1, (uint64_t)v.z | ((uint64_t)v.w << 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-__device__ void run_combine(const OpArg& op, int t, char* lds, int32_t* status) {
+__device__ __forceinline__ void run_combine(const OpArg& op, int t, char* lds, int32_t* status) {
     const int tid = threadIdx.x;
     const int k = op.ck;
     const int tok0 = t * kCombTokens;
@@ -389,7 +389,7 @@ enum : int32_t { HOW_PREFERRED = 0, HOW_OTHER = 1, HOW_AHEAD = 2, HOW_COMBINE = 
 // DONE itself is a plain store.  With a done word, the acquire takes in every
 // other workgroup's writes of this op before the word's system-scope release
 // publishes them.
-__device__ void finish_op(const KArgs& a, int o, int total) {
+__device__ __forceinline__ void finish_op(const KArgs& a, int o, int total) {
     Hdr* hdr = hdr_of(a.ws);
     OpDyn* d = dyn_of(a.ws) + o;
     uint32_t* dw = a.op[o].done_word;
@@ -493,7 +493,7 @@ __device__ __forceinline__ void tab_fill_commit(TabCache* tab, int o, const TabF
 // tile).  The own queue's range and entries are cached in LDS at the first
 // claim from it.  Returns, to lane 0, whether the claimed tile was not the own
 // queue's last (a next claim from it may succeed).
-__device__ bool take_tile(const KArgs& a, int o, int src, int t, int myx, TabCache* tab, Cmd* cmd,
+__device__ __forceinline__ bool take_tile(const KArgs& a, int o, int src, int t, int myx, TabCache* tab, Cmd* cmd,
                   unsigned long long t_boundary, unsigned long long now) {
     const int lane = threadIdx.x;
     Hdr* hdr = hdr_of(a.ws);
@@ -594,7 +594,7 @@ __device__ __forceinline__ int phase_of(const KArgs& a, int o) { return a.op[o].
 // have_pre; else read now), claim, and only then wait for the commit's
 // completion count, so the commit and the claim share one round trip.
 template <bool COMB>
-__device__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool have_prev, int64_t& idle,
+__device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cmd* cmd, bool have_prev, int64_t& idle,
                          TabCache* tab, bool have_pre, Polls pre, int pre_t, const int32_t* n3s, int& n_traced) {
     const int lane = threadIdx.x;
     Hdr* hdr = hdr_of(a.ws);
@@ -908,7 +908,7 @@ __device__ void build_row_tiles(const OpArg& op, uint64_t* table, uint32_t* grp,
     store_row_tiles(op, table, grp, gmax, scan, s_cnt, s_off, *s_total, nullptr, nullptr, nullptr);
 }
 
-__device__ void instantiate(const KArgs& a, int o, int32_t* scan, int32_t* s_cnt, int32_t* s_off) {
+__device__ __forceinline__ void instantiate(const KArgs& a, int o, int32_t* scan, int32_t* s_cnt, int32_t* s_off) {
     const OpArg& op = a.op[o];
     OpDyn* d = dyn_of(a.ws) + o;
     if (op.rel) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");  // system scope: peer-written inputs
