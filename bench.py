@@ -418,6 +418,8 @@ def main():
         roof["measured_peaks"] = meas
         roof["frac_of_measured_mfma"] = round(roof["achieved_tflops"] / meas[f"mfma_{dtype}_tflops"], 4)
         roof["frac_of_measured_hbm"] = round(abytes / (ffn_ms * 1e-3) / 1e9 / meas["hbm_read_gbs"], 4)
+        if dtype == "bf16":
+            roof["vs_vendor_dense_gemm"] = round(roof["achieved_tflops"] / meas["vendor_gemm_bf16_16384x3072x3072_tflops"], 4)
 
     cpu = None
     parity = None

@@ -1,8 +1,9 @@
 """Achievable peaks of the GPU this runs on, measured with the kernels of
 libmoe_peaks.so (csrc/peaks.hip): the bf16 and fp8 MFMA throughput of a loop
 of nothing but independent MFMAs on every SIMD, and the HBM read rate of a
-streaming read of a buffer far larger than the caches.  Used as context
-beside the vendor peaks (bench.py reports the hot path's kernel against both).
+streaming read of a buffer far larger than the caches, and the vendor
+library's dense bf16 GEMM at an expert GEMM's shape.  Used as context beside
+the vendor peaks (bench.py reports the hot path's kernel against both).
 
     python -m paper_2607_18002_amd.peaks
 """
@@ -76,9 +77,24 @@ def stream_read_gbs(gib: float = 4.0, blocks: int = 2048, reps: int = 5) -> floa
     return n / t / 1e9
 
 
+def vendor_gemm_tflops(M: int = 16384, N: int = 3072, K: int = 3072, reps: int = 20) -> float:
+    """bf16 dense GEMM throughput of the vendor library (torch.matmul on
+    contiguous operands, hipBLASLt) at one expert GEMM's shape with all routed
+    rows in one matrix: what a library GEMM reaches without grouping, gating or
+    scheduling, as context for the grouped kernel's MFMA fraction."""
+    import torch
+    g = torch.Generator(device="cuda").manual_seed(0)
+    a = torch.randn((M, K), generator=g, device="cuda").to(torch.bfloat16)
+    b = torch.randn((K, N), generator=g, device="cuda").to(torch.bfloat16)
+    t = _time(lambda: torch.matmul(a, b), reps)
+    del a, b
+    return 2.0 * M * N * K / t / 1e12
+
+
 def measure() -> dict:
     return {"mfma_bf16_tflops": round(mfma_tflops(1), 1), "mfma_fp8_tflops": round(mfma_tflops(2), 1),
-            "hbm_read_gbs": round(stream_read_gbs(), 1)}
+            "hbm_read_gbs": round(stream_read_gbs(), 1),
+            "vendor_gemm_bf16_16384x3072x3072_tflops": round(vendor_gemm_tflops(), 1)}
 
 
 if __name__ == "__main__":
