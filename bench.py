@@ -45,7 +45,7 @@ sys.path.insert(0, ROOT)
 
 # The pipeline the benchmark times (tests build the same one from here).
 DEFAULTS = dict(quota=64, decode_layout="masked", prefill_layout="contiguous", fused_combine=False,
-                group_row_tiles=0, gather="fused")
+                group_row_tiles=0, gather="fused", prefill_tile_rows=0)
 
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0}
@@ -71,6 +71,8 @@ def parse():
                     help="most row tiles of one expert that share each weight slice fetch (0 = library default)")
     ap.add_argument("--gather", choices=("fused", "copy"), default="fused",
                     help="GEMM-1 reads x rows through row_to_assign (fused) or from the permuted copy x_perm")
+    ap.add_argument("--prefill-tile-rows", type=int, choices=(0, 128, 192), default=DEFAULTS["prefill_tile_rows"],
+                    help="128: bf16 prefill ops run 128-row tiles (shorter preemption waits); 0/192: 192-row tiles")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--dump-trace", default=None, help="write the traced launch's per-tile records (.npy)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -111,13 +113,14 @@ def build_specs(cfg, dev):
 
 def pipeline_kwargs(quota=DEFAULTS["quota"], decode_layout=DEFAULTS["decode_layout"],
                     prefill_layout=DEFAULTS["prefill_layout"], fused_combine=DEFAULTS["fused_combine"],
-                    group_row_tiles=DEFAULTS["group_row_tiles"], gather=DEFAULTS["gather"]):
+                    group_row_tiles=DEFAULTS["group_row_tiles"], gather=DEFAULTS["gather"],
+                    prefill_tile_rows=DEFAULTS["prefill_tile_rows"]):
     """MoEPipeline arguments of a benchmark configuration (the masked layouts
     need the fused gather)."""
     fused = gather == "fused"
     return dict(decode_quota_wg=quota, fused_gather=fused, fused_combine=fused_combine,
                 masked_decode=decode_layout == "masked" and fused, masked_prefill=prefill_layout == "masked" and fused,
-                group_row_tiles=group_row_tiles)
+                group_row_tiles=group_row_tiles, prefill_tile_rows=prefill_tile_rows)
 
 
 def tile_clock(tr):
@@ -313,7 +316,7 @@ def main():
     specs, layers = build_specs(cfg, dev)
     t_gen = time.perf_counter() - t_gen
     pkw = pipeline_kwargs(args.quota, args.decode_layout, args.prefill_layout, args.fused_combine,
-                          args.group_row_tiles, args.gather)
+                          args.group_row_tiles, args.gather, args.prefill_tile_rows)
     # the per-tile trace costs no round trip (each workgroup writes its own
     # block), so the timed launches carry it: the last one gives the decode
     # latency and clock figures in the timed loop's own steady state
@@ -446,7 +449,7 @@ def main():
                    "prefill_tokens": cfg.prefill_tokens, "decode_tokens": cfg.decode_tokens,
                    "experts_local": cfg.E_local, "experts_global": cfg.E_global, "top_k": cfg.top_k,
                    "hidden": cfg.H, "intermediate": cfg.I, "decode_quota_wg": args.quota,
-                   "group_row_tiles": args.group_row_tiles,
+                   "group_row_tiles": args.group_row_tiles, "prefill_tile_rows": args.prefill_tile_rows or 192,
                    "gather": args.gather, "combine": "fused" if args.fused_combine else "separate",
                    "decode_layout": "masked" if pkw["masked_decode"] else "contiguous",
                    "prefill_layout": "masked" if pkw["masked_prefill"] else "contiguous", "local_rows": rows},

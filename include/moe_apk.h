@@ -339,7 +339,11 @@ typedef struct moe_sched_config {
                                  as Green Contexts): workgroups below the fixed q' take
                                  only decode tiles, the others only prefill tiles, and
                                  neither borrows idle workgroups of the other phase   */
-    int32_t reserved1;
+    int32_t prefill_tile_rows;/* 0 or 192: bf16 prefill ops run 192-row tiles (Eq. (3)'s
+                                 M_t = 192).  128: they run the 128-row tiles, which
+                                 shortens the longest prefill tile a decode op can wait
+                                 for ("Bounded Tile-level Preemption") at some cost in
+                                 prefill throughput                                   */
 } moe_sched_config;
 
 /* Segment alignment the FFN needs for ops of this phase and dtype (32 rows,

@@ -51,7 +51,7 @@ class SchedConfig(C.Structure):
         ("n_workgroups", _i32), ("decode_quota_wg", _i32), ("decode_quota_max_wg", _i32),
         ("x_moe_expected", _i32), ("round_multiple", _i32), ("group_row_tiles", _i32),
         ("abort_word", _p), ("trace", _p), ("trace_capacity", _i64), ("op_stats", _p),
-        ("spin_limit", _i64), ("static_partition", _i32), ("reserved1", _i32),
+        ("spin_limit", _i64), ("static_partition", _i32), ("prefill_tile_rows", _i32),
     ]
 
 

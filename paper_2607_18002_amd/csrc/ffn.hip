@@ -1132,7 +1132,9 @@ namespace {
 // Checks every op descriptor and fills the kernel's per-op arguments and the
 // init kernel's readiness fields; off = the ops' array bytes.  Shared by the
 // persistent launch and the plain-grid baseline.
-moe_status_t fill_ops(const moe_op_desc* ops, int32_t n_ops, int wc_khz, KArgs& a, InitArgs& ia, size_t& off) {
+// prefill_rows: 0 or 192 = the tall prefill tiles; 128 = bf16 prefill ops run the 128-row tile class.
+moe_status_t fill_ops(const moe_op_desc* ops, int32_t n_ops, int wc_khz, KArgs& a, InitArgs& ia, size_t& off,
+                      int prefill_rows = 0) {
     using moeapk_host::fail;
     off = 0;                                          // bytes from the arrays base
     for (int o = 0; o < n_ops; ++o) {
@@ -1142,7 +1144,8 @@ moe_status_t fill_ops(const moe_op_desc* ops, int32_t n_ops, int wc_khz, KArgs& 
             return fail(MOE_ERR_UNSUPPORTED, "op %d: dtype %d not supported by the FFN kernel", o, d.dtype);
         if (d.weight_layout != MOE_LAYOUT_PACKED)
             return fail(MOE_ERR_UNSUPPORTED, "op %d: weights must be in MOE_LAYOUT_PACKED (moe_pack_weights)", o);
-        const int cls = class_of(d.phase, d.dtype);
+        int cls = class_of(d.phase, d.dtype);
+        if (cls == CLS_P_BF16 && prefill_rows == 128) cls = CLS_D_BF16;
         const ClassInfo ci = class_info(cls);
         if (d.E_local < 1 || d.E_local > 1024) return fail(MOE_ERR_UNSUPPORTED, "op %d: E_local=%d outside [1,1024]", o, d.E_local);
         // H and I are the K of a GEMM (whole pairs of K steps) and split into whole output tiles
@@ -1255,7 +1258,9 @@ moe_status_t launch_ffn(const moe_op_desc* ops, int32_t n_ops, const moe_sched_c
     InitArgs ia;
     memset(&ia, 0, sizeof(ia));
     size_t off = 0;
-    st = fill_ops(ops, n_ops, wc_khz, a, ia, off);
+    if (cfg->prefill_tile_rows != 0 && cfg->prefill_tile_rows != 192 && cfg->prefill_tile_rows != 128)
+        return fail(MOE_ERR_INVALID_ARG, "prefill_tile_rows=%d must be 0, 192 or 128", cfg->prefill_tile_rows);
+    st = fill_ops(ops, n_ops, wc_khz, a, ia, off, cfg->prefill_tile_rows);
     if (st != MOE_OK) return st;
     if (kArraysOff + off > (size_t)INT32_MAX) return fail(MOE_ERR_UNSUPPORTED, "scheduler workspace too large");
     int n_wg = cfg->n_workgroups > 0 ? cfg->n_workgroups : cu;

@@ -132,6 +132,7 @@ class MoEPipeline:
                  trace_capacity: int = 0, spin_limit: int = 0, abort_word: Optional[torch.Tensor] = None,
                  y_dtype: torch.dtype = torch.bfloat16, fused_gather: bool = False, group_row_tiles: int = 0,
                  static_partition: bool = False, fused_combine: bool = False, masked_decode: bool = False,
+                 prefill_tile_rows: int = 0,
                  masked_prefill: bool = False):
         """fused_gather: GEMM-1 reads its rows straight from x through row_to_assign
         (permute then only builds the maps), instead of from a permuted copy x_perm.
@@ -195,7 +196,8 @@ class MoEPipeline:
                                abort_word=abort_word.data_ptr() if abort_word is not None else None,
                                trace=self.trace.data_ptr() if trace_capacity > 0 else None,
                                trace_capacity=trace_capacity, op_stats=self.stats.data_ptr(),
-                               spin_limit=spin_limit, static_partition=int(static_partition))
+                               spin_limit=spin_limit, static_partition=int(static_partition),
+                               prefill_tile_rows=prefill_tile_rows)
         self._descs = [self._desc(i, b, fused_gather, fused_combine) for i, b in enumerate(self.bufs)]
         self._route_args = []
         for b in self.bufs:

@@ -758,3 +758,23 @@ def test_plain_grid_baseline_matches_persistent_bitwise(dev, dtype):
             valid = (r - e * b.slots) < b.counts.long()[e]
         assert torch.equal(h0[valid], h1[valid])
         assert torch.equal(y0[valid], y1[valid])
+
+
+def test_prefill_128_row_tiles_match_oracle(dev):
+    """With prefill_tile_rows = 128 the bf16 prefill op of a mixed launch runs
+    the 128-row tiles (every traced prefill tile has at most 128 rows and the
+    op's tile count follows Eq. (3) at M_t = 128); both ops still match the
+    oracle."""
+    cfg = custom_config(2, cfg_id=403, H=512, I=512, prefill_tokens=1500, decode_tokens=200, E_global=64,
+                        E_local=16, top_k=4, zipf_s=(1.1,))
+    specs, lay, _ = layer_specs(cfg, 0, dev)
+    pipe = _run_pipeline(dev, specs, trace_capacity=1 << 16, fused_gather=True, prefill_tile_rows=128)
+    assert pipe.statuses() == (0, 0)
+    tr = pipe.trace_records()
+    st = pipe.op_stats()
+    for i, ph in enumerate(lay.phases):
+        _check_op(pipe, i, cfg, lay, ph)
+        mine = tr[tr["op"] == i]
+        assert len(mine) and int(mine["rows"].max()) <= 128
+        counts = pipe.bufs[i].counts.cpu().numpy()
+        assert int(st["x_moe"][i]) == oracle.x_moe(counts, 128)
