@@ -187,11 +187,18 @@ struct InitArgs {
 
 // Zeroes the scheduler state (16-byte stores; the row-tile tables too, so an
 // entry read before it was written reads as invalid rather than as a previous
-// launch's tile) and writes the readiness fields; one workgroup, launched on
-// the same stream right before the persistent kernel.
+// launch's tile) and writes the readiness fields; launched on the same stream
+// right before the persistent kernel.  Workgroup 0 zeroes the header, op and
+// queue lines and then writes the fields; the others zero the per-op arrays.
 __global__ __launch_bounds__(256) void apk_init_kernel(const InitArgs a) {
     const u32x4 z = {0u, 0u, 0u, 0u};
-    for (int i = threadIdx.x; i < a.ws_vec; i += 256) ((u32x4*)a.ws)[i] = z;
+    const int head = (int)(kArraysOff / 16);
+    if (blockIdx.x > 0) {
+        for (int i = head + (blockIdx.x - 1) * 256 + threadIdx.x; i < a.ws_vec; i += (gridDim.x - 1) * 256)
+            ((u32x4*)a.ws)[i] = z;
+        return;
+    }
+    for (int i = threadIdx.x; i < head && i < a.ws_vec; i += 256) ((u32x4*)a.ws)[i] = z;
     __syncthreads();
     if (threadIdx.x == 0) {
         OpStatic* st = static_of(a.ws);
@@ -680,7 +687,12 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
     //     reaches -n3: then it turns COMBINING, and its combine tiles can be
     //     claimed (every y_perm row they read was stored before its commit).
     const int n3_l = COMB && lane < a.n_ops ? n3s[lane] : 0;
-    const uint64_t fmask = __ballot(pl.left == 0 && ((state == ST_ACTIVE && n3_l == 0) || (COMB && state == ST_COMBINING)));
+    //     The polls were issued before this workgroup's commit: if they show
+    //     its op one tile short, that tile is this workgroup's own and the
+    //     commit just issued completes the op (no further poll needed).
+    const bool own_last = have_prev && prev.stage != 3 && lane == prev.op && pl.left == -1;
+    const uint64_t fmask = __ballot((pl.left == 0 || own_last) &&
+                                    ((state == ST_ACTIVE && n3_l == 0) || (COMB && state == ST_COMBINING)));
     const uint64_t cmask = COMB ? __ballot(state == ST_ACTIVE && n3_l > 0 && pl.left == -n3_l) : 0ull;
     if (fmask | cmask) {
         int won = 0;
@@ -1323,7 +1335,9 @@ moe_status_t launch_ffn(const moe_op_desc* ops, int32_t n_ops, const moe_sched_c
     ia.ws = (char*)workspace;
     ia.status = status_word;
     hipStream_t s = (hipStream_t)stream;
-    hipLaunchKernelGGL(apk_init_kernel, dim3(1), dim3(256), 0, s, ia);
+    const int arr_vec = ia.ws_vec - (int)(kArraysOff / 16);
+    const int init_wg = 1 + (arr_vec <= 0 ? 0 : (arr_vec + 1023) / 1024 < 16 ? (arr_vec + 1023) / 1024 : 16);
+    hipLaunchKernelGGL(apk_init_kernel, dim3(init_wg), dim3(256), 0, s, ia);
     if (comb) hipLaunchKernelGGL(apk_kernel<true>, dim3(n_wg), dim3(256), kLdsBytes, s, a);
     else hipLaunchKernelGGL(apk_kernel<false>, dim3(n_wg), dim3(256), kLdsBytes, s, a);
     const hipError_t err = hipGetLastError();
