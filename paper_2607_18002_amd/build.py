@@ -64,6 +64,60 @@ def _scratch_check(src: str, lines) -> None:
                                        "its kernel arguments were copied to scratch")
 
 
+# data operand: the first of a buffer store, the second of a global, flat or scratch store
+_STORE_WIDE = re.compile(r"^(?:buffer_store_dwordx[34]\s+|(?:global|flat|scratch)_store_dwordx[34]\s+\S+,\s*)"
+                         r"v\[(\d+):(\d+)\]")
+_VREG = re.compile(r"^v\[(\d+):(\d+)\]|^v(\d+)$")
+
+
+def _vregs(tok: str):
+    m = _VREG.match(tok.rstrip(","))
+    if not m:
+        return set()
+    if m.group(3) is not None:
+        return {int(m.group(3))}
+    return set(range(int(m.group(1)), int(m.group(2)) + 1))
+
+
+def _store_data_check(src: str, asm: str) -> None:
+    """A store of more than 8 bytes reads its data registers after it issues;
+    on gfx950 two wait states must pass before a VALU instruction writes them.
+    Refuse code in which the next VALU instruction writes them sooner."""
+    lines = [ln.strip() for ln in asm.splitlines()]
+    for i, t in enumerate(lines):
+        m = _STORE_WIDE.match(t)
+        if not m:
+            continue
+        data = set(range(int(m.group(1)), int(m.group(2)) + 1))
+        states = 0
+        for u in lines[i + 1:i + 12]:
+            # labels, comments and directives emit nothing; control falls through a label
+            if not u or u.startswith(";") or u.startswith(".") or u.endswith(":"):
+                continue
+            op = u.split()[0]
+            if op in ("s_branch", "s_setpc_b64", "s_endpgm"):
+                break
+            if op == "s_nop":
+                states += int(u.split()[1], 0) + 1
+            else:
+                if op.startswith("v_") and len(u.split()) > 1 and _vregs(u.split()[1]) & data:
+                    raise RuntimeError(f"{src}: '{u}' overwrites the data of '{t}' after {states} wait states (2 needed)")
+                states += 1
+            if states >= 2:
+                break
+
+
+def _compile_asm_check(src: str, build_dir: str = BUILD, defines=()) -> None:
+    asm_path = os.path.join(build_dir, os.path.splitext(src)[0] + ".device.s")
+    cmd = [HIPCC, *FLAGS, *[f"-D{d}" for d in defines], "--cuda-device-only", "-S", "-x", "hip",
+           os.path.join(CSRC, src), "-o", asm_path]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"device assembly failed: {src}\n" + (r.stdout + r.stderr)[-3000:])
+    with open(asm_path) as f:
+        _store_data_check(src, f.read())
+
+
 def _compile(src: str, verbose: bool, build_dir: str = BUILD, defines=()) -> str:
     obj = os.path.join(build_dir, os.path.splitext(src)[0] + ".o")
     cmd = [HIPCC, *FLAGS, *[f"-D{d}" for d in defines], "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj]
@@ -111,8 +165,12 @@ def build(verbose: bool = False, out_dir: str = "", defines=()) -> str:
     bdir = os.path.join(out_dir, "_obj") if out_dir else BUILD
     os.makedirs(bdir, exist_ok=True)
     allsrc = SOURCES if out_dir else SOURCES + PEAKS_SOURCES
-    with cf.ThreadPoolExecutor(max_workers=min(8, len(allsrc))) as ex:
+    with cf.ThreadPoolExecutor(max_workers=8) as ex:
+        # every kernel's device code is also checked for the store-data hazard
+        asm_checks = [ex.submit(_compile_asm_check, s, bdir, defines) for s in allsrc if s.endswith(".hip")]
         objs = list(ex.map(lambda s: _compile(s, verbose, bdir, defines), allsrc))
+        for c in asm_checks:
+            c.result()
     lib = os.path.join(out_dir, "libmoe_apk.so") if out_dir else LIB
     _link(objs[:len(SOURCES)], lib)
     if not out_dir:

@@ -16,6 +16,10 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x8 __attribute__((ext_vector_type(8)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+// 16 bytes that may alias any other type: the epilogues stage results in LDS
+// with 2- or 4-byte stores and read them back 16 bytes at a time, so the
+// read-back must not be reordered above those stores by type-based aliasing.
+typedef unsigned int u32x4_alias __attribute__((ext_vector_type(4), may_alias));
 
 constexpr int kWave = 64;
 

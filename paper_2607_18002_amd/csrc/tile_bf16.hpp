@@ -275,7 +275,7 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
     const uint32_t ooff = (uint32_t)orow * (uint32_t)ldo * 2u + (uint32_t)(wn * OC + och * 8) * 2u;
 #pragma unroll
     for (int p = 0; p < MACT * 32 / RPI; ++p) {
-        const u32x4 v = *(const u32x4*)(stg + (p * RPI + orow) * ORB + och * 16);
+        const u32x4 v = *(const u32x4_alias*)(stg + (p * RPI + orow) * ORB + och * 16);
         __builtin_amdgcn_raw_buffer_store_b128(v, Ob, (int)ooff, (int)((uint32_t)(p * RPI) * (uint32_t)ldo * 2u),
                                                kStoreDevice);
     }

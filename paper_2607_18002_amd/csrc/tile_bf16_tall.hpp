@@ -191,10 +191,16 @@ __device__ __forceinline__ void gemm_tile_tall(const uint16_t* __restrict__ A, i
 #pragma unroll
         for (int p = 0; p < 4 * 32 / RPI; ++p) {
             if (p * RPI >= nb_h * 32) break;
-            const u32x4 v = *(const u32x4*)(stg + (p * RPI + orow) * ORB + och * 16);
+            const u32x4 v = *(const u32x4_alias*)(stg + (p * RPI + orow) * ORB + och * 16);
             __builtin_amdgcn_raw_buffer_store_b128(
                 v, Ob, (int)ooff, (int)((uint32_t)(i0 * 32 + p * RPI) * (uint32_t)ldo * 2u), kStoreDevice);
         }
+        // A 16-byte store reads its data registers after it issues: two wait
+        // states must pass before a VALU instruction overwrites them.  The next
+        // part's first instructions are VALU work that may reuse those
+        // registers, and the compiler does not insert the wait states across
+        // the scheduling barrier that starts the part.
+        if (h + 1 < (MACT + 3) / 4) asm volatile("s_nop 1");
     }
 }
 

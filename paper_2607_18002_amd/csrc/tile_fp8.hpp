@@ -187,7 +187,7 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
             // they run, so partials take 2 * NBW accumulators, not MACT * NBW.
             auto frag = [&](int i, int kk) {
                 const char* p = cur + arow + i * 32 * S::LDS_ROW + kk * 64;
-                const u32x4 lo = *(const u32x4*)p, hi = *(const u32x4*)(p + 16);
+                const u32x4 lo = *(const u32x4_alias*)p, hi = *(const u32x4_alias*)(p + 16);
                 return i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
             };
             f32x16 part[2][S::NBW];
@@ -297,7 +297,7 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
         const uint32_t ooff = (uint32_t)orow * (uint32_t)ldo * 2u + (uint32_t)(wn * S::WCOLS + och * 8) * 2u;
 #pragma unroll
         for (int p = 0; p < MACT * 32 / RPI; ++p) {
-            const u32x4 v = *(const u32x4*)(stg + (p * RPI + orow) * S::OUT_ROW + och * 16);
+            const u32x4 v = *(const u32x4_alias*)(stg + (p * RPI + orow) * S::OUT_ROW + och * 16);
             __builtin_amdgcn_raw_buffer_store_b128(v, Ob, (int)ooff, (int)((uint32_t)(p * RPI) * (uint32_t)ldo * 2u),
                                                    kStoreDevice);
         }
