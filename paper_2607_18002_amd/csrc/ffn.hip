@@ -835,6 +835,29 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
         }
     }
     finish_prev();
+    // Nothing claimable, every op instantiated and every queue of every active
+    // op found empty above: no tile can become claimable here any more (no
+    // template waits for its release, no combine tiles will follow), so the
+    // workgroup leaves now rather than polling until the last op is finished
+    // by the workgroups still running its tiles.
+    // The polls predate this boundary's commit, so that commit may have been
+    // the last of its op: once it has completed, an op whose count reads full
+    // is finished here (unless another workgroup wins it), since no
+    // workgroup may be left to see it full later.
+    if (!COMB && !a.split && __ballot(state == ST_WAIT || state == ST_INIT) == 0) {
+        wait_own_stores();
+        int won = 0;
+        if (lane < a.n_ops && state == ST_ACTIVE && ld_relaxed_agent(&dyn[lane].left) == 0)
+            won = atomicCAS(&dyn[lane].state, ST_ACTIVE, ST_FINISHING) == ST_ACTIVE;
+        uint64_t wmask = __ballot(won);
+        while (wmask) {                                              // wave-uniform loop
+            const int o = __ffsll((long long)wmask) - 1;
+            wmask &= wmask - 1;
+            if (lane == 0) finish_op(a, o, ld_relaxed_agent(&dyn[o].total));
+        }
+        if (lane == 0) cmd->kind = CMD_EXIT;
+        return;
+    }
     if (lane == 0) cmd->kind = CMD_IDLE;
     ++idle;
 }

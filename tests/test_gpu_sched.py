@@ -234,6 +234,27 @@ def test_results_independent_of_schedule(dev):
             np.testing.assert_array_equal(a, b)
 
 
+@pytest.mark.parametrize("n_ops,n_wg", [(16, 0), (16, 24), (2, 0)])
+def test_every_op_finished_when_workgroups_leave_early(dev, n_ops, n_wg):
+    """Workgroups leave as soon as every op is instantiated and every queue is
+    empty; an op whose last commit no polling workgroup saw must still be
+    finished (done word, statistics) by the workgroup that committed it."""
+    cfg = custom_config(2, cfg_id=402, H=256, I=256, prefill_tokens=96, decode_tokens=32, E_global=16,
+                        E_local=8, top_k=2, n_layers=n_ops // 2, zipf_s=(1.1, 0.7))
+    specs = []
+    for layer in range(n_ops // 2):
+        s, _, _ = layer_specs(cfg, layer, dev)
+        specs += s
+    for _ in range(3):
+        pipe = _pipe(dev, specs, n_workgroups=n_wg, trace_capacity=1 << 16)
+        assert pipe.statuses() == (0, 0)
+        st = pipe.op_stats()
+        for i in range(len(specs)):
+            xm, ntiles = _tiles_per_op(pipe, i)
+            assert int(pipe.bufs[i].done_word.item()) == 1, i
+            assert st["x_moe"][i] == xm and st["n_tiles"][i] == ntiles and st["t_done"][i] > 0, i
+
+
 def test_adaptive_quota_eq4(dev):
     cfg = _mixed_cfg()
     specs, _, _ = layer_specs(cfg, 0, dev)
