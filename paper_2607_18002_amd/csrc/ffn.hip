@@ -70,9 +70,6 @@ enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1, CLS_FP8 = 2 };
 enum : int32_t { ST_WAIT = 0, ST_INIT = 1, ST_ACTIVE = 2, ST_DONE = 3, ST_FINISHING = 4, ST_COMBINING = 5 };
 constexpr int kCombTokens = 32;           // tokens per fused-combine tile
 enum : int32_t { CMD_EXIT = 0, CMD_TILE = 1, CMD_INST = 2, CMD_IDLE = 3 };
-// Standby (boundary step 4b): a decode template whose predecessor has at most
-// this many uncommitted tiles is about to be released.
-constexpr int kHoldTiles = 64;
 
 struct OpArg {
     const int32_t* counts;
@@ -103,7 +100,6 @@ struct KArgs {
     int32_t pre_dec_all;       // no prefill op in the launch: every workgroup claims decode tiles ahead
     int32_t split;             // static partition: decode only below pre_wg, prefill only at or above
     int32_t inst_wg;           // decode templates are instantiated by workgroups below this (0: any)
-    int64_t hold_ticks;        // standby: how soon a decode template's release must be (wall-clock ticks)
     int64_t spin_limit;
     const uint32_t* abort_word;
     moe_trace_rec* trace;
@@ -759,24 +755,6 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
                     now >= ld_relaxed_agent(&dyn[dep].t_done) + (uint64_t)sta[o_l].gap;
         }
     }
-    // 4b. standby: the first workgroup of each XCD among those below q' takes
-    //     no prefill tile while a decode template is about to be released (its
-    //     release time is near, its predecessor is done and only the gap runs,
-    //     or its predecessor has few tiles left), so the op finds a workgroup
-    //     at a boundary when it arrives instead of behind a whole prefill tile.
-    //     It still takes every decode tile it can claim.
-    bool soon = false;
-    if (!a.split && wg < kXcds && wg < q && state == ST_WAIT && phase == MOE_DECODE && !ready &&
-        sta[o_l].rel_word == nullptr) {
-        const int dep = sta[o_l].dep;
-        if (dep < 0) {
-            soon = sta[o_l].rel_after >= 0 && t0 + (uint64_t)sta[o_l].rel_after <= now + (uint64_t)a.hold_ticks;
-        } else {
-            const int ds = ld_relaxed_agent(&dyn[dep].state);
-            soon = ds == ST_DONE || ((ds == ST_ACTIVE || ds == ST_FINISHING) && ld_relaxed_agent(&dyn[dep].left) >= -kHoldTiles);
-        }
-    }
-    const bool hold = __ballot(soon) != 0;
     const uint64_t rmask = __ballot(ready);
     if (rmask) {
         const int o = __ffsll((long long)rmask) - 1;
@@ -799,7 +777,7 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
     const uint64_t own_avail = __ballot(active && own_claim < own_size);
     const bool prefer_decode = a.split ? wg < a.pre_wg : wg < q;
     const uint64_t order[2] = {prefer_decode ? dmask : pmask, prefer_decode ? pmask : dmask};
-    for (int p = 0; p < (a.split || hold ? 1 : 2); ++p) {          // a static partition never borrows
+    for (int p = 0; p < (a.split ? 1 : 2); ++p) {                   // a static partition never borrows
         uint64_t m = order[p];
         while (m) {                                                  // wave-uniform loop
             const int o = __ffsll((long long)m) - 1;
@@ -1349,7 +1327,6 @@ moe_status_t launch_ffn(const moe_op_desc* ops, int32_t n_ops, const moe_sched_c
     a.pre_wg = !any_decode ? 0 : (a.x_star <= 0 ? moeapk::decode_quota(a.q, 0, 0, a.q_max, a.c) : a.q_max);
     // the smallest q' of any decode op (Eq. (4) is non-decreasing in x_moe >= 1)
     a.inst_wg = a.x_star <= 0 ? a.pre_wg : moeapk::decode_quota(a.q, 1, a.x_star, a.q_max, a.c);
-    a.hold_ticks = (int64_t)100 * wc_khz / 1000;             // 100 us
     a.spin_limit = cfg->spin_limit > 0 ? cfg->spin_limit : (int64_t)2000000;
     a.abort_word = cfg->abort_word;
     a.trace = cfg->trace;

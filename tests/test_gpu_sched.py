@@ -255,26 +255,6 @@ def test_every_op_finished_when_workgroups_leave_early(dev, n_ops, n_wg):
             assert st["x_moe"][i] == xm and st["n_tiles"][i] == ntiles and st["t_done"][i] > 0, i
 
 
-def test_standby_workgroups_wait_for_an_imminent_decode_op(dev):
-    """The first workgroup of each XCD below q' starts no prefill tile while a
-    decode template is due within the standby window (here released 50 us
-    after the start), so the op finds them at a boundary when it arrives; the
-    other workgroups run prefill from the start."""
-    cfg = _mixed_cfg()
-    specs, _, _ = layer_specs(cfg, 0, dev, decode=dict(release_after_ns=50_000))
-    pipe = _pipe(dev, specs, trace_capacity=1 << 16, decode_quota_wg=64)
-    assert pipe.statuses() == (0, 0)
-    tr = pipe.trace_records()
-    t0 = pipe.kernel_t0()
-    release = t0 + int(50_000 / TICK_NS)
-    pre = tr[tr["op"] == 0]
-    standby = pre[pre["wg"] < 8]
-    assert np.all(standby["t_start"] >= release)
-    assert np.any(pre[pre["wg"] >= 8]["t_start"] < release)               # the rest did not wait
-    dec = tr[tr["op"] == 1]
-    assert np.any(dec["wg"] < 8)                                           # and they took decode tiles
-
-
 def test_adaptive_quota_eq4(dev):
     cfg = _mixed_cfg()
     specs, _, _ = layer_specs(cfg, 0, dev)
