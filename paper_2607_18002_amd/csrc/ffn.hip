@@ -14,7 +14,11 @@
 // thread-block clusters, so the scheduling unit is the workgroup: at every
 // tile boundary wave 0 commits the finished tile, polls the operation words
 // (one lane per operation), claims the next tile with one device-scope atomic
-// and broadcasts it through LDS; the whole workgroup runs the tile.  Each
+// and broadcasts it through LDS; the whole workgroup runs the tile.  A
+// template whose inputs were in place at the launch is built ahead of its
+// ready signal (row tiles, queues, counters) by a workgroup that never
+// prefers decode; the signal then only flips its state word, and the
+// workgroup that flips it claims the first tile in the same boundary.  Each
 // operation's tiles are numbered GEMM-1 tiles first (row-tile major), then
 // GEMM-2 tiles; a GEMM-2 tile waits (bounded) on a per-row-tile counter that
 // GEMM-1 tiles bump once their h rows are visible.  Every claimed tile belongs
@@ -68,6 +72,12 @@ constexpr int kLdsBytes = kMax2(kMax2(TallLds<ShapeP>::bytes, ShapeD::LDS), Shap
 
 enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1, CLS_FP8 = 2 };
 enum : int32_t { ST_WAIT = 0, ST_INIT = 1, ST_ACTIVE = 2, ST_DONE = 3, ST_FINISHING = 4, ST_COMBINING = 5 };
+// A template built ahead of its ready signal (row tiles, queues and counters
+// in place, nothing claimable) waits in a state word that also carries what
+// its activation needs: ST_BUILT | (no row tiles) << 4 | q' << 5.
+constexpr int32_t ST_BUILT = 6;
+__device__ __forceinline__ bool is_built(int32_t s) { return (s & 15) == ST_BUILT; }
+__device__ __forceinline__ int32_t built_word(int xm, int qd) { return ST_BUILT | (xm == 0 ? 16 : 0) | (qd << 5); }
 constexpr int kCombTokens = 32;           // tokens per fused-combine tile
 enum : int32_t { CMD_EXIT = 0, CMD_TILE = 1, CMD_INST = 2, CMD_IDLE = 3 };
 
@@ -678,7 +688,7 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
         if (lane == 0) cmd->kind = CMD_EXIT;
         return;
     }
-    const int q = __shfl(pl.q, 0, 64);
+    int q = __shfl(pl.q, 0, 64);
     // 2b. an op whose every tile had committed when polled is finished by the
     //     workgroup that wins its ACTIVE -> FINISHING transition (left only
     //     grows and is 0 only once the last tile committed, so a stale poll can
@@ -715,10 +725,10 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
     }
     const uint64_t now = wall_ticks();
     // phases with claimable work in the polls this decision uses (recorded in the trace)
-    const bool active = state == ST_ACTIVE || (COMB && state == ST_COMBINING);
-    const uint64_t dmask = __ballot(active && phase == MOE_DECODE);
-    const uint64_t pmask = __ballot(active && phase == MOE_PREFILL);
-    const int phases_seen = (dmask ? 1 : 0) | (pmask ? 2 : 0);
+    bool active = state == ST_ACTIVE || (COMB && state == ST_COMBINING);
+    uint64_t dmask = __ballot(active && phase == MOE_DECODE);
+    uint64_t pmask = __ballot(active && phase == MOE_PREFILL);
+    int phases_seen = (dmask ? 1 : 0) | (pmask ? 2 : 0);
 
     // 3b. a claim made ahead during the previous tile (the hook claimed in this
     //     XCD's queue of op prev.pre_next): take it if it landed inside the queue
@@ -742,9 +752,12 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
     //    smallest q' the launch can produce, which therefore prefers decode and
     //    takes the op's first tile at its very next boundary: a decode op waits
     //    for one tile boundary of those workgroups plus its instantiation.
+    //    A template built ahead (4b) needs no instantiation: the same
+    //    workgroups activate it and claim its first tile in the same boundary.
     bool ready = false;
+    const bool built = is_built(state);
     const bool may_inst = phase == MOE_PREFILL || a.inst_wg == 0 || wg < a.inst_wg;
-    if (state == ST_WAIT && may_inst) {
+    if ((state == ST_WAIT || built) && may_inst) {
         ready = true;
         const uint32_t* rw = sta[o_l].rel_word;
         if (rw) ready = __hip_atomic_load(rw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != 0u;
@@ -755,7 +768,43 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
                     now >= ld_relaxed_agent(&dyn[dep].t_done) + (uint64_t)sta[o_l].gap;
         }
     }
-    const uint64_t rmask = __ballot(ready);
+    // 4a. activation of a built template: one transition of its state word.
+    //     Its queue words and table entries reached the coherence point before
+    //     the word turned BUILT, so every claim that follows the transition
+    //     finds them.  An op with no row tiles finishes here (or turns
+    //     COMBINING: its combine tiles write zeros).
+    const uint64_t amask = __ballot(ready && built);
+    if (amask) {
+        const int o = __ffsll((long long)amask) - 1;
+        int to = 0;
+        if (lane == o) {
+            const bool empty = (state >> 4) & 1;
+            const int next = !empty ? ST_ACTIVE : (n3_l > 0 ? ST_COMBINING : ST_FINISHING);
+            if (atomicCAS(&dyn[o].state, state, next) == state) {
+                to = next;
+                __hip_atomic_store(&dyn[o].t_seen, (unsigned long long)now, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                __hip_atomic_store(&dyn[o].t_ready, (unsigned long long)now, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                if (empty) {
+                    __hip_atomic_store(&dyn[o].t_first, (unsigned long long)now, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    if (next == ST_FINISHING) finish_op(a, o, 0);
+                } else if (phase == MOE_DECODE) {
+                    __hip_atomic_store(&hdr->quota, state >> 5, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                }
+            }
+        }
+        to = __shfl(to, o, 64);
+        const int qd = __shfl(state >> 5, o, 64);
+        if (to != 0) {
+            if (lane == o) state = to == ST_FINISHING ? ST_DONE : to;
+            if (to == ST_ACTIVE && phase_of(a, o) == MOE_DECODE) q = qd;
+            active = state == ST_ACTIVE || (COMB && state == ST_COMBINING);
+            dmask = __ballot(active && phase == MOE_DECODE);
+            pmask = __ballot(active && phase == MOE_PREFILL);
+            phases_seen = (dmask ? 1 : 0) | (pmask ? 2 : 0);
+            idle = 0;
+        }
+    }
+    const uint64_t rmask = __ballot(ready && !built);
     if (rmask) {
         const int o = __ffsll((long long)rmask) - 1;
         int won = 0;
@@ -765,9 +814,26 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
         }
         if (__ballot(won)) {
             finish_prev();
-            if (lane == 0) { cmd->kind = CMD_INST; cmd->op = o; }
+            if (lane == 0) { cmd->kind = CMD_INST; cmd->op = o; cmd->stage = 1; }
             idle = 0;
             return;
+        }
+    }
+    // 4b. build ahead: a template whose inputs were in place at the launch (no
+    //     release word) is built before its ready signal, by a workgroup that
+    //     never prefers decode, and waits BUILT.
+    if (wg >= a.pre_wg) {
+        const uint64_t bmask = __ballot(state == ST_WAIT && !ready && sta[o_l].rel_word == nullptr);
+        if (bmask) {
+            const int o = __ffsll((long long)bmask) - 1;
+            int won = 0;
+            if (lane == o) won = atomicCAS(&dyn[o].state, ST_WAIT, ST_INIT) == ST_WAIT;
+            if (__ballot(won)) {
+                finish_prev();
+                if (lane == 0) { cmd->kind = CMD_INST; cmd->op = o; cmd->stage = 0; }
+                idle = 0;
+                return;
+            }
         }
     }
 
@@ -835,7 +901,7 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
         }
     }
     finish_prev();
-    // Nothing claimable, every op instantiated and every queue of every active
+    // Nothing claimable, every op activated and every queue of every active
     // op found empty above: no tile can become claimable here any more (no
     // template waits for its release, no combine tiles will follow), so the
     // workgroup leaves now rather than polling until the last op is finished
@@ -844,7 +910,7 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
     // the last of its op: once it has completed, an op whose count reads full
     // is finished here (unless another workgroup wins it), since no
     // workgroup may be left to see it full later.
-    if (!COMB && !a.split && __ballot(state == ST_WAIT || state == ST_INIT) == 0) {
+    if (!COMB && !a.split && __ballot(state == ST_WAIT || state == ST_INIT || is_built(state)) == 0) {
         wait_own_stores();
         int won = 0;
         if (lane < a.n_ops && state == ST_ACTIVE && ld_relaxed_agent(&dyn[lane].left) == 0)
@@ -943,7 +1009,11 @@ __device__ void build_row_tiles(const OpArg& op, uint64_t* table, uint32_t* grp,
     store_row_tiles(op, table, grp, gmax, scan, s_cnt, s_off, *s_total, nullptr, nullptr, nullptr);
 }
 
-__device__ __forceinline__ void instantiate(const KArgs& a, int o, int32_t* scan, int32_t* s_cnt, int32_t* s_off) {
+// Whole workgroup: builds op o's row tiles, queues and counters; with act,
+// the op then turns ACTIVE (its ready signal was seen), else it waits BUILT
+// for its activation (4a in boundary), which sets the decode quota.
+__device__ __forceinline__ void instantiate(const KArgs& a, int o, bool act, int32_t* scan, int32_t* s_cnt,
+                                            int32_t* s_off) {
     const OpArg& op = a.op[o];
     OpDyn* d = dyn_of(a.ws) + o;
     if (op.rel) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");  // system scope: peer-written inputs
@@ -963,12 +1033,12 @@ __device__ __forceinline__ void instantiate(const KArgs& a, int o, int32_t* scan
         store_row_tiles(op, (uint64_t*)(arr + op.table_off), (uint32_t*)(arr + op.grp_off), gmax, scan, s_cnt, s_off,
                         xm, s_cut, (uint64_t*)(arr + op.qtab_off), (uint32_t*)(arr + op.qtab_off + kXcds * kTabCache * 8));
     }
+    int qd = 0;
     if (threadIdx.x == 0 && !bad) {
         Hdr* hdr = hdr_of(a.ws);
-        int qd = 0;
         if (op.phase == MOE_DECODE) {
             qd = decode_quota(a.q, xm, a.x_star, a.q_max, a.c);
-            __hip_atomic_store(&hdr->quota, qd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (act) __hip_atomic_store(&hdr->quota, qd, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         __hip_atomic_store(&d->x_moe, xm, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         // the commit counter is set before any queue can hand out a tile
@@ -993,6 +1063,10 @@ __device__ __forceinline__ void instantiate(const KArgs& a, int o, int32_t* scan
         if (bad) {
             set_status(a.status, MOE_ERR_CAPACITY);
             st_release_agent(&hdr_of(a.ws)->stop, 1);
+            return;
+        }
+        if (!act) {
+            __hip_atomic_store(&d->state, built_word(xm, qd), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             return;
         }
         const unsigned long long t = wall_ticks();
@@ -1064,8 +1138,9 @@ __global__ __launch_bounds__(256, 1) void apk_kernel(const KArgs a) {
         }
         if (kind == CMD_INST) {
             const int o = __builtin_amdgcn_readfirstlane(cmd.op);
+            const bool act = __builtin_amdgcn_readfirstlane(cmd.stage) != 0;
             __syncthreads();
-            instantiate(a, o, scan, s_cnt, s_off);
+            instantiate(a, o, act, scan, s_cnt, s_off);
             __syncthreads();
             continue;
         }

@@ -182,10 +182,11 @@ def test_bounded_preemption(dev, release_us):
     """Bounded tile-level preemption, term by term from the trace: a decode op
     released while prefill tiles run is seen at the first tile boundary of a
     workgroup below q' after its release (so no later than the remaining time
-    of those workgroups' prefill tiles, plus one boundary), is instantiated
-    by that workgroup, which takes the op's first tile at its very next
-    boundary.  The epoch (one boundary's decision) is the longest boundary
-    measured in the same launch."""
+    of those workgroups' prefill tiles, plus one boundary) and activated by
+    that workgroup (its template was built ahead, so no instantiation is
+    left), which takes the op's first tile in the same boundary.  The epoch
+    (one boundary's decision) is the longest boundary measured in the same
+    launch."""
     cfg = custom_config(2, cfg_id=405, H=1024, I=1024, prefill_tokens=8192, decode_tokens=256, E_global=64,
                         E_local=16, top_k=8)
     specs, _, _ = layer_specs(cfg, 0, dev, decode=dict(release_after_ns=release_us * 1000))
@@ -209,13 +210,14 @@ def test_bounded_preemption(dev, release_us):
     seen, ready = int(st["t_seen"][1]), int(st["t_ready"][1])
     first = int(tr[tr["op"] == 1]["t_start"].min())
     us = lambda t: t * TICK_NS / 1000.0  # noqa: E731
-    print(f"release {release_us} us: seen +{us(seen - R):.1f} us (bound {us(min(rem) + epoch):.1f}), instantiated "
+    print(f"release {release_us} us: seen +{us(seen - R):.1f} us (bound {us(min(rem) + epoch):.1f}), activated "
           f"in {us(ready - seen):.1f} us, first tile +{us(first - ready):.1f} us after (epoch {us(epoch):.1f}); "
           f"wait {us(first - R):.1f} us, longest prefill tile {us(int((pre['t_end'] - pre['t_start']).max())):.1f} us")
     assert seen >= R
     assert seen - R <= min(rem) + epoch
+    assert ready == seen
     assert first - ready <= epoch
-    # the first decode tile ran on the workgroup that instantiated the op, or on another below q'
+    # the first decode tile ran on the workgroup that activated the op, or on another below q'
     fd = tr[(tr["op"] == 1)]
     assert fd[np.argmin(fd["t_start"])]["wg"] < q
 
@@ -236,7 +238,7 @@ def test_results_independent_of_schedule(dev):
 
 @pytest.mark.parametrize("n_ops,n_wg", [(16, 0), (16, 24), (2, 0)])
 def test_every_op_finished_when_workgroups_leave_early(dev, n_ops, n_wg):
-    """Workgroups leave as soon as every op is instantiated and every queue is
+    """Workgroups leave as soon as every op is activated and every queue is
     empty; an op whose last commit no polling workgroup saw must still be
     finished (done word, statistics) by the workgroup that committed it."""
     cfg = custom_config(2, cfg_id=402, H=256, I=256, prefill_tokens=96, decode_tokens=32, E_global=16,
@@ -338,6 +340,68 @@ def test_fused_combine_tiles_follow_gemm_and_precede_dependants(dev):
         dep = specs[o].depends_on_op
         if dep >= 0:
             assert m["t_claim"].min() >= int(st["t_done"][dep])
+
+
+@pytest.mark.parametrize("fused_combine", [False, True])
+def test_templates_built_ahead_then_activated(dev, fused_combine):
+    """Ops whose inputs are in place at the launch and that wait for a
+    dependency or a release time are built ahead and then activated by one
+    transition of their state word: seen and ready at the same tick, no
+    earlier than their release condition allows.  An op with no local rows
+    finishes at its activation (with a fused combine: after its combine
+    tiles, which write zeros) and releases its dependant; an op with a
+    release word is instantiated after its release, as before.  Outputs are
+    bitwise those of the same ops all ready at the launch."""
+    cfg = custom_config(2, cfg_id=732, H=512, I=512, prefill_tokens=1024, decode_tokens=96, E_global=64,
+                        E_local=12, top_k=4, zipf_s=(1.1,), n_layers=3)
+    word = torch.ones(1, dtype=torch.int32, device=dev)
+
+    def build(chained):
+        specs = []
+        for layer in range(3):
+            ready = {"prefill": {}, "decode": {}}
+            if chained:
+                ready["prefill"] = dict(depends_on_op=-1 if layer == 0 else 2 * (layer - 1))
+                ready["decode"] = (dict(release_after_ns=15_000) if layer == 0 else
+                                   dict(depends_on_op=2 * layer - 1, gap_ns=10_000))
+                if layer == 2:
+                    ready["decode"]["release_word"] = word
+            s, _, _ = layer_specs(cfg, layer, dev, **ready)
+            specs += s
+        # layer 1's decode op routes no token to a local expert: no row tiles
+        lg = specs[3].logits.clone()
+        lg[:, cfg.local_begin:cfg.local_begin + cfg.E_local] = -50.0
+        specs[3].logits = lg
+        from paper_2607_18002_amd.pipeline import MoEPipeline
+        p = MoEPipeline(specs, fused_gather=True, fused_combine=fused_combine, trace_capacity=1 << 16)
+        p.run()
+        torch.cuda.synchronize()
+        assert p.statuses() == (0, 0)
+        return specs, p
+
+    base_specs, base = build(False)
+    specs, pipe = build(True)
+    st = pipe.op_stats()
+    t0 = pipe.kernel_t0()
+    assert st["x_moe"][3] == 0 and st["x_moe"][1] > 0
+    for o, sp in enumerate(specs):
+        assert int(pipe.bufs[o].done_word.item()) == 1, o
+        seen, ready = int(st["t_seen"][o]), int(st["t_ready"][o])
+        if o == 0:
+            continue                                          # ready at the launch: instantiated
+        if sp.release_word is not None:
+            assert ready > seen, o                            # built only after its release
+        else:
+            assert ready == seen, o                           # built ahead, activated in one transition
+        if sp.release_after_ns >= 0:
+            assert ready >= t0 + int(sp.release_after_ns / TICK_NS), o
+        if sp.depends_on_op >= 0:
+            assert ready >= int(st["t_done"][sp.depends_on_op]) + int(sp.gap_ns / TICK_NS), o
+        assert int(st["t_done"][o]) >= ready, o
+    if not fused_combine:                                       # (with a fused combine its tiles write zeros)
+        assert int(st["t_done"][3]) - int(st["t_ready"][3]) < 2000  # the empty op finished at its activation
+    for b0, b1 in zip(base.bufs, pipe.bufs):
+        np.testing.assert_array_equal(b1.y.view(torch.int16).cpu().numpy(), b0.y.view(torch.int16).cpu().numpy())
 
 
 # Queue words of the scheduler workspace: a 256-byte header, 16 op states and
