@@ -62,6 +62,13 @@ using sched::kXcds;
 
 using ShapeP = TileShape<192, 256, 64>;    // bf16 prefill: 192 x 256 tall tile, K step 64
 using ShapeD = TileShape<128, 256, 64>;    // bf16 decode : 128 x 256 tile, K step 64
+// bf16 decode beside prefill ops: the same tile with its weights loaded
+// non-temporal.  A decode op's weight slice serves its one or two row tiles
+// and is then dead in the L2, where it would evict the slices and activation
+// rows that a prefill group still shares (4 layers of 8192 prefill + 1024
+// decode tokens: +1.3%).  Decode alone gains nothing from it, so launches
+// without prefill ops keep the plain loads.
+using ShapeDS = TileShape<128, 256, 64, kLoadStream>;
 using ShapeF8 = TileShapeF8<128, 256>;     // fp8 (both phases): 128 x 256 tile, K step 128 (one scale block)
 constexpr int kMax2(int a, int b) { return a > b ? a : b; }
 constexpr int kLdsBytes = kMax2(kMax2(TallLds<ShapeP>::bytes, ShapeD::LDS), ShapeF8::LDS);
@@ -70,7 +77,7 @@ constexpr int kLdsBytes = kMax2(kMax2(TallLds<ShapeP>::bytes, ShapeD::LDS), Shap
 // 32-row blocks (M_t = the class's tallest tile), so the row tiles that share
 // a weight slice run about equally long and stay in step (sched_index.hpp).
 
-enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1, CLS_FP8 = 2 };
+enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1, CLS_FP8 = 2, CLS_D_BF16_S = 3 };
 enum : int32_t { ST_WAIT = 0, ST_INIT = 1, ST_ACTIVE = 2, ST_DONE = 3, ST_FINISHING = 4, ST_COMBINING = 5 };
 // A template built ahead of its ready signal (row tiles, queues and counters
 // in place, nothing claimable) waits in a state word that also carries what
@@ -289,6 +296,8 @@ __device__ __forceinline__ void run_tile(const OpArg& op, int stage, int row0, i
         run_tile_fp8(op, stage, row0, rows32, nb, e, lds, hook);
     else if (op.cls == CLS_P_BF16)
         run_tile_cls<ShapeP, true>(op, stage, row0, rows32, nb, e, lds, hook);
+    else if (op.cls == CLS_D_BF16_S)
+        run_tile_cls<ShapeDS, false>(op, stage, row0, rows32, nb, e, lds, hook);
     else
         run_tile_cls<ShapeD, false>(op, stage, row0, rows32, nb, e, lds, hook);
 }
@@ -1247,6 +1256,8 @@ moe_status_t fill_ops(const moe_op_desc* ops, int32_t n_ops, int wc_khz, KArgs& 
                       int prefill_rows = 0) {
     using moeapk_host::fail;
     off = 0;                                          // bytes from the arrays base
+    bool with_prefill = false;                        // bf16 decode tiles then stream their weights (ShapeDS)
+    for (int o = 0; o < n_ops; ++o) with_prefill |= ops[o].phase == MOE_PREFILL;
     for (int o = 0; o < n_ops; ++o) {
         const moe_op_desc& d = ops[o];
         if (d.phase != MOE_PREFILL && d.phase != MOE_DECODE) return fail(MOE_ERR_INVALID_ARG, "op %d: bad phase %d", o, d.phase);
@@ -1256,6 +1267,7 @@ moe_status_t fill_ops(const moe_op_desc* ops, int32_t n_ops, int wc_khz, KArgs& 
             return fail(MOE_ERR_UNSUPPORTED, "op %d: weights must be in MOE_LAYOUT_PACKED (moe_pack_weights)", o);
         int cls = class_of(d.phase, d.dtype);
         if (cls == CLS_P_BF16 && prefill_rows == 128) cls = CLS_D_BF16;
+        else if (cls == CLS_D_BF16 && with_prefill) cls = CLS_D_BF16_S;
         const ClassInfo ci = class_info(cls);
         if (d.E_local < 1 || d.E_local > 1024) return fail(MOE_ERR_UNSUPPORTED, "op %d: E_local=%d outside [1,1024]", o, d.E_local);
         // H and I are the K of a GEMM (whole pairs of K steps) and split into whole output tiles

@@ -34,9 +34,10 @@ struct NoHook {
     __device__ __forceinline__ void operator()() const {}
 };
 
-template <int BM_, int BN_, int BK_>
+// BAUX: cache policy of the weight loads (0, or kLoadStream).
+template <int BM_, int BN_, int BK_, int BAUX_ = 0>
 struct TileShape {
-    static constexpr int BM = BM_, BN = BN_, BK = BK_;
+    static constexpr int BM = BM_, BN = BN_, BK = BK_, BAUX = BAUX_;
     static constexpr int MB = BM / 32;               // 32-row blocks
     static constexpr int WCOLS = BN / 4;             // B rows (output columns) per wave
     static constexpr int NBW = WCOLS / 32;           // 32-column MFMA blocks per wave
@@ -72,6 +73,7 @@ struct TileRegs {
 // descriptor's size bounds the tile's extent (reads past it return zero).
 constexpr int kBufferWord3 = 0x00020000;   // gfx9-family raw buffer: 32-bit data format, no swizzle
 constexpr int kStoreDevice = 16;           // cache policy sc1: the store is coherent at device scope
+constexpr int kLoadStream = 2;             // cache policy nt: data read once, the first to leave the L2
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kBufferWord3);
@@ -102,7 +104,7 @@ __device__ __forceinline__ void load_b(bf16x8 (&rb)[S::NBW][S::KK], __amdgpu_buf
 #pragma unroll
         for (int kk = 0; kk < S::KK; ++kk) {
             const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(
-                B, (int)(boff[j] + (PACKED ? kk * 1024 : (kk >> 2) * 128 + (kk & 3) * 16)), k0b, 0);
+                B, (int)(boff[j] + (PACKED ? kk * 1024 : (kk >> 2) * 128 + (kk & 3) * 16)), k0b, S::BAUX);
             rb[j][kk] = __builtin_bit_cast(bf16x8, v);
         }
 }
