@@ -70,6 +70,7 @@ using ShapeD = TileShape<128, 256, 64>;    // bf16 decode : 128 x 256 tile, K st
 // without prefill ops keep the plain loads.
 using ShapeDS = TileShape<128, 256, 64, kLoadStream>;
 using ShapeF8 = TileShapeF8<128, 256>;     // fp8 (both phases): 128 x 256 tile, K step 128 (one scale block)
+using ShapeF8S = TileShapeF8<128, 256, kLoadStream>;   // fp8 decode beside prefill ops (as ShapeDS)
 constexpr int kMax2(int a, int b) { return a > b ? a : b; }
 constexpr int kLdsBytes = kMax2(kMax2(TallLds<ShapeP>::bytes, ShapeD::LDS), ShapeF8::LDS);
 // Expert segments are aligned to 32 rows (one MFMA row block).  An expert's m
@@ -77,7 +78,8 @@ constexpr int kLdsBytes = kMax2(kMax2(TallLds<ShapeP>::bytes, ShapeD::LDS), Shap
 // 32-row blocks (M_t = the class's tallest tile), so the row tiles that share
 // a weight slice run about equally long and stay in step (sched_index.hpp).
 
-enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1, CLS_FP8 = 2, CLS_D_BF16_S = 3 };
+enum : int32_t { CLS_P_BF16 = 0, CLS_D_BF16 = 1, CLS_FP8 = 2, CLS_D_BF16_S = 3, CLS_FP8_S = 4 };
+__host__ __device__ __forceinline__ bool is_fp8_cls(int cls) { return cls == CLS_FP8 || cls == CLS_FP8_S; }
 enum : int32_t { ST_WAIT = 0, ST_INIT = 1, ST_ACTIVE = 2, ST_DONE = 3, ST_FINISHING = 4, ST_COMBINING = 5 };
 // A template built ahead of its ready signal (row tiles, queues and counters
 // in place, nothing claimable) waits in a state word that also carries what
@@ -91,7 +93,7 @@ enum : int32_t { CMD_EXIT = 0, CMD_TILE = 1, CMD_INST = 2, CMD_IDLE = 3 };
 struct OpArg {
     const int32_t* counts;
     const int32_t* offsets;
-    const uint16_t* x;         // bf16 elements, or fp8 codes (bytes) for CLS_FP8: x_perm, or x when gathered
+    const uint16_t* x;         // bf16 elements, or fp8 codes (bytes) for the fp8 classes: x_perm, or x when gathered
     const uint16_t* wgu;
     const uint16_t* wd;
     uint16_t* h;
@@ -265,10 +267,9 @@ __device__ __forceinline__ void run_tile_cls(const OpArg& op, int stage, int row
 }
 
 // fp8: GEMM-1 tiles cover 128 h columns (one h scale group), GEMM-2 tiles 256 y columns.
-template <class Hook>
+template <class S, class Hook>
 __device__ __forceinline__ void run_tile_fp8(const OpArg& op, int stage, int row0, int rows32, int nb, int e,
                                              char* lds, Hook hook) {
-    using S = ShapeF8;
     const long H = op.H, I = op.I;
     const uint8_t* x = (const uint8_t*)op.x;
     uint8_t* h = (uint8_t*)op.h;
@@ -293,7 +294,9 @@ template <class Hook>
 __device__ __forceinline__ void run_tile(const OpArg& op, int stage, int row0, int rows32, int nb, int e, char* lds,
                                          Hook hook) {
     if (op.cls == CLS_FP8)
-        run_tile_fp8(op, stage, row0, rows32, nb, e, lds, hook);
+        run_tile_fp8<ShapeF8>(op, stage, row0, rows32, nb, e, lds, hook);
+    else if (op.cls == CLS_FP8_S)
+        run_tile_fp8<ShapeF8S>(op, stage, row0, rows32, nb, e, lds, hook);
     else if (op.cls == CLS_P_BF16)
         run_tile_cls<ShapeP, true>(op, stage, row0, rows32, nb, e, lds, hook);
     else if (op.cls == CLS_D_BF16_S)
@@ -1191,7 +1194,7 @@ struct ClassInfo {
     int bm, bn, bk;            // tallest row tile (Eq. 3's M_t), output columns, K step
 };
 ClassInfo class_info(int cls) {
-    if (cls == CLS_FP8) return ClassInfo{ShapeF8::BM, ShapeF8::BN, ShapeF8::BK};
+    if (is_fp8_cls(cls)) return ClassInfo{ShapeF8::BM, ShapeF8::BN, ShapeF8::BK};
     return cls == CLS_P_BF16 ? ClassInfo{ShapeP::BM, ShapeP::BN, ShapeP::BK} : ClassInfo{ShapeD::BM, ShapeD::BN, ShapeD::BK};
 }
 int class_of(int phase, int dtype) {
@@ -1268,6 +1271,7 @@ moe_status_t fill_ops(const moe_op_desc* ops, int32_t n_ops, int wc_khz, KArgs& 
         int cls = class_of(d.phase, d.dtype);
         if (cls == CLS_P_BF16 && prefill_rows == 128) cls = CLS_D_BF16;
         else if (cls == CLS_D_BF16 && with_prefill) cls = CLS_D_BF16_S;
+        else if (cls == CLS_FP8 && d.phase == MOE_DECODE && with_prefill) cls = CLS_FP8_S;
         const ClassInfo ci = class_info(cls);
         if (d.E_local < 1 || d.E_local > 1024) return fail(MOE_ERR_UNSUPPORTED, "op %d: E_local=%d outside [1,1024]", o, d.E_local);
         // H and I are the K of a GEMM (whole pairs of K steps) and split into whole output tiles
@@ -1275,7 +1279,7 @@ moe_status_t fill_ops(const moe_op_desc* ops, int32_t n_ops, int wc_khz, KArgs& 
             return fail(MOE_ERR_UNSUPPORTED, "op %d: H=%d must be a positive multiple of 256", o, d.H);
         if (d.I < ci.bn / 2 || d.I % (ci.bn / 2) != 0 || d.I % (2 * ci.bk) != 0 || d.I % 256 != 0)
             return fail(MOE_ERR_UNSUPPORTED, "op %d: I=%d must be a positive multiple of 256", o, d.I);
-        if (cls == CLS_FP8) {
+        if (is_fp8_cls(cls)) {
             if (d.H > 128 * ShapeF8::MAX_KB || d.I > 128 * ShapeF8::MAX_KB)
                 return fail(MOE_ERR_UNSUPPORTED, "op %d: fp8 H, I must be at most %d", o, 128 * ShapeF8::MAX_KB);
             if (!(d.x ? d.x_scales : d.x_perm_scales) || !d.w_gate_up_scales || !d.w_down_scales || !d.h_scales)
@@ -1297,7 +1301,7 @@ moe_status_t fill_ops(const moe_op_desc* ops, int32_t n_ops, int wc_khz, KArgs& 
         if (d.x) {
             if (!d.row_to_assign || d.T < 1 || d.top_k < 1)
                 return fail(MOE_ERR_INVALID_ARG, "op %d: gathered operand needs row_to_assign, T >= 1, top_k >= 1", o);
-            if ((int64_t)d.T * d.H * (cls == CLS_FP8 ? 1 : 2) >= ((int64_t)1 << 31))
+            if ((int64_t)d.T * d.H * (is_fp8_cls(cls) ? 1 : 2) >= ((int64_t)1 << 31))
                 return fail(MOE_ERR_UNSUPPORTED, "op %d: T*H of the gathered operand exceeds 2^31 bytes", o);
         }
         if (d.y) {                                    // fused combine

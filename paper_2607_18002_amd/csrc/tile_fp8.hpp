@@ -32,9 +32,10 @@
 
 namespace moeapk {
 
-template <int BM_, int BN_>
+// BAUX: cache policy of the weight loads (0, or kLoadStream).
+template <int BM_, int BN_, int BAUX_ = 0>
 struct TileShapeF8 {
-    static constexpr int BM = BM_, BN = BN_, BK = 128;
+    static constexpr int BM = BM_, BN = BN_, BK = 128, BAUX = BAUX_;
     static constexpr int MB = BM / 32;                // 32-token blocks
     static constexpr int WCOLS = BN / 4;              // features per wave
     static constexpr int NBW = WCOLS / 32;            // 32-feature blocks per wave
@@ -82,8 +83,8 @@ __device__ __forceinline__ void load_w8(i32x8 (&rw)[S::NBW][S::KK], __amdgpu_buf
     for (int j = 0; j < S::NBW; ++j)
 #pragma unroll
         for (int kk = 0; kk < S::KK; ++kk) {
-            const u32x4 lo = __builtin_amdgcn_raw_buffer_load_b128(B, (int)(boff[j] + kk * 2048), k0b, 0);
-            const u32x4 hi = __builtin_amdgcn_raw_buffer_load_b128(B, (int)(boff[j] + kk * 2048 + 1024), k0b, 0);
+            const u32x4 lo = __builtin_amdgcn_raw_buffer_load_b128(B, (int)(boff[j] + kk * 2048), k0b, S::BAUX);
+            const u32x4 hi = __builtin_amdgcn_raw_buffer_load_b128(B, (int)(boff[j] + kk * 2048 + 1024), k0b, S::BAUX);
             rw[j][kk] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
         }
 }
