@@ -74,6 +74,9 @@ struct TileRegs {
 constexpr int kBufferWord3 = 0x00020000;   // gfx9-family raw buffer: 32-bit data format, no swizzle
 constexpr int kStoreDevice = 16;           // cache policy sc1: the store is coherent at device scope
 constexpr int kLoadStream = 2;             // cache policy nt: data read once, the first to leave the L2
+// sc1 + nt: GEMM-2 outputs (y_perm rows), read only by the combine, so they
+// need not displace weight slices and activation rows from the L2
+constexpr int kStoreDeviceStream = kStoreDevice | kLoadStream;
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kBufferWord3);
@@ -279,7 +282,7 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
     for (int p = 0; p < MACT * 32 / RPI; ++p) {
         const u32x4 v = *(const u32x4_alias*)(stg + (p * RPI + orow) * ORB + och * 16);
         __builtin_amdgcn_raw_buffer_store_b128(v, Ob, (int)ooff, (int)((uint32_t)(p * RPI) * (uint32_t)ldo * 2u),
-                                               kStoreDevice);
+                                               GLU ? kStoreDevice : kStoreDeviceStream);
     }
 }
 

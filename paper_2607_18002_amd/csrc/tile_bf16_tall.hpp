@@ -193,7 +193,8 @@ __device__ __forceinline__ void gemm_tile_tall(const uint16_t* __restrict__ A, i
             if (p * RPI >= nb_h * 32) break;
             const u32x4 v = *(const u32x4_alias*)(stg + (p * RPI + orow) * ORB + och * 16);
             __builtin_amdgcn_raw_buffer_store_b128(
-                v, Ob, (int)ooff, (int)((uint32_t)(i0 * 32 + p * RPI) * (uint32_t)ldo * 2u), kStoreDevice);
+                v, Ob, (int)ooff, (int)((uint32_t)(i0 * 32 + p * RPI) * (uint32_t)ldo * 2u),
+                GLU ? kStoreDevice : kStoreDeviceStream);
         }
         // A 16-byte store reads its data registers after it issues: two wait
         // states must pass before a VALU instruction overwrites them.  The next

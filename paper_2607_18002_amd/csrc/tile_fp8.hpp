@@ -300,7 +300,7 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
         for (int p = 0; p < MACT * 32 / RPI; ++p) {
             const u32x4 v = *(const u32x4_alias*)(stg + (p * RPI + orow) * S::OUT_ROW + och * 16);
             __builtin_amdgcn_raw_buffer_store_b128(v, Ob, (int)ooff, (int)((uint32_t)(p * RPI) * (uint32_t)ldo * 2u),
-                                                   kStoreDevice);
+                                                   kStoreDeviceStream);
         }
     }
 }
