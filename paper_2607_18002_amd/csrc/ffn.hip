@@ -766,10 +766,14 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
     //    for one tile boundary of those workgroups plus its instantiation.
     //    A template built ahead (4b) needs no instantiation: the same
     //    workgroups activate it and claim its first tile in the same boundary.
+    //    The release condition is also read by a workgroup that may build a
+    //    template ahead (4b), so that one already released is left to the
+    //    workgroups that instantiate it at once.
     bool ready = false;
     const bool built = is_built(state);
     const bool may_inst = phase == MOE_PREFILL || a.inst_wg == 0 || wg < a.inst_wg;
-    if ((state == ST_WAIT || built) && may_inst) {
+    const bool may_build = wg >= a.pre_wg && state == ST_WAIT && sta[o_l].rel_word == nullptr;
+    if ((state == ST_WAIT || built) && (may_inst || may_build)) {
         ready = true;
         const uint32_t* rw = sta[o_l].rel_word;
         if (rw) ready = __hip_atomic_load(rw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != 0u;
@@ -780,6 +784,8 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
                     now >= ld_relaxed_agent(&dyn[dep].t_done) + (uint64_t)sta[o_l].gap;
         }
     }
+    const bool released = ready;                          // (read where may_inst or may_build)
+    ready = ready && may_inst;
     // 4a. activation of a built template: one transition of its state word.
     //     Its queue words and table entries reached the coherence point before
     //     the word turned BUILT, so every claim that follows the transition
@@ -835,7 +841,7 @@ __device__ __forceinline__ void boundary(const KArgs& a, uint64_t t0, int wg, Cm
     //     release word) is built before its ready signal, by a workgroup that
     //     never prefers decode, and waits BUILT.
     if (wg >= a.pre_wg) {
-        const uint64_t bmask = __ballot(state == ST_WAIT && !ready && sta[o_l].rel_word == nullptr);
+        const uint64_t bmask = __ballot(may_build && !released);
         if (bmask) {
             const int o = __ffsll((long long)bmask) - 1;
             int won = 0;
