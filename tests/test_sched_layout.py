@@ -111,8 +111,8 @@ def test_masked_offsets_and_edge_cases():
     _check(np.zeros(7, np.int64), np.arange(7) * 32, 128, 8, 2, 2)
     big = np.full(40, 2000)
     _check(big, _contiguous_offsets(big), 32, 64, 2, 2)     # 2500 row tiles, queues of ~300 > cache
-    cfg4_like = np.array([3034] + [480] * 31)
-    _check(cfg4_like, _contiguous_offsets(cfg4_like), 192, 8, 12, 12)
+    hot_expert = np.array([3034] + [480] * 31)
+    _check(hot_expert, _contiguous_offsets(hot_expert), 192, 8, 12, 12)
 
 
 def test_claims_resolve_the_same_on_every_xcd():
