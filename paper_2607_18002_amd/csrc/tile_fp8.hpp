@@ -48,7 +48,12 @@ struct TileShapeF8 {
     static constexpr int H_ROW = (BN / 2) * 4 + 16;   // GLU epilogue: fp32 h row of BN/2 features
     static constexpr int OUT_ROW = WCOLS * 2 + 16;    // GEMM-2 epilogue: per-wave bf16 row
     static constexpr int EPI = BM * H_ROW > 4 * BM * OUT_ROW ? BM * H_ROW : 4 * BM * OUT_ROW;
-    static constexpr int LDS = SX_OFF + SX_BYTES > EPI ? SX_OFF + SX_BYTES : EPI;
+    // weight scales of each wave's feature blocks, [wave][j][kb] (f32): read
+    // from LDS in the K loop, since a global load there would be the youngest
+    // in flight and waiting for it would drain the weight prefetch as well
+    static constexpr int SW_OFF = SX_OFF + SX_BYTES;
+    static constexpr int SW_BYTES = 4 * NBW * MAX_KB * 4;
+    static constexpr int LDS = SW_OFF + SW_BYTES > EPI ? SW_OFF + SW_BYTES : EPI;
     static constexpr int CPR = BK / 16;               // 16-byte chunks per activation row and step
     static constexpr int RPP = 256 / CPR;             // activation rows per load pass
     static_assert(NBW == 2, "GLU pairs one gate and one up block per wave");
@@ -139,7 +144,13 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
     char* lds1 = lds + S::A_STAGE;
     float* sx = (float*)(lds + S::SX_OFF);
 
-    // activation scales of the tile, transposed to [kb][token]
+    // this wave's weight scale rows, then the tile's activation scales
+    // transposed to [kb][token]
+    float* swl = (float*)(lds + S::SW_OFF) + wn * (S::NBW * S::MAX_KB);
+    for (int idx = lane; idx < S::NBW * nkb; idx += 64) {
+        const int j = idx / nkb, kb = idx - j * nkb;
+        swl[j * S::MAX_KB + kb] = sw[j][kb];
+    }
     for (int idx = tid; idx < MACT * 32 * nkb; idx += 256) {
         const int r = idx / nkb, kb = idx - r * nkb;
         int src = r;
@@ -166,12 +177,18 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
     // Branch-free K loop (K/128 is a multiple of D): loads are clamped to the
     // last step instead of skipped, so the compiler's wait counts stay exact
     // and a step's waits leave the later steps' weight loads in flight.
+    // In every step the next step's A loads are issued before this step's
+    // weight loads, so waiting for A leaves those weights in flight; the
+    // prologue keeps that order too (the last weight step after A of step 1),
+    // since the loop's wait counts hold for its entry as well.
     const int last = nkb - 1;
-    load_a<CA>(ra, Ab, aoff, 0);
 #pragma unroll
-    for (int d = 0; d < D; ++d) load_w8<S>(rw[d], Bb, boff, d * KBW);
+    for (int d = 0; d + 1 < D; ++d) load_w8<S>(rw[d], Bb, boff, d * KBW);
+    load_a<CA>(ra, Ab, aoff, 0);
     store_a<CA>(lds0, ra, alds);
     load_a<CA>(ra, Ab, aoff, (1 < last ? 1 : last) * S::BK);
+    __builtin_amdgcn_sched_barrier(0);                 // keep the issue order
+    load_w8<S>(rw[D - 1], Bb, boff, (D - 1) * KBW);
     __syncthreads();
     for (int s0 = 0; s0 < nkb; s0 += D) {
 #pragma unroll
@@ -180,7 +197,7 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
             const char* cur = (d & 1) ? lds1 : lds0;
             float cw[S::NBW];
 #pragma unroll
-            for (int j = 0; j < S::NBW; ++j) cw[j] = sw[j][s];
+            for (int j = 0; j < S::NBW; ++j) cw[j] = swl[j * S::MAX_KB + s];
             const float* sxs = sx + s * S::BM + (lane & 31);
             // Row block by row block: the block's two MFMAs per feature block
             // go into a fresh partial (two partial sets alternate), and the
@@ -213,8 +230,9 @@ __device__ __forceinline__ void gemm_tile_fp8(const uint8_t* __restrict__ A, int
             }
             store_a<CA>((d & 1) ? lds0 : lds1, ra, alds);
             const int sw_ = s + D < last ? s + D : last, sa = s + 2 < last ? s + 2 : last;
-            load_w8<S>(rw[d], Bb, boff, sw_ * KBW);
             load_a<CA>(ra, Ab, aoff, sa * S::BK);
+            __builtin_amdgcn_sched_barrier(0);
+            load_w8<S>(rw[d], Bb, boff, sw_ * KBW);
             fold_block<S, MACT>(tot, part[(MACT - 1) & 1], MACT - 1, sxs[32 * (MACT - 1)], cw);
             __syncthreads();
         }
