@@ -58,12 +58,13 @@ struct TileShape {
 template <class S, int MACT>
 struct TileRegs {
     static constexpr int CA = MACT * 32 / S::RPP;    // A chunks per thread and K step
-    // K steps of B in flight.  One step of B takes NBW * KK * 4 registers; the
-    // MFMA accumulators take MACT * NBW * 16, so fewer valid rows leave room
-    // for more steps (budget: 128 registers at 4 row blocks, 256 at 1).
+    // K steps of A and B in flight (both rings have this depth).  One step of
+    // B takes NBW * KK * 4 registers and one of A CA * 4; the MFMA
+    // accumulators take MACT * NBW * 16, so fewer valid rows leave room for
+    // more steps (budget: 128 registers at 3-4 row blocks, 192 at 2, 256 at 1).
     static constexpr int B_STEP_REGS = S::NBW * S::KK * 4;
     static constexpr int B_BUDGET = MACT == 1 ? 256 : MACT == 2 ? 192 : 128;
-    static constexpr int DEPTH_RAW = B_BUDGET / B_STEP_REGS;
+    static constexpr int DEPTH_RAW = B_BUDGET / (B_STEP_REGS + CA * 4);
     static constexpr int DEPTH = DEPTH_RAW >= 8 ? 8 : DEPTH_RAW < 2 ? 2 : (DEPTH_RAW & ~1);
 };
 
@@ -203,40 +204,50 @@ __device__ __forceinline__ void gemm_tile_bf16(const uint16_t* __restrict__ A, i
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    u32x4 ra[2][CA];                                  // A of steps s+1 and s+2 (slot = step & 1)
+    u32x4 ra[D][CA];                                  // A of steps s+1 .. s+D (slot = step % D)
     bf16x8 rb[D][S::NBW][S::KK];                      // B of steps s .. s+D-1 (slot = step % D)
     const int nk = K / S::BK;                         // a multiple of D (see gemm_tile_bf16_rows)
     constexpr int KB = S::BK * 2;                     // bytes per K step of a row-major row
     constexpr int KBB = PACKED ? S::BK * 64 : KB;     // bytes per K step of a weight fragment stream
     static_assert(S::BK % 64 == 0, "K steps are whole 64-element chunks");
-    static_assert(D % 2 == 0, "the A slots (step & 1) repeat within one pass of the B ring");
+    static_assert(D % 2 == 0, "the LDS stages (step & 1) repeat within one pass of the ring");
 
     // The K loop has no branches: a step's loads are clamped to the last K
     // step instead of skipped (the spare loads are re-reads of data just
     // loaded, never consumed).  With no path-dependent loads the compiler's
-    // wait counts stay exact, so the waits for one step's operands leave the
-    // later steps' loads in flight.
-    // Prologue: A of step 0 into LDS stage 0; A of steps 1, 2 and B of steps
-    // 0 .. D-1 in flight.  A loads go before the B loads of the same step, so
-    // waiting for an A slot (vmcnt counts in issue order) leaves later B loads
-    // in flight.
+    // wait counts stay exact.
+    // vmcnt counts loads in issue order, so waiting for one load waits for
+    // every load issued before it.  A runs as far ahead as B: step s stores
+    // A of step s+1 into LDS and issues A of step s+1+D, then B of step s+D,
+    // so A of step s+1 was issued right before B of step s (which step s
+    // needs anyway) and waiting for it leaves B of steps s+1 .. s+D-1 in
+    // flight.  (With A loaded two steps ahead and issued after B, that wait
+    // also drained every B load older than two steps: the ring held about
+    // two steps, whatever its depth.)  The prologue issues the same pairs.
     const int last = nk - 1;
     load_a<CA>(ra[0], Ab, aoff, 0);
 #pragma unroll
-    for (int d = 0; d < D; ++d) load_b<S, PACKED>(rb[d], Bb, boff, d * KBB);
+    for (int y = 0; y + 1 < D; ++y) {
+        load_a<CA>(ra[y + 1], Ab, aoff, (y + 1 < last ? y + 1 : last) * KB);
+        __builtin_amdgcn_sched_barrier(0);
+        load_b<S, PACKED>(rb[y], Bb, boff, y * KBB);
+        __builtin_amdgcn_sched_barrier(0);
+    }
     store_a<CA>(lds0, ra[0], alds);
-    load_a<CA>(ra[1], Ab, aoff, (1 < last ? 1 : last) * KB);
-    load_a<CA>(ra[0], Ab, aoff, (2 < last ? 2 : last) * KB);
+    load_a<CA>(ra[0], Ab, aoff, (D < last ? D : last) * KB);
+    __builtin_amdgcn_sched_barrier(0);
+    load_b<S, PACKED>(rb[D - 1], Bb, boff, (D - 1) * KBB);
     __syncthreads();
     for (int s0 = 0; s0 < nk; s0 += D) {
 #pragma unroll
         for (int d = 0; d < D; ++d) {
-            const int s = s0 + d;                     // uniform; d, s & 1 and s % D are compile-time
+            const int s = s0 + d;                     // uniform; d and s & 1 are compile-time
             mma_step<S, MACT>(acc, rb[d], (d & 1) ? lds1 : lds0, lane);
-            store_a<CA>((d & 1) ? lds0 : lds1, ra[(d + 1) & 1], alds);
-            const int sb = s + D < last ? s + D : last, sa = s + 3 < last ? s + 3 : last;
+            store_a<CA>((d & 1) ? lds0 : lds1, ra[(d + 1) % D], alds);
+            const int sb = s + D < last ? s + D : last, sa = s + 1 + D < last ? s + 1 + D : last;
+            load_a<CA>(ra[(d + 1) % D], Ab, aoff, sa * KB);
+            __builtin_amdgcn_sched_barrier(0);
             load_b<S, PACKED>(rb[d], Bb, boff, sb * KBB);
-            load_a<CA>(ra[(d + 1) & 1], Ab, aoff, sa * KB);
             __syncthreads();
         }
     }
